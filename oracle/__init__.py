@@ -1,0 +1,280 @@
+"""CPU oracle of the GPU query path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It shares no code with the GPU library
+(``paper_2608_23553_amd``); both consume the seeded inputs from ``synth``.
+
+All arithmetic is exact int64 on grid integers (``oracle.h`` explains the
+convention); this module only marshals numpy arrays into ``liboracle.so``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+KEY_SCALE = 2.0 ** -22  # one key unit
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is not built; run __graft_entry__.build() (make -C oracle)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "orc_grid_k": ([ctypes.c_double], I32),
+        "orc_grid_f32": ([P, I64, P], None),
+        "orc_grid_bf16": ([P, I64, P], None),
+        "orc_assign": ([P, I64, P, I32, I32, P, ctypes.c_int], None),
+        "orc_ivf_docs": ([P, P, I64, I32, P, P], I64),
+        "orc_residual_hist": ([P, P, I64, P, I32, P], None),
+        "orc_quantizer": ([P, ctypes.c_int, P, P], ctypes.c_int),
+        "orc_encode": ([P, P, I64, P, I32, P, ctypes.c_int, P], None),
+        "orc_pack": ([P, I64, I32, ctypes.c_int, P], None),
+        "orc_unpack": ([P, I64, I32, ctypes.c_int, P], None),
+        "orc_centroid_scores": ([P, I32, P, I32, I32, P], None),
+        "orc_probe": ([P, I32, I32, I32, P, P], None),
+        "orc_candidates": ([P, I32, I32, P, P, I64, P], I64),
+        "orc_partial_scores": ([P, P, I32, I32, I32, P, P, I64, P, P], I64),
+        "orc_topk": ([P, P, I64, I64, P, P], I64),
+        "orc_doc_scores": ([P, I32, I32, P, I32, P, I64, P, P, P, P, P], None),
+        "orc_key_to_score": ([I64], ctypes.c_float),
+        "orc_exact_chamfer": ([P, I32, I32, P, P, I64, P], None),
+        "orc_search": ([P, I32, I32, P, I64, P, P, P, P, P, P, I64, I32, I32, I32, I32,
+                        P, P, P, P, P, P, P, P, ctypes.c_int], ctypes.c_int),
+        "orc_prune_batch": ([P, I32, I32, I64, P, P, P, I64, I32, I32, I32, P, P, P, P, P, P,
+                             ctypes.c_int], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def _p(a):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle inputs must be C-contiguous"
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+# ------------------------------------------------------------------ grid
+def grid_k(x: float) -> int:
+    return int(_load().orc_grid_k(float(x)))
+
+
+def grid_f32(x) -> np.ndarray:
+    x = _c(x, np.float32)
+    out = np.empty(x.shape, dtype=np.int16)
+    _load().orc_grid_f32(_p(x), x.size, _p(out))
+    return out
+
+
+def grid_bf16(bits) -> np.ndarray:
+    bits = _c(bits, np.uint16)
+    out = np.empty(bits.shape, dtype=np.int16)
+    _load().orc_grid_bf16(_p(bits), bits.size, _p(out))
+    return out
+
+
+# ------------------------------------------------------- index building
+def assign(tok_k, cent_k, nthreads: int = 0) -> np.ndarray:
+    tok_k, cent_k = _c(tok_k, np.int16), _c(cent_k, np.int16)
+    out = np.empty(tok_k.shape[0], dtype=np.int32)
+    _load().orc_assign(_p(tok_k), tok_k.shape[0], _p(cent_k), cent_k.shape[0], cent_k.shape[1], _p(out), nthreads)
+    return out
+
+
+def ivf_docs(cid, doc_off, ncent: int):
+    cid, doc_off = _c(cid, np.int32), _c(doc_off, np.int64)
+    ndocs = doc_off.shape[0] - 1
+    off = np.empty(ncent + 1, dtype=np.int64)
+    nnz = _load().orc_ivf_docs(_p(cid), _p(doc_off), ndocs, ncent, _p(off), None)
+    docs = np.empty(max(nnz, 1), dtype=np.int32)
+    _load().orc_ivf_docs(_p(cid), _p(doc_off), ndocs, ncent, _p(off), _p(docs))
+    return off, docs[:nnz]
+
+
+def residual_hist(tok_k, cid, cent_k, hist=None) -> np.ndarray:
+    tok_k, cid, cent_k = _c(tok_k, np.int16), _c(cid, np.int32), _c(cent_k, np.int16)
+    if hist is None:
+        hist = np.zeros(8193, dtype=np.int64)
+    _load().orc_residual_hist(_p(tok_k), _p(cid), cid.shape[0], _p(cent_k), cent_k.shape[1], _p(hist))
+    return hist
+
+
+def quantizer(hist, nbits: int):
+    hist = _c(hist, np.int64)
+    B = 1 << nbits
+    cut = np.empty(B - 1, dtype=np.int32)
+    w = np.empty(B, dtype=np.int32)
+    if _load().orc_quantizer(_p(hist), nbits, _p(cut), _p(w)) != 0:
+        raise ValueError("empty residual histogram")
+    return cut, w
+
+
+def encode(tok_k, cid, cent_k, cut_k, nbits: int) -> np.ndarray:
+    tok_k, cid, cent_k, cut_k = _c(tok_k, np.int16), _c(cid, np.int32), _c(cent_k, np.int16), _c(cut_k, np.int32)
+    out = np.empty(tok_k.shape, dtype=np.uint8)
+    _load().orc_encode(_p(tok_k), _p(cid), cid.shape[0], _p(cent_k), cent_k.shape[1], _p(cut_k), nbits, _p(out))
+    return out
+
+
+def pack(codes, nbits: int) -> np.ndarray:
+    codes = _c(codes, np.uint8)
+    ntok, dim = codes.shape
+    out = np.empty((ntok, dim * nbits // 8), dtype=np.uint8)
+    _load().orc_pack(_p(codes), ntok, dim, nbits, _p(out))
+    return out
+
+
+def unpack(packed, dim: int, nbits: int) -> np.ndarray:
+    packed = _c(packed, np.uint8)
+    ntok = packed.shape[0]
+    out = np.empty((ntok, dim), dtype=np.uint8)
+    _load().orc_unpack(_p(packed), ntok, dim, nbits, _p(out))
+    return out
+
+
+# ----------------------------------------------------------- query path
+def centroid_scores(q_k, cent_k) -> np.ndarray:
+    q_k, cent_k = _c(q_k, np.int16), _c(cent_k, np.int16)
+    Tq, dim = q_k.shape
+    S = np.empty((Tq, cent_k.shape[0]), dtype=np.int64)
+    _load().orc_centroid_scores(_p(q_k), Tq, _p(cent_k), cent_k.shape[0], dim, _p(S))
+    return S
+
+
+def probe(S, nprobe: int):
+    S = _c(S, np.int64)
+    Tq, ncent = S.shape
+    ids = np.empty((Tq, nprobe), dtype=np.int32)
+    keys = np.empty((Tq, nprobe), dtype=np.int64)
+    _load().orc_probe(_p(S), Tq, ncent, nprobe, _p(ids), _p(keys))
+    return ids, keys
+
+
+def candidates(cent_ids, ivf_off, ivf_doc, ndocs: int) -> np.ndarray:
+    cent_ids = _c(cent_ids, np.int32)
+    Tq, nprobe = cent_ids.shape
+    out = np.empty(max(ndocs, 1), dtype=np.int32)
+    n = _load().orc_candidates(_p(cent_ids), Tq, nprobe, _p(_c(ivf_off, np.int64)), _p(_c(ivf_doc, np.int32)),
+                               ndocs, _p(out))
+    return out[:n].copy()
+
+
+def partial_scores(S, cent_ids, ivf_off, ivf_doc, ndocs: int):
+    S, cent_ids = _c(S, np.int64), _c(cent_ids, np.int32)
+    Tq, ncent = S.shape
+    nprobe = cent_ids.shape[1]
+    docs = np.empty(max(ndocs, 1), dtype=np.int32)
+    fp = np.empty(max(ndocs, 1), dtype=np.int64)
+    n = _load().orc_partial_scores(_p(S), _p(cent_ids), Tq, ncent, nprobe, _p(_c(ivf_off, np.int64)),
+                                   _p(_c(ivf_doc, np.int32)), ndocs, _p(docs), _p(fp))
+    return docs[:n].copy(), fp[:n].copy()
+
+
+def topk(ids, keys, k: int):
+    ids, keys = _c(ids, np.int32), _c(keys, np.int64)
+    n = ids.shape[0]
+    oi = np.empty(max(min(k, n), 1), dtype=np.int32)
+    ok = np.empty(max(min(k, n), 1), dtype=np.int64)
+    m = _load().orc_topk(_p(ids), _p(keys), n, k, _p(oi), _p(ok))
+    return oi[:m].copy(), ok[:m].copy()
+
+
+def doc_scores(S, q_k, w_k, tok_begin, tok_len, cid, codes) -> np.ndarray:
+    S, q_k, w_k = _c(S, np.int64), _c(q_k, np.int16), _c(w_k, np.int32)
+    tok_begin, tok_len = _c(tok_begin, np.int64), _c(tok_len, np.int32)
+    cid, codes = _c(cid, np.int32), _c(codes, np.uint8)
+    Tq, ncent = S.shape
+    n = tok_begin.shape[0]
+    out = np.empty(max(n, 1), dtype=np.int64)
+    _load().orc_doc_scores(_p(S), Tq, ncent, _p(q_k), q_k.shape[1], _p(w_k), n, _p(tok_begin), _p(tok_len),
+                           _p(cid), _p(codes), _p(out))
+    return out[:n].copy()
+
+
+def key_to_score(key: int) -> float:
+    return float(_load().orc_key_to_score(int(key)))
+
+
+def keys_to_scores(keys) -> np.ndarray:
+    """Vector form of the key -> fp32 score rule (single rounding, then 2^-22)."""
+    keys = np.asarray(keys, dtype=np.int64)
+    out = np.array([key_to_score(int(x)) for x in keys.ravel()], dtype=np.float32).reshape(keys.shape)
+    out[keys == np.iinfo(np.int64).min] = -np.inf
+    return out
+
+
+def exact_chamfer(q_k, tok_k, doc_off) -> np.ndarray:
+    q_k, tok_k, doc_off = _c(q_k, np.int16), _c(tok_k, np.int16), _c(doc_off, np.int64)
+    Tq, dim = q_k.shape
+    ndocs = doc_off.shape[0] - 1
+    F = np.empty(max(ndocs, 1), dtype=np.int64)
+    _load().orc_exact_chamfer(_p(q_k), Tq, dim, _p(tok_k), _p(doc_off), ndocs, _p(F))
+    return F[:ndocs].copy()
+
+
+# ------------------------------------------------------- oracle index
+class OracleIndex:
+    """The oracle's own view of a corpus: assignment given by the corpus,
+    quantiser, codes and posting lists computed here from raw grid tokens."""
+
+    def __init__(self, cent_k, doc_off, cid, nbits: int, tok_k=None, hist=None, with_codes=True):
+        self.cent_k = _c(cent_k, np.int16)
+        self.doc_off = _c(doc_off, np.int64)
+        self.cid = _c(cid, np.int32)
+        self.nbits = nbits
+        self.ncent, self.dim = self.cent_k.shape
+        self.ndocs = self.doc_off.shape[0] - 1
+        if hist is None:
+            hist = residual_hist(tok_k, self.cid, self.cent_k)
+        self.hist = hist
+        self.cut_k, self.w_k = quantizer(hist, nbits)
+        self.codes = encode(tok_k, self.cid, self.cent_k, self.cut_k, nbits) if with_codes else None
+        self.ivf_off, self.ivf_doc = ivf_docs(self.cid, self.doc_off, self.ncent)
+
+    def search(self, q_k, nprobe: int, ncand: int, k: int, nthreads: int = 0):
+        """Full path for queries q_k [nq, Tq, dim]; returns a dict of arrays."""
+        q_k = _c(q_k, np.int16)
+        nq, Tq, dim = q_k.shape
+        out = dict(
+            cent_ids=np.empty((nq, Tq, nprobe), np.int32), cent_keys=np.empty((nq, Tq, nprobe), np.int64),
+            n_sq=np.empty(nq, np.int64), cand=np.full((nq, ncand), -1, np.int32),
+            cand_keys=np.zeros((nq, ncand), np.int64), n_cand=np.empty(nq, np.int64),
+            ids=np.empty((nq, k), np.int32), keys=np.empty((nq, k), np.int64))
+        _load().orc_search(_p(self.cent_k), self.ncent, dim, _p(self.doc_off), self.ndocs, _p(self.cid),
+                           _p(self.codes), _p(self.w_k), _p(self.ivf_off), _p(self.ivf_doc), _p(q_k), nq, Tq,
+                           nprobe, ncand, k, _p(out["cent_ids"]), _p(out["cent_keys"]), _p(out["n_sq"]),
+                           _p(out["cand"]), _p(out["cand_keys"]), _p(out["n_cand"]), _p(out["ids"]),
+                           _p(out["keys"]), nthreads)
+        out["scores"] = keys_to_scores(out["keys"])
+        return out
+
+    def prune(self, q_k, nprobe: int, ncand: int, nthreads: int = 0):
+        q_k = _c(q_k, np.int16)
+        nq, Tq, dim = q_k.shape
+        out = dict(
+            cent_ids=np.empty((nq, Tq, nprobe), np.int32), cent_keys=np.empty((nq, Tq, nprobe), np.int64),
+            n_sq=np.empty(nq, np.int64), cand=np.full((nq, ncand), -1, np.int32),
+            cand_keys=np.zeros((nq, ncand), np.int64), n_cand=np.empty(nq, np.int64))
+        _load().orc_prune_batch(_p(self.cent_k), self.ncent, dim, self.ndocs, _p(self.ivf_off), _p(self.ivf_doc),
+                                _p(q_k), nq, Tq, nprobe, ncand, _p(out["cent_ids"]), _p(out["cent_keys"]),
+                                _p(out["n_sq"]), _p(out["cand"]), _p(out["cand_keys"]), _p(out["n_cand"]),
+                                nthreads)
+        return out

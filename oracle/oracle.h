@@ -1,0 +1,133 @@
+/*
+ * oracle.h - plain, slow CPU reference of the GPU query path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU
+ * baseline leg of the benchmark may load this library.  It shares no code,
+ * header, table or helper with the GPU library; the two meet only at the
+ * seeded input generator (synth/) and at the documented index layout.
+ *
+ * Paper: "Chimera: Efficient Multi-Vector Retrieval via GPU-CPU
+ * Co-Processing".  Every function names the passage it follows.
+ *
+ * Arithmetic.  Every vector component is on the grid G (bf16 values that
+ * are multiples of 2^-11) and is carried as the integer k = x * 2^11.  An
+ * inner product is then the exact integer sum of k_a * k_b, in units of
+ * 2^-22; every score, partial score and document score below is such an
+ * int64 "key".  No floating point is used anywhere in the search; a score
+ * leaves the oracle only through orc_key_to_score.
+ *
+ * Parity status: every function is pinned by the CPU tests (brute force,
+ * closed forms, library routines, invariants); none is "parity unpinned".
+ */
+#ifndef CHIMERA_ORACLE_H
+#define CHIMERA_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- Value grid G (the fixed-point reading of the paper's fp32 sums). ---- */
+/* Nearest grid value of x, ties to even, as k = x * 2^11. */
+int32_t orc_grid_k(double x);
+void orc_grid_f32(const float *x, int64_t n, int16_t *k_out);
+void orc_grid_bf16(const uint16_t *bits, int64_t n, int16_t *k_out);
+
+/* ---- IVF assignment (Sec. 2.3, inverted file: nearest centroid). ----
+ * cid[t] = argmax_c <v_t, c>, ties to the lowest c. */
+void orc_assign(const int16_t *tok_k, int64_t ntok, const int16_t *cent_k, int32_t ncent, int32_t dim,
+                int32_t *cid, int nthreads);
+
+/* ---- Posting lists (Sec. 2.3; Sec. 3.2 candidate generation). ----
+ * Doc-level list of centroid c: ascending distinct docs that own a token
+ * assigned to c.  Call with ivf_doc == NULL to get nnz; ivf_off is
+ * [ncent+1]. Returns nnz. */
+int64_t orc_ivf_docs(const int32_t *cid, const int64_t *doc_off, int64_t ndocs, int32_t ncent,
+                     int64_t *ivf_off, int32_t *ivf_doc);
+
+/* ---- Residual quantiser (bucketed residual codes; the paper only names
+ * residual compression among related systems, so this is the build's
+ * reading: pooled empirical quantiles). ---- */
+/* Adds the residual r = v - c_cid of every component to hist[r + 4096]
+ * (hist has 8193 int64 bins). */
+void orc_residual_hist(const int16_t *tok_k, const int32_t *cid, int64_t ntok, const int16_t *cent_k,
+                       int32_t dim, int64_t *hist);
+/* B = 2^nbits buckets: cutoffs cut_k[i-1] = Q(i/B), i = 1..B-1; weights
+ * w_k[u] = G(Q((2u+1)/(2B))), where Q(a) is the floor(a*n)-th smallest
+ * residual (0-based, clamped to n-1).  Returns 0, or -1 if hist is empty. */
+int orc_quantizer(const int64_t *hist, int nbits, int32_t *cut_k, int32_t *w_k);
+/* code[t][d] = #{i : cut_i < r_{t,d}} (a residual equal to a cutoff goes to
+ * the lower bucket). */
+void orc_encode(const int16_t *tok_k, const int32_t *cid, int64_t ntok, const int16_t *cent_k, int32_t dim,
+                const int32_t *cut_k, int nbits, uint8_t *codes);
+/* Packed layout: 2-bit puts dim 4i+s in bits [2s, 2s+1] of byte i; 4-bit puts
+ * dim 2i in the low nibble and 2i+1 in the high nibble of byte i. */
+void orc_pack(const uint8_t *codes, int64_t ntok, int32_t dim, int nbits, uint8_t *packed);
+void orc_unpack(const uint8_t *packed, int64_t ntok, int32_t dim, int nbits, uint8_t *codes);
+
+/* ---- Query path (Alg. 1). ---- */
+/* S[j][c] = <Q_j, c> as keys; S is [Tq][ncent]. (Sec. 2.3: a query vector is
+ * compared against all centroids.) */
+void orc_centroid_scores(const int16_t *q_k, int32_t Tq, const int16_t *cent_k, int32_t ncent, int32_t dim,
+                         int64_t *S);
+/* C_j = first nprobe centroids in the order (S[j][c] desc, c asc)
+ * (Sec. 3.2, candidate generation). Outputs are [Tq][nprobe]. */
+void orc_probe(const int64_t *S, int32_t Tq, int32_t ncent, int32_t nprobe, int32_t *cent_ids,
+               int64_t *cent_keys);
+/* S_Q: ascending docs with a token in a probed list (Sec. 3.2 candidate
+ * generation).  out needs ndocs entries; returns |S_Q|. */
+int64_t orc_candidates(const int32_t *cent_ids, int32_t Tq, int32_t nprobe, const int64_t *ivf_off,
+                       const int32_t *ivf_doc, int64_t ndocs, int32_t *out);
+/* Partial Chamfer score F'(V) of every V in S_Q (Sec. 3.2 candidate
+ * refinement, the F' definition; S[j][c] stands in for the 1-bit token
+ * distance): per query token the max over its probed lists that hold V, 0
+ * if none, summed over query tokens.  docs/fprime need ndocs entries;
+ * returns |S_Q| with docs ascending. */
+int64_t orc_partial_scores(const int64_t *S, const int32_t *cent_ids, int32_t Tq, int32_t ncent,
+                           int32_t nprobe, const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs,
+                           int32_t *docs, int64_t *fprime);
+/* First min(k, n) of (key desc, id asc) (Alg. 1 topK; Alg. 2 last step).
+ * Returns the count written. */
+int64_t orc_topk(const int32_t *ids, const int64_t *keys, int64_t n, int64_t k, int32_t *out_ids,
+                 int64_t *out_keys);
+/* Complete document score over all tokens of each listed doc (Sec. 3.2
+ * document scoring on the GPU; Chamfer, Def. 1) with dequantised tokens
+ * c_cid + w[code]: F^(V) = sum_j max_t (S[j][cid t] + sum_d q_jd w[code_td]).
+ * Tokens of doc i are rows tok_begin[i] .. tok_begin[i]+tok_len[i]-1 of
+ * cid/codes ([rows][dim] unpacked codes). */
+void orc_doc_scores(const int64_t *S, int32_t Tq, int32_t ncent, const int16_t *q_k, int32_t dim,
+                    const int32_t *w_k, int64_t ndocs_r, const int64_t *tok_begin, const int32_t *tok_len,
+                    const int32_t *cid, const uint8_t *codes, int64_t *fhat);
+/* Score value of a key: the int64 rounded once to float, times 2^-22. */
+float orc_key_to_score(int64_t key);
+
+/* Exact Chamfer similarity (Def. 1) of one query against every doc, over
+ * the raw grid tokens. F is [ndocs]. */
+void orc_exact_chamfer(const int16_t *q_k, int32_t Tq, int32_t dim, const int16_t *tok_k,
+                       const int64_t *doc_off, int64_t ndocs, int64_t *F);
+
+/* Whole path for a batch of queries, in memory (Alg. 1 without the CPU
+ * full-bit re-rank), OpenMP over queries only.  Per query q:
+ *   cent_ids/cent_keys [Tq][nprobe]   (may be NULL)
+ *   n_sq[q] = |S_Q|                    (may be NULL)
+ *   cand/cand_keys [ncand], n_cand[q]  (order: F' desc, doc asc; may be NULL)
+ *   ids [k], keys [k]                  (order: F^ desc, doc asc; padded -1 / INT64_MIN)
+ * codes are the unpacked codes of every token ([ntok][dim]).  Returns 0. */
+int orc_search(const int16_t *cent_k, int32_t ncent, int32_t dim, const int64_t *doc_off, int64_t ndocs,
+               const int32_t *cid, const uint8_t *codes, const int32_t *w_k, const int64_t *ivf_off,
+               const int32_t *ivf_doc, const int16_t *q_k, int64_t nq, int32_t Tq, int32_t nprobe,
+               int32_t ncand, int32_t k, int32_t *cent_ids, int64_t *cent_keys, int64_t *n_sq,
+               int32_t *cand, int64_t *cand_keys, int64_t *n_cand, int32_t *ids, int64_t *keys,
+               int nthreads);
+
+/* Only the prune half of orc_search (probe, candidates, F', top-ncand), for
+ * corpora whose codes are produced on demand. */
+int orc_prune_batch(const int16_t *cent_k, int32_t ncent, int32_t dim, int64_t ndocs, const int64_t *ivf_off,
+                    const int32_t *ivf_doc, const int16_t *q_k, int64_t nq, int32_t Tq, int32_t nprobe,
+                    int32_t ncand, int32_t *cent_ids, int64_t *cent_keys, int64_t *n_sq, int32_t *cand,
+                    int64_t *cand_keys, int64_t *n_cand, int nthreads);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,251 @@
+/*
+ * synth.c - seeded synthetic multi-vector corpora.  See synth.h for the recipe.
+ * Input generation only: nothing in this file scores, probes, quantises or
+ * selects.
+ */
+#include "synth.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define GOLDEN_GAMMA 0x9E3779B97F4A7C15ULL
+
+enum {
+  STREAM_CENT = 1,
+  STREAM_LEN = 2,
+  STREAM_TOKCLUSTER = 3,
+  STREAM_TOKNOISE = 4,
+  STREAM_PERM = 5,
+  STREAM_QSRC = 6,
+  STREAM_QNOISE = 7,
+  STREAM_QSEED = 8
+};
+
+struct synth_ctx {
+  synth_cfg cfg;
+  int16_t *cent;  /* [ncent][dim] */
+  double *zipf_cdf; /* [ncent], cumulative unnormalised weights (zipf only) */
+  int32_t *perm;  /* [ncent] rank -> centroid id (zipf only) */
+};
+
+/* SplitMix64 output function. */
+static inline uint64_t sm_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+/* n-th output (0-based) of a SplitMix64 generator whose state starts at s. */
+uint64_t synth_splitmix64_at(uint64_t s, uint64_t n) { return sm_mix(s + (n + 1) * GOLDEN_GAMMA); }
+
+/* Stream key for (seed, stream, index): two chained SplitMix64 draws. */
+static inline uint64_t stream_key(uint64_t seed, uint64_t stream, uint64_t index) {
+  return synth_splitmix64_at(synth_splitmix64_at(seed, stream), index);
+}
+
+/* Uniform double in the open interval (0, 1). */
+static inline double u01(uint64_t key, uint64_t ctr) {
+  uint64_t x = synth_splitmix64_at(key, ctr);
+  return ((double)(x >> 11) + 0.5) * (1.0 / 9007199254740992.0);
+}
+
+/* Box-Muller: the two normals of pair p from counters 2p and 2p+1. */
+static inline void normal_pair(uint64_t key, uint64_t pair, double *z0, double *z1) {
+  double a = u01(key, 2 * pair), b = u01(key, 2 * pair + 1);
+  double r = sqrt(-2.0 * log(a));
+  double t = 6.283185307179586476925286766559 * b;
+  *z0 = r * cos(t);
+  *z1 = r * sin(t);
+}
+
+double synth_to_grid(double x) {
+  double a = fabs(x);
+  if (a < 0.0625) return nearbyint(x * 2048.0) / 2048.0;
+  int e;
+  frexp(a, &e); /* a = m * 2^e, m in [0.5, 1): bf16 spacing is 2^(e-1-7) */
+  double q = ldexp(1.0, e - 8);
+  return nearbyint(x / q) * q;
+}
+
+/* Unit-normalise v[dim] and write its grid integers to out. */
+static void normalise_to_grid(const double *v, int dim, int16_t *out) {
+  double ss = 0.0;
+  for (int i = 0; i < dim; ++i) ss += v[i] * v[i];
+  double inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
+  for (int i = 0; i < dim; ++i) {
+    double g = synth_to_grid(v[i] * inv);
+    out[i] = (int16_t)lrint(g * 2048.0);
+  }
+}
+
+synth_ctx *synth_create(const synth_cfg *cfg) {
+  if (!cfg || cfg->ncent <= 0 || cfg->dim <= 0 || (cfg->dim & 1) || cfg->ndocs < 0) return NULL;
+  if (cfg->len_lo < 1 || cfg->len_hi < cfg->len_lo) return NULL;
+  synth_ctx *ctx = (synth_ctx *)calloc(1, sizeof(synth_ctx));
+  if (!ctx) return NULL;
+  ctx->cfg = *cfg;
+  int n = cfg->ncent, dim = cfg->dim;
+  ctx->cent = (int16_t *)malloc((size_t)n * dim * sizeof(int16_t));
+  if (!ctx->cent) { synth_free(ctx); return NULL; }
+#pragma omp parallel
+  {
+    double *v = (double *)malloc((size_t)dim * sizeof(double));
+#pragma omp for schedule(static)
+    for (int c = 0; c < n; ++c) {
+      uint64_t key = stream_key(cfg->seed, STREAM_CENT, (uint64_t)c);
+      for (int p = 0; p < dim / 2; ++p) normal_pair(key, (uint64_t)p, &v[2 * p], &v[2 * p + 1]);
+      normalise_to_grid(v, dim, ctx->cent + (size_t)c * dim);
+    }
+    free(v);
+  }
+  if (cfg->pop_kind == SYNTH_POP_ZIPF) {
+    ctx->zipf_cdf = (double *)malloc((size_t)n * sizeof(double));
+    ctx->perm = (int32_t *)malloc((size_t)n * sizeof(int32_t));
+    if (!ctx->zipf_cdf || !ctx->perm) { synth_free(ctx); return NULL; }
+    double acc = 0.0;
+    for (int r = 0; r < n; ++r) {
+      acc += pow((double)(r + 1), -cfg->zipf_s);
+      ctx->zipf_cdf[r] = acc;
+    }
+    for (int i = 0; i < n; ++i) ctx->perm[i] = i;
+    uint64_t key = stream_key(cfg->seed, STREAM_PERM, 0);
+    for (int i = n - 1; i > 0; --i) { /* Fisher-Yates */
+      int j = (int)(u01(key, (uint64_t)i) * (double)(i + 1));
+      if (j > i) j = i;
+      int32_t t = ctx->perm[i];
+      ctx->perm[i] = ctx->perm[j];
+      ctx->perm[j] = t;
+    }
+  }
+  return ctx;
+}
+
+void synth_free(synth_ctx *ctx) {
+  if (!ctx) return;
+  free(ctx->cent);
+  free(ctx->zipf_cdf);
+  free(ctx->perm);
+  free(ctx);
+}
+
+const int16_t *synth_centroids(const synth_ctx *ctx) { return ctx->cent; }
+
+static int32_t doc_length(const synth_ctx *ctx, int64_t d) {
+  const synth_cfg *c = &ctx->cfg;
+  uint64_t key = stream_key(c->seed, STREAM_LEN, (uint64_t)d);
+  if (c->len_kind == SYNTH_LEN_FIXED) return c->len_lo;
+  if (c->len_kind == SYNTH_LEN_UNIFORM) {
+    int64_t span = (int64_t)c->len_hi - c->len_lo + 1;
+    int64_t off = (int64_t)(u01(key, 0) * (double)span);
+    if (off >= span) off = span - 1;
+    return (int32_t)(c->len_lo + off);
+  }
+  double z0, z1;
+  normal_pair(key, 0, &z0, &z1);
+  double mu = log(c->len_mean) - 0.5 * c->len_sigma * c->len_sigma;
+  double L = nearbyint(exp(mu + c->len_sigma * z0));
+  if (L < c->len_lo) L = c->len_lo;
+  if (L > c->len_hi) L = c->len_hi;
+  return (int32_t)L;
+}
+
+void synth_doc_lengths(const synth_ctx *ctx, int64_t d0, int64_t d1, int32_t *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t d = d0; d < d1; ++d) out[d - d0] = doc_length(ctx, d);
+}
+
+static int32_t token_cluster(const synth_ctx *ctx, int64_t d, int64_t t) {
+  const synth_cfg *c = &ctx->cfg;
+  uint64_t key = stream_key(c->seed, STREAM_TOKCLUSTER, (uint64_t)d);
+  double u = u01(key, (uint64_t)t);
+  if (c->pop_kind == SYNTH_POP_ZIPF) {
+    double x = u * ctx->zipf_cdf[c->ncent - 1];
+    int lo = 0, hi = c->ncent - 1; /* first rank r with cdf[r] > x */
+    while (lo < hi) {
+      int mid = lo + (hi - lo) / 2;
+      if (ctx->zipf_cdf[mid] > x) hi = mid; else lo = mid + 1;
+    }
+    return ctx->perm[lo];
+  }
+  int32_t k = (int32_t)(u * (double)c->ncent);
+  return k >= c->ncent ? c->ncent - 1 : k;
+}
+
+/* Token t of doc d; v is dim doubles of scratch. */
+static void gen_token(const synth_ctx *ctx, int64_t d, int64_t t, double *v, int16_t *out_k, int32_t *out_cl) {
+  const synth_cfg *c = &ctx->cfg;
+  int dim = c->dim;
+  int32_t cl = token_cluster(ctx, d, t);
+  if (out_cl) *out_cl = cl;
+  if (!out_k) return;
+  const int16_t *cent = ctx->cent + (size_t)cl * dim;
+  uint64_t key = stream_key(c->seed, STREAM_TOKNOISE, (uint64_t)d);
+  for (int p = 0; p < dim / 2; ++p) {
+    double z0, z1;
+    normal_pair(key, (uint64_t)t * (uint64_t)(dim / 2) + (uint64_t)p, &z0, &z1);
+    v[2 * p] = cent[2 * p] / 2048.0 + c->tok_sigma * z0;
+    v[2 * p + 1] = cent[2 * p + 1] / 2048.0 + c->tok_sigma * z1;
+  }
+  normalise_to_grid(v, dim, out_k);
+}
+
+void synth_doc_tokens(const synth_ctx *ctx, int64_t d0, int64_t d1, const int64_t *tok_off,
+                      const int32_t *lens, int16_t *out_k, int32_t *out_cluster, int nthreads) {
+  int dim = ctx->cfg.dim;
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#endif
+#pragma omp parallel num_threads(nthreads)
+  {
+    double *v = (double *)malloc((size_t)dim * sizeof(double));
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t d = d0; d < d1; ++d) {
+      int64_t row = tok_off[d - d0];
+      int32_t L = lens[d - d0];
+      for (int32_t t = 0; t < L; ++t)
+        gen_token(ctx, d, t, v, out_k ? out_k + (size_t)(row + t) * dim : NULL,
+                  out_cluster ? out_cluster + row + t : NULL);
+    }
+    free(v);
+  }
+}
+
+void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_t q1, int32_t Tq,
+                   int16_t *out_k, int64_t *out_src, int nthreads) {
+  const synth_cfg *c = &ctx->cfg;
+  int dim = c->dim;
+  uint64_t qseed = stream_key(c->seed, STREAM_QSEED, query_seed);
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#endif
+#pragma omp parallel num_threads(nthreads)
+  {
+    double *v = (double *)malloc((size_t)dim * sizeof(double));
+    int16_t *src_tok = (int16_t *)malloc((size_t)dim * sizeof(int16_t));
+#pragma omp for schedule(dynamic, 4)
+    for (int64_t q = q0; q < q1; ++q) {
+      uint64_t skey = stream_key(qseed, STREAM_QSRC, (uint64_t)q);
+      int64_t src = (int64_t)(u01(skey, 0) * (double)c->ndocs);
+      if (src >= c->ndocs) src = c->ndocs - 1;
+      if (out_src) out_src[q - q0] = src;
+      int32_t L = doc_length(ctx, src);
+      uint64_t nkey = stream_key(qseed, STREAM_QNOISE, (uint64_t)q);
+      for (int32_t j = 0; j < Tq; ++j) {
+        gen_token(ctx, src, j % L, v, src_tok, NULL);
+        for (int p = 0; p < dim / 2; ++p) {
+          double z0, z1;
+          normal_pair(nkey, (uint64_t)j * (uint64_t)(dim / 2) + (uint64_t)p, &z0, &z1);
+          v[2 * p] = src_tok[2 * p] / 2048.0 + c->q_sigma * z0;
+          v[2 * p + 1] = src_tok[2 * p + 1] / 2048.0 + c->q_sigma * z1;
+        }
+        normalise_to_grid(v, dim, out_k + ((size_t)(q - q0) * Tq + j) * dim);
+      }
+    }
+    free(v);
+    free(src_tok);
+  }
+}
