@@ -1,0 +1,212 @@
+/*
+ * chimera.h - C ABI of the MI355X (gfx950) multi-vector query path.
+ *
+ * Method: "Chimera: Efficient Multi-Vector Retrieval via GPU-CPU
+ * Co-Processing".  The library implements the GPU-resident part of the
+ * query pipeline of Alg. 1: candidate generation (Sec. 3.2), candidate
+ * refinement with a partial Chamfer score (Sec. 3.2, Alg. 2) and document
+ * scoring of the refined candidates over compressed codes (Sec. 3.2, the
+ * GPU half of Alg. 3), returning the top-k documents by Chamfer similarity
+ * (Def. 1) as the MVR problem asks (Def. 2, Eq. 1).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every call returns an int status: CHIMERA_OK (0) or a CHIMERA_E_* code.
+ *    chimera_last_error() then holds a message for the calling thread.
+ *  - Arguments are validated on the host before anything is launched; a call
+ *    that fails validation leaves every output untouched.
+ *  - "device pointer" means memory on the index's HIP device (hipMalloc or a
+ *    torch CUDA tensor).  The caller owns every pointer it passes in; the
+ *    index handle owns all device memory of the index and its scratch.
+ *  - Search calls are asynchronous on `hip_stream` (a hipStream_t; NULL is
+ *    the null stream); outputs are valid after that stream synchronises.
+ *    Successive calls on one index may use different streams: the library
+ *    orders them on its scratch.  Concurrent host calls on one index return
+ *    CHIMERA_E_BUSY.
+ *  - Value grid G: all vector values are used as bf16 numbers that are
+ *    integer multiples of 2^-11.  Inputs are rounded onto G (nearest, ties to
+ *    even), which leaves grid values unchanged.  On G every inner product is
+ *    an exact multiple of 2^-22, so scores are exact and independent of the
+ *    summation order provided every query token has L2 norm <= 2 (unit
+ *    vectors in the intended use).
+ *  - Orders: every "top" list is ordered by (score descending, id
+ *    ascending); equal scores are broken by the lowest id.
+ */
+#ifndef CHIMERA_H
+#define CHIMERA_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CHIMERA_ABI_VERSION 1
+
+enum {
+  CHIMERA_OK = 0,
+  CHIMERA_E_INVAL = 1,       /* bad argument */
+  CHIMERA_E_NOMEM = 2,       /* host or device allocation failed / would not fit */
+  CHIMERA_E_IO = 3,          /* file could not be opened, read or written */
+  CHIMERA_E_FORMAT = 4,      /* index file malformed, truncated, wrong version or checksum */
+  CHIMERA_E_DEVICE = 5,      /* HIP runtime error; the index must be freed */
+  CHIMERA_E_UNSUPPORTED = 6, /* valid but outside this build's limits (dim != 128, Tq > 64, nprobe > 64 ...) */
+  CHIMERA_E_BUSY = 7         /* another host thread is inside a call on this index */
+};
+
+/* Element type of a query tensor. */
+enum { CHIMERA_F32 = 0, CHIMERA_BF16 = 1 };
+
+/* Limits of this build. */
+#define CHIMERA_DIM 128
+#define CHIMERA_MAX_TQ 64
+#define CHIMERA_MAX_NPROBE 64
+#define CHIMERA_MAX_NCAND (1 << 20)
+
+typedef struct chimera_index chimera_index;
+typedef struct chimera_builder chimera_builder;
+
+typedef struct {
+  int64_t ndocs;         /* documents */
+  int64_t ntokens;       /* document tokens */
+  int64_t nnz;           /* entries of all posting lists */
+  int32_t ncent;         /* IVF centroids */
+  int32_t dim;           /* vector dimension (128) */
+  int32_t nbits;         /* residual code bits per dimension (2 or 4) */
+  int32_t max_doc_len;   /* longest document, tokens */
+  int64_t device_bytes;  /* device memory held by the index data */
+  int32_t device;        /* HIP device ordinal */
+} chimera_index_info;
+
+/* Last error message of the calling thread; never NULL. */
+const char *chimera_last_error(void);
+
+/* ===================================================================== *
+ * Offline index building (Sec. 3.1): IVF posting lists over the
+ * centroids and per-token compressed codes, stored document-major so that
+ * each document's tokens are contiguous (the doc-reordered copy of the
+ * codes in Sec. 4.1).  Host only, no GPU needed.
+ *
+ * Compression: each token t with centroid c = cid[t] stores the residual
+ * r = v_t - c per dimension as a b-bit bucket code (b = nbits, 2 or 4).
+ * The 2^b buckets are cut at the pooled empirical quantiles i/2^b
+ * (i = 1 .. 2^b-1) of all residual components of the corpus; bucket u is
+ * represented by the grid value of the (2u+1)/2^(b+1) quantile.  A residual
+ * equal to a cutoff falls in the lower bucket.  (The paper compresses with
+ * RaBitQ codes; this residual-bucket reading is the library's code family.)
+ *
+ * Two passes over the same token stream, in document order:
+ *   1. chimera_builder_add_residuals for every token (any chunking);
+ *   2. chimera_builder_freeze_quantizer;
+ *   3. chimera_builder_add_docs for every document, in document order.
+ * The IVF assignment cid[] is an input: the caller gives, for each token,
+ * its centroid (normally its nearest centroid by inner product, Sec. 2.3).
+ * ===================================================================== */
+
+/* centroids_bf16: host [ncent][dim] bf16 bit patterns (copied).  dim must be
+ * 128; nbits 2 or 4; ncent >= 1.  *out receives the builder. */
+int chimera_builder_create(const uint16_t *centroids_bf16, int32_t ncent, int32_t dim, int32_t nbits,
+                           chimera_builder **out);
+/* Pass 1: tokens_bf16 host [ntok][dim], cids host [ntok] in [0, ncent). */
+int chimera_builder_add_residuals(chimera_builder *b, const uint16_t *tokens_bf16, const int32_t *cids,
+                                  int64_t ntok);
+/* Ends pass 1: fixes cutoffs and bucket weights.  E_INVAL if no residual. */
+int chimera_builder_freeze_quantizer(chimera_builder *b);
+/* Pass 2: ndocs documents; doc_lens host [ndocs] (>= 1 each), tokens and cids
+ * hold sum(doc_lens) rows in document order. */
+int chimera_builder_add_docs(chimera_builder *b, const uint16_t *tokens_bf16, const int32_t *cids,
+                             const int32_t *doc_lens, int64_t ndocs);
+/* Quantiser as fixed by freeze: cut_k [2^b - 1] cutoffs in units of 2^-11,
+ * weights_bf16 [2^b] bucket values.  Either pointer may be NULL. */
+int chimera_builder_quantizer(const chimera_builder *b, int32_t *cut_k, uint16_t *weights_bf16);
+/* Writes the index file (format "CHIMIDX1", little-endian, 256-byte aligned
+ * sections, each with a 64-bit FNV-1a checksum). */
+int chimera_builder_save(const chimera_builder *b, const char *path);
+/* Copies the built index to HIP device `hip_device`; *out receives a handle
+ * equivalent to chimera_index_load of the saved file. */
+int chimera_builder_upload(const chimera_builder *b, int hip_device, chimera_index **out);
+/* Host copies of built sections (for inspection and tests).  Sizes:
+ * doc_off [ndocs+1] i64, cid [ntok] i32, codes [ntok][dim*nbits/8] u8,
+ * ivf_off [ncent+1] i64, ivf_doc [nnz] i32.  Any pointer may be NULL. */
+int chimera_builder_sections(const chimera_builder *b, int64_t *doc_off, int32_t *cid, uint8_t *codes,
+                             int64_t *ivf_off, int32_t *ivf_doc);
+int chimera_builder_info(const chimera_builder *b, chimera_index_info *out);
+void chimera_builder_free(chimera_builder *b); /* NULL-safe */
+
+/* ===================================================================== *
+ * Device-resident index (Sec. 3: every GPU-side structure is preloaded,
+ * only queries move at run time).
+ * ===================================================================== */
+
+/* Reads and verifies an index file and copies it to HIP device `hip_device`.
+ * E_IO (open/read), E_FORMAT (magic, version, sizes, checksums), E_NOMEM. */
+int chimera_index_load(const char *path, int hip_device, chimera_index **out);
+void chimera_index_free(chimera_index *idx); /* NULL-safe; waits for pending work */
+int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out);
+
+/* ===================================================================== *
+ * Search (Alg. 1 without the CPU full-bit stage).
+ *
+ *   Q       device [nq][Tq][d], q_dtype CHIMERA_F32 or CHIMERA_BF16, row-major
+ *   nq      >= 0 queries (0: no-op)
+ *   Tq      1 .. 64 tokens per query
+ *   d       must equal the index dimension (128)
+ *   nprobe  1 .. min(ncent, 64): centroids probed per query token
+ *   ncand   >= k: documents kept by the refinement (k_refine of Alg. 1);
+ *           values above ndocs are clamped to ndocs
+ *   k       >= 1 results per query
+ *   ids     device [nq][k] int32, scores device [nq][k] float32
+ *
+ * Steps, per query:
+ *  1. S[j][c] = <Q_j, c> for every centroid c, and C_j = the nprobe best
+ *     centroids of query token j (Sec. 2.3 IVF probe; Sec. 3.2 candidate
+ *     generation).
+ *  2. S_Q = documents with a token in some probed posting list (Sec. 3.2,
+ *     the candidate set S).
+ *  3. F'(V) = sum_j max{S[j][c] : c in C_j, V has a token in list c}, a term
+ *     being 0 when no probed list of Q_j holds V (Sec. 3.2, the partial score
+ *     F'; the centroid score stands in for the per-token distance); keep the
+ *     ncand best of S_Q (Alg. 2).
+ *  4. For each kept V: F^(V) = sum_j max_{t in V} <Q_j, c_cid(t) + w(code_t)>,
+ *     the complete score over all of V's tokens from their decoded residual
+ *     codes (Sec. 3.2 document scoring; Sec. 4.2 aggregation).
+ *  5. ids/scores = the k best by F^, padded with (-1, -INFINITY) when fewer
+ *     than k documents were kept.
+ * Scores are exact multiples of 2^-22, rounded once to float32.
+ * ===================================================================== */
+int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                   int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream);
+
+/* Stage taps: the same inputs as chimera_search, stopping after a stage.
+ * They exist so that each stage can be compared with an independent
+ * reference; they cost as much as the stages they run. */
+
+/* After step 1: cent_ids device [nq][Tq][nprobe] int32, ordered; cent_keys
+ * device [nq][Tq][nprobe] int32, S in units of 2^-22. */
+int chimera_probe(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                  int32_t nprobe, int32_t *cent_ids, int32_t *cent_keys, void *hip_stream);
+
+/* After step 2: offsets device [nq+1] int64 (CSR), doc_ids device
+ * [capacity] int32, each query's S_Q ascending.  Synchronises the stream.
+ * E_INVAL if sum |S_Q| > capacity; offsets are still written then. */
+int chimera_candidates(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                       int32_t nprobe, int64_t *offsets, int32_t *doc_ids, int64_t capacity, void *hip_stream);
+
+/* After step 3: cand_ids device [nq][ncand] int32 holding the kept documents
+ * in ascending id order, cand_keys device [nq][ncand] int32 their F' in units
+ * of 2^-22, n_valid device [nq] int32 the number kept (min(ncand, |S_Q|));
+ * entries past n_valid are -1 / 0.  ncand is clamped to ndocs. */
+int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                  int32_t nprobe, int32_t ncand, int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid,
+                  void *hip_stream);
+
+/* Per-stage device time of the last search on this index, in ms, measured
+ * with HIP events when the environment variable CHIMERA_STAGE_TIMING=1 was
+ * set at load time: [0] query rounding, [1] probe, [2] candidate walk,
+ * [3] refinement select, [4] residual scoring, [5] final top-k.  Summed over
+ * sub-batches.  E_INVAL if timing is off. */
+int chimera_stage_times(const chimera_index *idx, float *ms6);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

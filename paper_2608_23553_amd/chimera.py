@@ -1,0 +1,291 @@
+"""Thin ctypes binding of ``libchimera.so`` (see ``include/chimera.h``).
+
+Argument marshalling only: every step of the query path runs in the HIP
+library.  Device buffers and streams come from PyTorch (ROCm); host buffers
+for the index builder are numpy arrays.  If the library is missing the import
+of this module still works, but every call raises ``RuntimeError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Callable, Iterable, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libchimera.so")
+
+OK, E_INVAL, E_NOMEM, E_IO, E_FORMAT, E_DEVICE, E_UNSUPPORTED, E_BUSY = range(8)
+F32, BF16 = 0, 1
+_ERR_NAMES = {1: "INVAL", 2: "NOMEM", 3: "IO", 4: "FORMAT", 5: "DEVICE", 6: "UNSUPPORTED", 7: "BUSY"}
+
+_lib = None
+
+
+class ChimeraError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"chimera error {_ERR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("ndocs", ctypes.c_int64), ("ntokens", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("ncent", ctypes.c_int32), ("dim", ctypes.c_int32), ("nbits", ctypes.c_int32),
+                ("max_doc_len", ctypes.c_int32), ("device_bytes", ctypes.c_int64), ("device", ctypes.c_int32)]
+
+
+def lib():
+    """Loads libchimera.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, INT = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int
+    sig = {
+        "chimera_last_error": ([], ctypes.c_char_p),
+        "chimera_builder_create": ([P, I32, I32, I32, P], INT),
+        "chimera_builder_add_residuals": ([P, P, P, I64], INT),
+        "chimera_builder_freeze_quantizer": ([P], INT),
+        "chimera_builder_add_docs": ([P, P, P, P, I64], INT),
+        "chimera_builder_quantizer": ([P, P, P], INT),
+        "chimera_builder_save": ([P, ctypes.c_char_p], INT),
+        "chimera_builder_upload": ([P, INT, P], INT),
+        "chimera_builder_sections": ([P, P, P, P, P, P], INT),
+        "chimera_builder_info": ([P, P], INT),
+        "chimera_builder_free": ([P], None),
+        "chimera_index_load": ([ctypes.c_char_p, INT, P], INT),
+        "chimera_index_free": ([P], None),
+        "chimera_index_info_get": ([P, P], INT),
+        "chimera_search": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
+        "chimera_probe": ([P, P, INT, I64, I32, I32, I32, P, P, P], INT),
+        "chimera_candidates": ([P, P, INT, I64, I32, I32, I32, P, P, I64, P], INT),
+        "chimera_prune": ([P, P, INT, I64, I32, I32, I32, I32, P, P, P, P], INT),
+        "chimera_stage_times": ([P, P], INT),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    return lib().chimera_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise ChimeraError(rc, last_error())
+
+
+def _np(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _info(st: _Info) -> dict:
+    return {k: getattr(st, k) for k, _ in _Info._fields_}
+
+
+# --------------------------------------------------------------- builder
+class Builder:
+    """Offline index builder (host only).  Two passes over the same stream of
+    tokens in document order: add_residuals(...) for all tokens, freeze(),
+    then add_docs(...) for all documents."""
+
+    def __init__(self, centroids_bf16: np.ndarray, nbits: int):
+        c = np.ascontiguousarray(centroids_bf16, dtype=np.uint16)
+        h = ctypes.c_void_p()
+        _check(lib().chimera_builder_create(_np(c), c.shape[0], c.shape[1], nbits, ctypes.byref(h)))
+        self._h = h
+        self.ncent, self.dim, self.nbits = c.shape[0], c.shape[1], nbits
+
+    def __del__(self):
+        self.close()
+
+    def close(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.chimera_builder_free(self._h)
+            self._h = None
+
+    def add_residuals(self, tokens_bf16: np.ndarray, cids: np.ndarray):
+        t = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
+        c = np.ascontiguousarray(cids, dtype=np.int32)
+        _check(lib().chimera_builder_add_residuals(self._h, _np(t), _np(c), c.shape[0]))
+
+    def freeze(self):
+        _check(lib().chimera_builder_freeze_quantizer(self._h))
+
+    def add_docs(self, tokens_bf16: np.ndarray, cids: np.ndarray, doc_lens: np.ndarray):
+        t = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
+        c = np.ascontiguousarray(cids, dtype=np.int32)
+        l = np.ascontiguousarray(doc_lens, dtype=np.int32)
+        _check(lib().chimera_builder_add_docs(self._h, _np(t), _np(c), _np(l), l.shape[0]))
+
+    def quantizer(self) -> Tuple[np.ndarray, np.ndarray]:
+        B = 1 << self.nbits
+        cut = np.empty(B - 1, np.int32)
+        w = np.empty(B, np.uint16)
+        _check(lib().chimera_builder_quantizer(self._h, _np(cut), _np(w)))
+        return cut, w
+
+    def info(self) -> dict:
+        st = _Info()
+        _check(lib().chimera_builder_info(self._h, ctypes.byref(st)))
+        return _info(st)
+
+    def sections(self) -> dict:
+        inf = self.info()
+        out = dict(doc_off=np.empty(inf["ndocs"] + 1, np.int64), cid=np.empty(inf["ntokens"], np.int32),
+                   codes=np.empty((inf["ntokens"], self.dim * self.nbits // 8), np.uint8),
+                   ivf_off=np.empty(self.ncent + 1, np.int64), ivf_doc=np.empty(inf["nnz"], np.int32))
+        _check(lib().chimera_builder_sections(self._h, _np(out["doc_off"]), _np(out["cid"]), _np(out["codes"]),
+                                              _np(out["ivf_off"]), _np(out["ivf_doc"])))
+        return out
+
+    def save(self, path: str):
+        _check(lib().chimera_builder_save(self._h, path.encode()))
+
+    def upload(self, device: int = 0) -> "Index":
+        h = ctypes.c_void_p()
+        _check(lib().chimera_builder_upload(self._h, device, ctypes.byref(h)))
+        return Index(h)
+
+
+def build_index(centroids_bf16: np.ndarray, nbits: int,
+                chunks: Callable[[], Iterable[Tuple[np.ndarray, np.ndarray, np.ndarray]]]) -> Builder:
+    """Two-pass streaming build.  ``chunks()`` must yield the same sequence of
+    (tokens_bf16 [rows,dim], cids [rows], doc_lens [ndocs_chunk]) each time it
+    is called, covering every document in order."""
+    b = Builder(centroids_bf16, nbits)
+    for tok, cid, _ in chunks():
+        b.add_residuals(tok, cid)
+    b.freeze()
+    for tok, cid, lens in chunks():
+        b.add_docs(tok, cid, lens)
+    return b
+
+
+# ----------------------------------------------------------------- index
+def _stream_ptr(stream) -> ctypes.c_void_p:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _q_args(Q):
+    import torch
+    if not Q.is_cuda:
+        raise ValueError("Q must be a device tensor")
+    if Q.dim() != 3:
+        raise ValueError("Q must be [nq, Tq, d]")
+    Q = Q.contiguous()
+    if Q.dtype == torch.float32:
+        dt = F32
+    elif Q.dtype == torch.bfloat16:
+        dt = BF16
+    else:
+        raise ValueError("Q must be float32 or bfloat16")
+    return Q, dt
+
+
+class Index:
+    """A device-resident index (owns its HBM); see ``chimera_index_load``."""
+
+    def __init__(self, handle: ctypes.c_void_p):
+        self._h = handle
+        self._info = self.info()
+
+    @classmethod
+    def load(cls, path: str, device: int = 0) -> "Index":
+        h = ctypes.c_void_p()
+        _check(lib().chimera_index_load(path.encode(), device, ctypes.byref(h)))
+        return cls(h)
+
+    def close(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.chimera_index_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+    def info(self) -> dict:
+        st = _Info()
+        _check(lib().chimera_index_info_get(self._h, ctypes.byref(st)))
+        return _info(st)
+
+    @property
+    def device(self):
+        import torch
+        return torch.device("cuda", self._info["device"])
+
+    def search(self, Q, nprobe: int, ncand: int, k: int, out=None, stream=None):
+        """Top-k (ids int32 [nq,k], scores float32 [nq,k]) for queries Q [nq,Tq,d]."""
+        import torch
+        Q, dt = _q_args(Q)
+        nq, Tq, d = Q.shape
+        if out is None:
+            ids = torch.empty((nq, k), dtype=torch.int32, device=Q.device)
+            scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
+        else:
+            ids, scores = out
+        _check(lib().chimera_search(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, k,
+                                    ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(scores.data_ptr()),
+                                    _stream_ptr(stream)))
+        return ids, scores
+
+    def search_raw(self, q_ptr: int, q_dtype: int, nq: int, Tq: int, d: int, nprobe: int, ncand: int, k: int,
+                   ids_ptr: int, scores_ptr: int, stream_ptr: int) -> int:
+        """Direct call with raw pointers; returns the status code."""
+        return lib().chimera_search(self._h, ctypes.c_void_p(q_ptr), q_dtype, nq, Tq, d, nprobe, ncand, k,
+                                    ctypes.c_void_p(ids_ptr), ctypes.c_void_p(scores_ptr), ctypes.c_void_p(stream_ptr))
+
+    def probe(self, Q, nprobe: int, stream=None):
+        import torch
+        Q, dt = _q_args(Q)
+        nq, Tq, d = Q.shape
+        ids = torch.empty((nq, Tq, nprobe), dtype=torch.int32, device=Q.device)
+        keys = torch.empty((nq, Tq, nprobe), dtype=torch.int32, device=Q.device)
+        _check(lib().chimera_probe(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe,
+                                   ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(keys.data_ptr()),
+                                   _stream_ptr(stream)))
+        return ids, keys
+
+    def candidates(self, Q, nprobe: int, capacity: int | None = None, stream=None):
+        import torch
+        Q, dt = _q_args(Q)
+        nq, Tq, d = Q.shape
+        if capacity is None:
+            capacity = nq * self._info["ndocs"]
+        offsets = torch.empty(nq + 1, dtype=torch.int64, device=Q.device)
+        doc_ids = torch.empty(max(capacity, 1), dtype=torch.int32, device=Q.device)
+        _check(lib().chimera_candidates(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe,
+                                        ctypes.c_void_p(offsets.data_ptr()), ctypes.c_void_p(doc_ids.data_ptr()),
+                                        capacity, _stream_ptr(stream)))
+        return offsets, doc_ids
+
+    def prune(self, Q, nprobe: int, ncand: int, stream=None):
+        import torch
+        Q, dt = _q_args(Q)
+        nq, Tq, d = Q.shape
+        nc = min(ncand, self._info["ndocs"])
+        cand = torch.empty((nq, nc), dtype=torch.int32, device=Q.device)
+        keys = torch.empty((nq, nc), dtype=torch.int32, device=Q.device)
+        nval = torch.empty(nq, dtype=torch.int32, device=Q.device)
+        _check(lib().chimera_prune(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand,
+                                   ctypes.c_void_p(cand.data_ptr()), ctypes.c_void_p(keys.data_ptr()),
+                                   ctypes.c_void_p(nval.data_ptr()), _stream_ptr(stream)))
+        return cand, keys, nval
+
+    def stage_times(self) -> np.ndarray:
+        ms = np.zeros(6, np.float32)
+        _check(lib().chimera_stage_times(self._h, _np(ms)))
+        return ms

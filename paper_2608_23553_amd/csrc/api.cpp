@@ -1,0 +1,437 @@
+// api.cpp - the C ABI: errors, device index, validation and the per-batch
+// orchestration of the query path (Alg. 1 without the CPU full-bit stage).
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "internal.h"
+
+namespace chimera {
+
+static thread_local char g_err[512] = "no error";
+
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+  if (e == hipErrorOutOfMemory) return fail(CHIMERA_E_NOMEM, "%s: %s", what, hipGetErrorString(e));
+  return fail(CHIMERA_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(dev) == hipSuccess) ok = true;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+// Marks the index busy for the duration of a host call.
+struct BusyGuard {
+  chimera_index *idx;
+  bool ok;
+  explicit BusyGuard(chimera_index *i) : idx(i), ok(i->busy.exchange(1) == 0) {}
+  ~BusyGuard() {
+    if (ok) idx->busy.store(0);
+  }
+};
+
+static int upload(const HostIndex &h, int device, chimera_index **out) {
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) return fail(CHIMERA_E_DEVICE, "no HIP device available");
+  if (device < 0 || device >= ndev) return fail(CHIMERA_E_INVAL, "device %d out of range (%d devices)", device, ndev);
+  DeviceGuard dg(device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", device);
+  chimera_index *idx = new (std::nothrow) chimera_index;
+  if (!idx) return fail(CHIMERA_E_NOMEM, "handle allocation");
+  idx->device = device;
+  idx->ncent = h.ncent; idx->dim = h.dim; idx->nbits = h.nbits; idx->max_doc_len = h.max_doc_len;
+  idx->ndocs = h.ndocs; idx->ntok = h.ntok; idx->nnz = h.nnz;
+  std::memcpy(idx->h_weights, h.weights.data(), h.weights.size() * 2);
+  std::memcpy(idx->h_cut, h.cut_k.data(), h.cut_k.size() * 4);
+  struct Sec { void **dst; const void *src; size_t bytes; } secs[] = {
+      {(void **)&idx->d_cent, h.cent.data(), h.cent.size() * 2},
+      {(void **)&idx->d_doc_off, h.doc_off.data(), h.doc_off.size() * 8},
+      {(void **)&idx->d_cid, h.cid.data(), h.cid.size() * 4},
+      {(void **)&idx->d_codes, h.codes.data(), h.codes.size()},
+      {(void **)&idx->d_ivf_off, h.ivf_off.data(), h.ivf_off.size() * 8},
+      {(void **)&idx->d_ivf_doc, h.ivf_doc.data(), h.ivf_doc.size() * 4},
+  };
+  size_t need = 0;
+  for (auto &s : secs) need += s.bytes;
+  size_t free_b = 0, total_b = 0;
+  if (hipMemGetInfo(&free_b, &total_b) == hipSuccess && need > free_b) {
+    delete idx;
+    return fail(CHIMERA_E_NOMEM, "index needs %zu bytes, %zu free on device %d", need, free_b, device);
+  }
+  for (auto &s : secs) {
+    // one padding byte keeps every section non-empty
+    hipError_t e = hipMalloc(s.dst, s.bytes + 16);
+    if (e == hipSuccess && s.bytes) e = hipMemcpy(*s.dst, s.src, s.bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      int rc = hip_fail(e, "index upload");
+      chimera_index_free(idx);
+      return rc;
+    }
+    idx->device_bytes += (int64_t)s.bytes;
+  }
+  if (hipEventCreateWithFlags(&idx->scratch_done, hipEventDisableTiming) != hipSuccess) {
+    chimera_index_free(idx);
+    return fail(CHIMERA_E_DEVICE, "event creation failed");
+  }
+  const char *t = std::getenv("CHIMERA_STAGE_TIMING");
+  idx->timing = t && t[0] == '1';
+  *out = idx;
+  return CHIMERA_OK;
+}
+
+// ----------------------------------------------------------- validation
+static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                            int32_t nprobe) {
+  if (!idx) return fail(CHIMERA_E_INVAL, "null index");
+  if (nq < 0) return fail(CHIMERA_E_INVAL, "nq must be >= 0");
+  if (nq > 0 && !Q) return fail(CHIMERA_E_INVAL, "null query pointer");
+  if (q_dtype != CHIMERA_F32 && q_dtype != CHIMERA_BF16) return fail(CHIMERA_E_INVAL, "q_dtype must be F32 or BF16");
+  if (d != idx->dim) return fail(CHIMERA_E_INVAL, "query dim %d != index dim %d", d, idx->dim);
+  if (Tq < 1) return fail(CHIMERA_E_INVAL, "Tq must be >= 1");
+  if (Tq > CHIMERA_MAX_TQ) return fail(CHIMERA_E_UNSUPPORTED, "Tq %d > %d", Tq, CHIMERA_MAX_TQ);
+  if (nprobe < 1 || nprobe > idx->ncent) return fail(CHIMERA_E_INVAL, "nprobe must be in [1, ncent=%d]", idx->ncent);
+  if (nprobe > CHIMERA_MAX_NPROBE) return fail(CHIMERA_E_UNSUPPORTED, "nprobe %d > %d", nprobe, CHIMERA_MAX_NPROBE);
+  return CHIMERA_OK;
+}
+
+static const int kMaxK = 8192;
+
+// ------------------------------------------------------------- pipeline
+enum Stop { STOP_PROBE = 1, STOP_CANDIDATES = 2, STOP_PRUNE = 3, STOP_FULL = 4 };
+
+struct Outs {
+  int32_t *cent_ids = nullptr, *cent_keys = nullptr;            // probe tap [nq][Tq][nprobe]
+  int64_t *offsets = nullptr; int32_t *doc_ids = nullptr; int64_t capacity = 0;  // candidates tap
+  int32_t *cand_ids = nullptr, *cand_keys = nullptr, *n_valid = nullptr;         // prune tap
+  int32_t *ids = nullptr; float *scores = nullptr;                               // search
+};
+
+static size_t align_up(size_t x) { return (x + 255) / 256 * 256; }
+
+struct Carve {
+  char *base;
+  size_t off = 0;
+  template <class T>
+  T *take(size_t n) {
+    T *p = (T *)(base + off);
+    off += align_up(n * sizeof(T));
+    return p;
+  }
+};
+
+// Exact bytes the sub-batch loop below carves for nb queries.
+static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int nprobe, int ncand, Stop stop) {
+  const int64_t rows = nb * TQP;
+  const ProbePlan plan = plan_probe(rows, idx->ncent, nprobe);
+  size_t b = 0;
+  b += align_up((size_t)rows * 128 * 2);                       // Qs
+  b += align_up(probe_part_bytes(plan, rows));                 // partial lists
+  b += 2 * align_up((size_t)rows * nprobe * 4);                // cent ids / keys
+  if (stop >= STOP_FULL) b += align_up((size_t)nb * idx->ncent * TQP * 4);  // S^T
+  if (stop >= STOP_CANDIDATES) {
+    b += align_up((size_t)nb * idx->ndocs * (TQP == 32 ? 4 : 8));  // mask
+    b += align_up((size_t)nb * idx->ndocs * 4);                     // F'
+  }
+  if (stop == STOP_CANDIDATES) b += align_up((size_t)(nb + 1) * 8);  // counts
+  if (stop >= STOP_PRUNE) b += 3 * align_up((size_t)nb * ncand * 4) + align_up((size_t)nb * 4);  // cand, keys, F^, n
+  return b;
+}
+
+static int ensure_scratch(chimera_index *idx, size_t bytes) {
+  if (bytes <= idx->scratch_bytes) return CHIMERA_OK;
+  if (idx->scratch) {
+    CHIMERA_HIP(hipDeviceSynchronize());
+    CHIMERA_HIP(hipFree(idx->scratch));
+    idx->scratch = nullptr;
+    idx->scratch_bytes = 0;
+    idx->scratch_pending = false;
+  }
+  size_t want = bytes + bytes / 8;
+  hipError_t e = hipMalloc(&idx->scratch, want);
+  if (e != hipSuccess) {
+    idx->scratch = nullptr;
+    return hip_fail(e, "scratch allocation");
+  }
+  idx->scratch_bytes = want;
+  return CHIMERA_OK;
+}
+
+static size_t scratch_budget() {
+  const char *s = std::getenv("CHIMERA_SCRATCH_MB");
+  size_t mb = s ? (size_t)std::strtoull(s, nullptr, 10) : 8192;
+  if (mb < 16) mb = 16;
+  return mb << 20;
+}
+
+static void stage_mark(chimera_index *idx, hipStream_t s) {
+  if (!idx->timing) return;
+  if (idx->ev_used >= (int)idx->ev.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    idx->ev.push_back(e);
+  }
+  (void)hipEventRecord(idx->ev[idx->ev_used++], s);
+}
+
+static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int Tq, int nprobe, int ncand, int k,
+               Stop stop, Outs o, hipStream_t s) {
+  const int TQP = Tq <= 32 ? 32 : 64;
+  // sub-batch size from the scratch budget
+  const size_t perq = carve_bytes(idx, 1, TQP, nprobe, ncand, stop);
+  int64_t B = std::max<int64_t>(1, (int64_t)(scratch_budget() / perq));
+  B = std::min<int64_t>(B, nq);
+  B = std::min<int64_t>(B, 65535);
+  size_t need = carve_bytes(idx, B, TQP, nprobe, ncand, stop);
+  if (nq % B) need = std::max(need, carve_bytes(idx, nq % B, TQP, nprobe, ncand, stop));
+  int rc = ensure_scratch(idx, need);
+  if (rc) return rc;
+  if (idx->scratch_pending) CHIMERA_HIP(hipStreamWaitEvent(s, idx->scratch_done, 0));
+  idx->ev_used = 0;
+
+  std::vector<int64_t> host_counts;
+  int64_t total_hits = 0;
+  const size_t mask_word = TQP == 32 ? 4 : 8;
+
+  for (int64_t q0 = 0; q0 < nq; q0 += B) {
+    const int64_t nb = std::min<int64_t>(B, nq - q0);
+    const int64_t rows = nb * TQP;
+    const ProbePlan plan = plan_probe(rows, idx->ncent, nprobe);
+    Carve cv{(char *)idx->scratch};
+    uint16_t *Qs = cv.take<uint16_t>((size_t)rows * 128);
+    uint64_t *part = cv.take<uint64_t>(probe_part_bytes(plan, rows) / 8);
+    int32_t *ci = cv.take<int32_t>((size_t)rows * nprobe);
+    int32_t *ck = cv.take<int32_t>((size_t)rows * nprobe);
+    float *ST = stop >= STOP_FULL ? cv.take<float>((size_t)nb * idx->ncent * TQP) : nullptr;
+    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    const size_t qbytes = (size_t)Tq * 128 * (q_dtype == CHIMERA_F32 ? 4 : 2);
+    const void *Qb = (const char *)Q + (size_t)q0 * qbytes;
+
+    stage_mark(idx, s);
+    launch_round_queries(Qb, q_dtype, nb, Tq, TQP, Qs, s);
+    stage_mark(idx, s);
+    launch_probe(Qs, rows, TQP, idx->d_cent, idx->ncent, plan, part, ST, s);
+    launch_probe_merge(part, nb, Tq, TQP, plan, nprobe, ci, ck, s);
+    CHIMERA_HIP(hipGetLastError());
+    if (stop == STOP_PROBE) {
+      CHIMERA_HIP(hipMemcpy2DAsync(o.cent_ids + q0 * Tq * nprobe, (size_t)Tq * nprobe * 4, ci,
+                                   (size_t)TQP * nprobe * 4, (size_t)Tq * nprobe * 4, nb, hipMemcpyDeviceToDevice, s));
+      CHIMERA_HIP(hipMemcpy2DAsync(o.cent_keys + q0 * Tq * nprobe, (size_t)Tq * nprobe * 4, ck,
+                                   (size_t)TQP * nprobe * 4, (size_t)Tq * nprobe * 4, nb, hipMemcpyDeviceToDevice, s));
+      continue;
+    }
+    void *mask = cv.take<char>((size_t)nb * idx->ndocs * mask_word);
+    int32_t *fp = cv.take<int32_t>((size_t)nb * idx->ndocs);
+    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    stage_mark(idx, s);
+    launch_fill_zero(mask, (size_t)nb * idx->ndocs * mask_word, s);
+    launch_fill_zero(fp, (size_t)nb * idx->ndocs * 4, s);
+    launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, mask, fp, s);
+    CHIMERA_HIP(hipGetLastError());
+    if (stop == STOP_CANDIDATES) {
+      int64_t *cnt = cv.take<int64_t>((size_t)nb + 1);
+      if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+      launch_count_hits(mask, nb, TQP, idx->ndocs, cnt, s);
+      std::vector<int64_t> hc(nb);
+      CHIMERA_HIP(hipMemcpyAsync(hc.data(), cnt, nb * 8, hipMemcpyDeviceToHost, s));
+      CHIMERA_HIP(hipStreamSynchronize(s));
+      std::vector<int64_t> offs(nb + 1);
+      offs[0] = total_hits;
+      for (int64_t i = 0; i < nb; ++i) offs[i + 1] = offs[i] + hc[i];
+      bool fits = offs[nb] <= o.capacity;
+      if (fits && offs[nb] > total_hits) {
+        CHIMERA_HIP(hipMemcpyAsync(cnt, offs.data(), (nb + 1) * 8, hipMemcpyHostToDevice, s));
+        launch_list_hits(mask, nb, TQP, idx->ndocs, cnt, o.doc_ids, s);
+        CHIMERA_HIP(hipStreamSynchronize(s));
+      }
+      for (int64_t i = 0; i < nb; ++i) host_counts.push_back(hc[i]);
+      total_hits = offs[nb];
+      continue;
+    }
+    int32_t *cand = o.cand_ids ? o.cand_ids + q0 * ncand : cv.take<int32_t>((size_t)nb * ncand);
+    int32_t *candk = o.cand_keys ? o.cand_keys + q0 * ncand : cv.take<int32_t>((size_t)nb * ncand);
+    int32_t *nval = o.n_valid ? o.n_valid + q0 : cv.take<int32_t>((size_t)nb);
+    int32_t *fhat = stop >= STOP_FULL ? cv.take<int32_t>((size_t)nb * ncand) : nullptr;
+    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    stage_mark(idx, s);
+    launch_select(mask, fp, nb, TQP, idx->ndocs, ncand, cand, candk, nval, s);
+    CHIMERA_HIP(hipGetLastError());
+    if (stop == STOP_PRUNE) continue;
+    stage_mark(idx, s);
+    launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
+                          idx->h_weights, cand, nval, ncand, fhat, s);
+    stage_mark(idx, s);
+    launch_topk(fhat, cand, nval, nb, ncand, k, o.ids + q0 * k, o.scores + q0 * k, s);
+    stage_mark(idx, s);
+    CHIMERA_HIP(hipGetLastError());
+  }
+  CHIMERA_HIP(hipEventRecord(idx->scratch_done, s));
+  idx->scratch_pending = true;
+  if (stop == STOP_CANDIDATES) {
+    std::vector<int64_t> offs(nq + 1, 0);
+    for (int64_t i = 0; i < nq; ++i) offs[i + 1] = offs[i] + host_counts[i];
+    CHIMERA_HIP(hipMemcpyAsync(o.offsets, offs.data(), (nq + 1) * 8, hipMemcpyHostToDevice, s));
+    CHIMERA_HIP(hipStreamSynchronize(s));
+    if (offs[nq] > o.capacity)
+      return fail(CHIMERA_E_INVAL, "candidate sets hold %lld ids, capacity is %lld", (long long)offs[nq],
+                  (long long)o.capacity);
+  }
+  return CHIMERA_OK;
+}
+
+}  // namespace chimera
+
+using namespace chimera;
+
+extern "C" {
+
+const char *chimera_last_error(void) { return g_err; }
+
+int chimera_builder_upload(const chimera_builder *b, int hip_device, chimera_index **out) {
+  if (!b || !out) return fail(CHIMERA_E_INVAL, "null argument");
+  const HostIndex *h = builder_host(b);
+  if (h->weights.empty()) return fail(CHIMERA_E_INVAL, "quantiser not frozen");
+  return upload(*h, hip_device, out);
+}
+
+int chimera_index_load(const char *path, int hip_device, chimera_index **out) {
+  if (!path || !out) return fail(CHIMERA_E_INVAL, "null argument");
+  HostIndex h;
+  int rc = load_index(path, h);
+  if (rc) return rc;
+  return upload(h, hip_device, out);
+}
+
+void chimera_index_free(chimera_index *idx) {
+  if (!idx) return;
+  DeviceGuard dg(idx->device);
+  (void)hipDeviceSynchronize();
+  void *ptrs[] = {idx->d_cent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->d_ivf_off, idx->d_ivf_doc, idx->scratch};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  if (idx->scratch_done) (void)hipEventDestroy(idx->scratch_done);
+  for (hipEvent_t e : idx->ev) (void)hipEventDestroy(e);
+  delete idx;
+}
+
+int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out) {
+  if (!idx || !out) return fail(CHIMERA_E_INVAL, "null argument");
+  out->ndocs = idx->ndocs; out->ntokens = idx->ntok; out->nnz = idx->nnz; out->ncent = idx->ncent;
+  out->dim = idx->dim; out->nbits = idx->nbits; out->max_doc_len = idx->max_doc_len;
+  out->device_bytes = idx->device_bytes; out->device = idx->device;
+  return CHIMERA_OK;
+}
+
+int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
+                   int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  if (rc) return rc;
+  if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
+  if (ncand < k) return fail(CHIMERA_E_INVAL, "ncand (%d) must be >= k (%d)", ncand, k);
+  if (k > kMaxK) return fail(CHIMERA_E_UNSUPPORTED, "k %d > %d", k, kMaxK);
+  if (ncand > CHIMERA_MAX_NCAND) return fail(CHIMERA_E_UNSUPPORTED, "ncand %d > %d", ncand, CHIMERA_MAX_NCAND);
+  if (nq > 0 && (!ids || !scores)) return fail(CHIMERA_E_INVAL, "null output pointer");
+  if (nq == 0) return CHIMERA_OK;
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  int nc = (int)std::min<int64_t>(ncand, idx->ndocs);
+  Outs o;
+  o.ids = ids;
+  o.scores = scores;
+  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream);
+}
+
+int chimera_probe(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
+                  int32_t *cent_ids, int32_t *cent_keys, void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  if (rc) return rc;
+  if (nq > 0 && (!cent_ids || !cent_keys)) return fail(CHIMERA_E_INVAL, "null output pointer");
+  if (nq == 0) return CHIMERA_OK;
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  Outs o;
+  o.cent_ids = cent_ids;
+  o.cent_keys = cent_keys;
+  return run(idx, Q, q_dtype, nq, Tq, nprobe, 1, 1, STOP_PROBE, o, (hipStream_t)hip_stream);
+}
+
+int chimera_candidates(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                       int32_t nprobe, int64_t *offsets, int32_t *doc_ids, int64_t capacity, void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  if (rc) return rc;
+  if (!offsets || (capacity > 0 && !doc_ids) || capacity < 0) return fail(CHIMERA_E_INVAL, "bad output arguments");
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  if (nq == 0) {
+    int64_t z = 0;
+    CHIMERA_HIP(hipMemcpy(offsets, &z, 8, hipMemcpyHostToDevice));
+    return CHIMERA_OK;
+  }
+  Outs o;
+  o.offsets = offsets;
+  o.doc_ids = doc_ids;
+  o.capacity = capacity;
+  return run(idx, Q, q_dtype, nq, Tq, nprobe, 1, 1, STOP_CANDIDATES, o, (hipStream_t)hip_stream);
+}
+
+int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
+                  int32_t ncand, int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  if (rc) return rc;
+  if (ncand < 1) return fail(CHIMERA_E_INVAL, "ncand must be >= 1");
+  if (ncand > CHIMERA_MAX_NCAND) return fail(CHIMERA_E_UNSUPPORTED, "ncand %d > %d", ncand, CHIMERA_MAX_NCAND);
+  if (nq > 0 && (!cand_ids || !cand_keys || !n_valid)) return fail(CHIMERA_E_INVAL, "null output pointer");
+  if (nq == 0) return CHIMERA_OK;
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  int nc = (int)std::min<int64_t>(ncand, idx->ndocs);
+  if (nc == 0) return fail(CHIMERA_E_INVAL, "index has no documents");
+  Outs o;
+  o.cand_ids = cand_ids;
+  o.cand_keys = cand_keys;
+  o.n_valid = n_valid;
+  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_PRUNE, o, (hipStream_t)hip_stream);
+}
+
+int chimera_stage_times(const chimera_index *idx, float *ms6) {
+  if (!idx || !ms6) return fail(CHIMERA_E_INVAL, "null argument");
+  if (!idx->timing) return fail(CHIMERA_E_INVAL, "stage timing is off (set CHIMERA_STAGE_TIMING=1 before load)");
+  for (int i = 0; i < 6; ++i) ms6[i] = 0.f;
+  // events per full sub-batch: round, probe, walk, select, score, topk, end
+  const int per = 7;
+  if (idx->ev_used % per != 0 || idx->ev_used == 0) return fail(CHIMERA_E_INVAL, "no full search recorded");
+  CHIMERA_HIP(hipEventSynchronize(idx->ev[idx->ev_used - 1]));
+  for (int b = 0; b + per <= idx->ev_used; b += per)
+    for (int i = 0; i < 6; ++i) {
+      float ms = 0.f;
+      CHIMERA_HIP(hipEventElapsedTime(&ms, idx->ev[b + i], idx->ev[b + i + 1]));
+      ms6[i] += ms;
+    }
+  return CHIMERA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+// internal.h - shared declarations of the gfx950 query-path library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/chimera.h"
+
+namespace chimera {
+
+// ---- errors -------------------------------------------------------------
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int hip_fail(hipError_t e, const char *what);
+#define CHIMERA_HIP(call)                                   \
+  do {                                                      \
+    hipError_t e_ = (call);                                 \
+    if (e_ != hipSuccess) return ::chimera::hip_fail(e_, #call); \
+  } while (0)
+
+// ---- value grid (host side) ----------------------------------------------
+// Nearest multiple of max(2^-11, bf16 spacing), ties to even, of a bf16 or
+// float value; returned as the integer k = x * 2^11.
+int32_t grid_k_of_float(float x);
+uint16_t bf16_of_grid_k(int32_t k);
+float float_of_bf16(uint16_t b);
+
+// ---- host index (what the builder produces and the file stores) ---------
+struct HostIndex {
+  int32_t ncent = 0, dim = 0, nbits = 0, max_doc_len = 0;
+  int64_t ndocs = 0, ntok = 0, nnz = 0;
+  std::vector<uint16_t> cent;     // bf16 [ncent][dim]
+  std::vector<int64_t> doc_off;   // [ndocs+1]
+  std::vector<int32_t> cid;       // [ntok]
+  std::vector<uint8_t> codes;     // [ntok][dim*nbits/8]
+  std::vector<int32_t> cut_k;     // [2^nbits - 1]
+  std::vector<uint16_t> weights;  // bf16 [2^nbits]
+  std::vector<int64_t> ivf_off;   // [ncent+1]
+  std::vector<int32_t> ivf_doc;   // [nnz]
+  int64_t code_bytes() const { return (int64_t)dim * nbits / 8; }
+};
+
+int save_index(const HostIndex &h, const char *path);
+const HostIndex *builder_host(const chimera_builder *b);  // builds the lists on first use
+int load_index(const char *path, HostIndex &h);
+
+// ---- kernel launchers (one translation unit per pipeline step) -----------
+// Rounds Q [nq][Tq][128] (f32 or bf16) onto the grid as bf16, padding each
+// query to TQP rows with zeros: Qs [nq][TQP][128].
+void launch_round_queries(const void *Q, int q_dtype, int64_t nq, int Tq, int TQP, uint16_t *Qs,
+                          hipStream_t s);
+
+// Probe: S = Qs * cent^T on MFMA, top-nprobe per row.  rows = nq*TQP.
+// part: [nsplit][rows][pmax] u64 partial lists.  ST (optional): [nq][ncent][TQP] f32.
+struct ProbePlan {
+  int pmax = 0, nsplit = 0, tiles_per_split = 0;
+};
+ProbePlan plan_probe(int64_t rows, int ncent, int nprobe);
+size_t probe_part_bytes(const ProbePlan &p, int64_t rows);
+void launch_probe(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent,
+                  const ProbePlan &p, uint64_t *part, float *ST, hipStream_t s);
+// Merge partial lists into cent_ids/cent_keys [nq][TQP][nprobe] (rows j < Tq).
+void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const ProbePlan &p, int nprobe,
+                        int32_t *cent_ids, int32_t *cent_keys, hipStream_t s);
+
+// Candidate walk: mask [nq][ndocs] (u32 words when TQP == 32, u64 when 64),
+// fp [nq][ndocs] i32; both must be zero on entry.
+void launch_fill_zero(void *p, size_t bytes, hipStream_t s);
+void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
+                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, void *mask,
+                      int32_t *fp, hipStream_t s);
+
+// Refinement select: per query, the ncand best of {V : mask != 0} by
+// (fp desc, V asc), written in ascending V order; n_valid [nq].
+void launch_select(const void *mask, const int32_t *fp, int64_t nq, int TQP, int64_t ndocs, int ncand,
+                   int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s);
+// Candidate-set tap: counts [nq] of {V : mask != 0}; then ordered ids.
+void launch_count_hits(const void *mask, int64_t nq, int TQP, int64_t ndocs, int64_t *counts, hipStream_t s);
+void launch_list_hits(const void *mask, int64_t nq, int TQP, int64_t ndocs, const int64_t *offsets,
+                      int32_t *doc_ids, hipStream_t s);
+
+// Residual scoring: fhat [nq][ncand] i32 keys of the kept documents.
+void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,
+                           const int64_t *doc_off, const int32_t *cid, const uint8_t *codes, int nbits,
+                           const uint16_t *weights_host, const int32_t *cand_ids, const int32_t *n_valid,
+                           int ncand, int32_t *fhat, hipStream_t s);
+
+// Final top-k: ids/scores [nq][k].
+void launch_topk(const int32_t *fhat, const int32_t *cand_ids, const int32_t *n_valid, int64_t nq, int ncand,
+                 int k, int32_t *ids, float *scores, hipStream_t s);
+
+}  // namespace chimera
+
+// ---- the opaque handle -----------------------------------------------------
+struct chimera_index {
+  int device = 0;
+  int32_t ncent = 0, dim = 0, nbits = 0, max_doc_len = 0;
+  int64_t ndocs = 0, ntok = 0, nnz = 0;
+  int64_t device_bytes = 0;
+  uint16_t *d_cent = nullptr;
+  int64_t *d_doc_off = nullptr;
+  int32_t *d_cid = nullptr;
+  uint8_t *d_codes = nullptr;
+  int64_t *d_ivf_off = nullptr;
+  int32_t *d_ivf_doc = nullptr;
+  uint16_t h_weights[16] = {0};
+  int32_t h_cut[15] = {0};
+  // scratch arena, grown on demand, ordered across streams by scratch_done
+  void *scratch = nullptr;
+  size_t scratch_bytes = 0;
+  hipEvent_t scratch_done = nullptr;
+  bool scratch_pending = false;
+  std::atomic<int> busy{0};
+  // per-stage timing
+  bool timing = false;
+  std::vector<hipEvent_t> ev;  // 7 events per sub-batch
+  int ev_used = 0;
+};

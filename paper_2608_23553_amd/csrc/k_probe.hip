@@ -1,0 +1,240 @@
+// k_probe.hip - query rounding, query-token x centroid scores on MFMA and
+// top-nprobe centroid selection (Sec. 2.3: a query vector is compared with
+// all centroids and the top-n_probe clusters are kept; Sec. 3.2 candidate
+// generation, the lists C_q).
+//
+// S = Q C^T is the one dense contraction of the path: [rows,128] x [128,ncent]
+// in bf16 with fp32 accumulation.  On the value grid every product and partial
+// sum is an exact multiple of 2^-22 well inside fp32's 24-bit significand, so
+// the MFMA result is exact whatever its internal summation order, and the
+// selected ids are bit-exact.  S is never materialised for selection: each
+// lane keeps a running sorted list of its best (score, id) keys.
+#include "device_common.h"
+#include "internal.h"
+
+namespace chimera {
+
+// ------------------------------------------------------------ rounding
+__global__ __launch_bounds__(256) void k_round_queries(const void *__restrict__ Q, int q_dtype, int64_t nq, int Tq,
+                                                       int TQP, uint16_t *__restrict__ Qs) {
+  const int64_t total = nq * TQP * 128;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = e >> 7;
+    const int d = (int)(e & 127);
+    const int64_t q = row / TQP;
+    const int j = (int)(row - q * TQP);
+    uint16_t out = 0;
+    if (j < Tq) {
+      const int64_t src = (q * Tq + j) * 128 + d;
+      float x = q_dtype == CHIMERA_F32 ? ((const float *)Q)[src]
+                                       : __uint_as_float((uint32_t)((const uint16_t *)Q)[src] << 16);
+      out = grid_bf16_bits(x);
+    }
+    Qs[e] = out;
+  }
+}
+
+void launch_round_queries(const void *Q, int q_dtype, int64_t nq, int Tq, int TQP, uint16_t *Qs, hipStream_t s) {
+  const int64_t total = nq * TQP * 128;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65535 * 8) blocks = 65535 * 8;
+  if (blocks < 1) return;
+  hipLaunchKernelGGL(k_round_queries, dim3((unsigned)blocks), dim3(256), 0, s, Q, q_dtype, nq, Tq, TQP, Qs);
+}
+
+// --------------------------------------------------------------- probe
+// Insert K into L (sorted descending), dropping the smallest.
+template <int P>
+__device__ __forceinline__ void insert_desc(uint64_t (&L)[P], uint64_t K) {
+#pragma unroll
+  for (int i = 0; i < P; ++i) {
+    const uint64_t a = L[i];
+    const bool gt = K > a;
+    L[i] = gt ? K : a;
+    K = gt ? a : K;
+  }
+}
+
+// One workgroup: 32 query rows (one column block) x a range of centroid tiles.
+// Four waves stride over 32-centroid tiles; each wave computes a 32x32 tile
+// of S^T (rows = centroids, cols = query rows) with 8 MFMA 32x32x16 steps.
+// The contraction index k of MFMA step s, lane half h, element i is
+// dimension 64h + 8s + i for both operands (any common permutation of the
+// 128 dimensions gives the same exact sum), so every lane loads 128
+// contiguous bytes of its centroid row and of its query row.
+template <int PMAX, bool WRITE_ST>
+__global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, int TQP,
+                                               const uint16_t *__restrict__ cent, int ncent, int tiles_per_split,
+                                               int64_t rows, uint64_t *__restrict__ part, float *__restrict__ ST) {
+  __shared__ uint64_t lds[3][32][PMAX];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 31, h = lane >> 5;
+  const int64_t qrow = (int64_t)blockIdx.x * 32 + col;
+  const int split = blockIdx.y;
+
+  bf16x8 bq[8];
+  {
+    const uint4 *qp = (const uint4 *)(Qs + qrow * 128 + 64 * h);
+#pragma unroll
+    for (int s = 0; s < 8; ++s) bq[s] = as_bf16x8(qp[s]);
+  }
+  uint64_t L[PMAX];
+#pragma unroll
+  for (int i = 0; i < PMAX; ++i) L[i] = 0;  // every real key is > 0
+
+  const int ntiles = (ncent + 31) >> 5;
+  const int t0 = split * tiles_per_split;
+  const int t1 = min(ntiles, t0 + tiles_per_split);
+  const int64_t st_base = (qrow / TQP) * (int64_t)ncent * TQP + (qrow % TQP);
+
+  for (int t = t0 + wave; t < t1; t += 4) {
+    const int crow = t * 32 + col;
+    bf16x8 a[8];
+    if (crow < ncent) {
+      const uint4 *cp = (const uint4 *)(cent + (int64_t)crow * 128 + 64 * h);
+#pragma unroll
+      for (int s = 0; s < 8; ++s) a[s] = as_bf16x8(cp[s]);
+    } else {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) a[s] = as_bf16x8(make_uint4(0, 0, 0, 0));
+    }
+    f32x16 acc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], bq[s], acc, 0, 0, 0);
+    // D layout: lane (col, h), register v holds centroid 8(v/4) + 4h + v%4 of the tile
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int c = t * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+      if (c < ncent) {
+        if (WRITE_ST) ST[st_base + (int64_t)c * TQP] = acc[v];
+        const uint64_t K = pack_key(to_key(acc[v]), (uint32_t)c);
+        if (K > L[PMAX - 1]) insert_desc<PMAX>(L, K);
+      }
+    }
+  }
+  // lanes h=1 hand their lists to lanes h=0 (same query row)
+#pragma unroll
+  for (int i = 0; i < PMAX; ++i) {
+    const uint64_t K = shfl_xor_u64(L[i], 32);
+    if (h == 0 && K > L[PMAX - 1]) insert_desc<PMAX>(L, K);
+  }
+  if (wave > 0 && h == 0) {
+#pragma unroll
+    for (int i = 0; i < PMAX; ++i) lds[wave - 1][col][i] = L[i];
+  }
+  __syncthreads();
+  if (wave == 0 && h == 0) {
+    for (int w = 0; w < 3; ++w)
+      for (int i = 0; i < PMAX; ++i) {
+        const uint64_t K = lds[w][col][i];
+        if (K <= L[PMAX - 1]) break;  // the source list is sorted
+        insert_desc<PMAX>(L, K);
+      }
+    uint64_t *out = part + ((int64_t)split * rows + qrow) * PMAX;
+#pragma unroll
+    for (int i = 0; i < PMAX; ++i) out[i] = L[i];
+  }
+}
+
+ProbePlan plan_probe(int64_t rows, int ncent, int nprobe) {
+  ProbePlan p;
+  p.pmax = nprobe <= 8 ? 8 : nprobe <= 16 ? 16 : nprobe <= 32 ? 32 : 64;
+  const int ntiles = (ncent + 31) / 32;
+  const int64_t ncb = rows / 32;
+  // aim at ~2048 workgroups, at least 4 tiles (one per wave) per split
+  int64_t want = (2048 + ncb - 1) / ncb;
+  int64_t maxsplit = (ntiles + 3) / 4;
+  int64_t ns = want < 1 ? 1 : want;
+  if (ns > maxsplit) ns = maxsplit;
+  if (ns > 65535) ns = 65535;
+  p.tiles_per_split = (int)((ntiles + ns - 1) / ns);
+  p.nsplit = (ntiles + p.tiles_per_split - 1) / p.tiles_per_split;
+  return p;
+}
+
+size_t probe_part_bytes(const ProbePlan &p, int64_t rows) { return (size_t)p.nsplit * rows * p.pmax * 8; }
+
+template <int P>
+static void launch_probe_t(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent,
+                           const ProbePlan &p, uint64_t *part, float *ST, hipStream_t s) {
+  dim3 grid((unsigned)(rows / 32), (unsigned)p.nsplit);
+  if (ST)
+    hipLaunchKernelGGL((k_probe<P, true>), grid, dim3(256), 0, s, Qs, TQP, cent, ncent, p.tiles_per_split, rows, part, ST);
+  else
+    hipLaunchKernelGGL((k_probe<P, false>), grid, dim3(256), 0, s, Qs, TQP, cent, ncent, p.tiles_per_split, rows, part,
+                       ST);
+}
+
+void launch_probe(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent, const ProbePlan &p,
+                  uint64_t *part, float *ST, hipStream_t s) {
+  switch (p.pmax) {
+    case 8: launch_probe_t<8>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 16: launch_probe_t<16>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 32: launch_probe_t<32>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    default: launch_probe_t<64>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+  }
+}
+
+// --------------------------------------------------------------- merge
+// One wave per query row: each lane folds the sorted partial lists of splits
+// lane, lane+64, ... into its own list; then nprobe rounds of a wave-wide
+// maximum pop the winners in order.
+template <int PMAX>
+__global__ __launch_bounds__(256) void k_probe_merge(const uint64_t *__restrict__ part, int64_t nq, int Tq, int TQP,
+                                                     int nsplit, int nprobe, int32_t *__restrict__ cent_ids,
+                                                     int32_t *__restrict__ cent_keys) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wrow = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // over nq*Tq valid rows
+  if (wrow >= nq * Tq) return;
+  const int64_t q = wrow / Tq;
+  const int j = (int)(wrow - q * Tq);
+  const int64_t row = q * TQP + j;
+  const int64_t rows = nq * TQP;
+  uint64_t L[PMAX];
+#pragma unroll
+  for (int i = 0; i < PMAX; ++i) L[i] = 0;
+  for (int sp = lane; sp < nsplit; sp += 64) {
+    const uint64_t *src = part + ((int64_t)sp * rows + row) * PMAX;
+    for (int i = 0; i < PMAX; ++i) {
+      const uint64_t K = src[i];
+      if (K <= L[PMAX - 1]) break;
+      insert_desc<PMAX>(L, K);
+    }
+  }
+  int32_t *oi = cent_ids + row * nprobe;
+  int32_t *ok = cent_keys + row * nprobe;
+  for (int r = 0; r < nprobe; ++r) {
+    uint64_t best = L[0];
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const uint64_t o = shfl_xor_u64(best, m);
+      best = o > best ? o : best;
+    }
+    // keys are unique (distinct ids), so exactly one lane owns the winner
+    if (L[0] == best) {
+#pragma unroll
+      for (int i = 0; i < PMAX - 1; ++i) L[i] = L[i + 1];
+      L[PMAX - 1] = 0;
+    }
+    if (lane == 0) {
+      oi[r] = (int32_t)key_id(best);
+      ok[r] = key_score(best);
+    }
+  }
+}
+
+void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const ProbePlan &p, int nprobe,
+                        int32_t *cent_ids, int32_t *cent_keys, hipStream_t s) {
+  const int64_t nrows = nq * Tq;
+  dim3 grid((unsigned)((nrows + 3) / 4));
+  switch (p.pmax) {
+    case 8: hipLaunchKernelGGL(k_probe_merge<8>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
+    case 16: hipLaunchKernelGGL(k_probe_merge<16>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
+    case 32: hipLaunchKernelGGL(k_probe_merge<32>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
+    default: hipLaunchKernelGGL(k_probe_merge<64>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
+  }
+}
+
+}  // namespace chimera
