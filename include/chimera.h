@@ -199,12 +199,16 @@ int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, in
                   int32_t nprobe, int32_t ncand, int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid,
                   void *hip_stream);
 
-/* Per-stage device time of the last search on this index, in ms, measured
- * with HIP events when the environment variable CHIMERA_STAGE_TIMING=1 was
- * set at load time: [0] query rounding, [1] probe, [2] candidate walk,
- * [3] refinement select, [4] residual scoring, [5] final top-k.  Summed over
- * sub-batches.  E_INVAL if timing is off. */
-int chimera_stage_times(const chimera_index *idx, float *ms6);
+/* Per-stage device time of the searches run on this index since the last
+ * call, in ms, measured with HIP events recorded on the search stream when
+ * the environment variable CHIMERA_STAGE_TIMING=1 was set at load time.
+ * ms7 receives [0] query rounding, [1] probe (GEMM + top-nprobe), [2]
+ * candidate walk, [3] refinement select, [4] residual scoring, [5] final
+ * top-k, each summed over searches and sub-batches, and [6] the number of
+ * sub-batches (one launch of each kernel per sub-batch).  Synchronises on
+ * the last recorded event, then clears the record.  E_INVAL if timing is
+ * off or nothing was recorded. */
+int chimera_stage_times(chimera_index *idx, float *ms7);
 
 #ifdef __cplusplus
 }

@@ -286,6 +286,8 @@ class Index:
         return cand, keys, nval
 
     def stage_times(self) -> np.ndarray:
-        ms = np.zeros(6, np.float32)
+        """[round, probe, walk, select, score, topk] ms summed since the last
+        call, then the number of sub-batches (see chimera_stage_times)."""
+        ms = np.zeros(7, np.float32)
         _check(lib().chimera_stage_times(self._h, _np(ms)))
         return ms

@@ -75,9 +75,15 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
     delete idx;
     return fail(CHIMERA_E_NOMEM, "index needs %zu bytes, %zu free on device %d", need, free_b, device);
   }
+  // Token arrays (cid, codes) are followed by kTokenPad zeroed tokens: the
+  // residual scorer reads whole 16-token tiles and may run up to 15 tokens
+  // past the last document.  Every section gets at least 256 spare bytes.
+  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256};
+  int si = 0;
   for (auto &s : secs) {
-    // one padding byte keeps every section non-empty
-    hipError_t e = hipMalloc(s.dst, s.bytes + 16);
+    const size_t pad = pad_bytes[si++];
+    hipError_t e = hipMalloc(s.dst, s.bytes + pad);
+    if (e == hipSuccess) e = hipMemset((char *)*s.dst + s.bytes, 0, pad);
     if (e == hipSuccess && s.bytes) e = hipMemcpy(*s.dst, s.src, s.bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       int rc = hip_fail(e, "index upload");
@@ -180,8 +186,8 @@ static size_t scratch_budget() {
   return mb << 20;
 }
 
-static void stage_mark(chimera_index *idx, hipStream_t s) {
-  if (!idx->timing) return;
+static void stage_mark(chimera_index *idx, hipStream_t s, bool on) {
+  if (!idx->timing || !on) return;
   if (idx->ev_used >= (int)idx->ev.size()) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return;
@@ -203,7 +209,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
   int rc = ensure_scratch(idx, need);
   if (rc) return rc;
   if (idx->scratch_pending) CHIMERA_HIP(hipStreamWaitEvent(s, idx->scratch_done, 0));
-  idx->ev_used = 0;
+  const bool mark = stop == STOP_FULL;
 
   std::vector<int64_t> host_counts;
   int64_t total_hits = 0;
@@ -223,9 +229,9 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     const size_t qbytes = (size_t)Tq * 128 * (q_dtype == CHIMERA_F32 ? 4 : 2);
     const void *Qb = (const char *)Q + (size_t)q0 * qbytes;
 
-    stage_mark(idx, s);
+    stage_mark(idx, s, mark);
     launch_round_queries(Qb, q_dtype, nb, Tq, TQP, Qs, s);
-    stage_mark(idx, s);
+    stage_mark(idx, s, mark);
     launch_probe(Qs, rows, TQP, idx->d_cent, idx->ncent, plan, part, ST, s);
     launch_probe_merge(part, nb, Tq, TQP, plan, nprobe, ci, ck, s);
     CHIMERA_HIP(hipGetLastError());
@@ -239,9 +245,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     void *mask = cv.take<char>((size_t)nb * idx->ndocs * mask_word);
     int32_t *fp = cv.take<int32_t>((size_t)nb * idx->ndocs);
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
-    stage_mark(idx, s);
-    launch_fill_zero(mask, (size_t)nb * idx->ndocs * mask_word, s);
-    launch_fill_zero(fp, (size_t)nb * idx->ndocs * 4, s);
+    stage_mark(idx, s, mark);
     launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, mask, fp, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_CANDIDATES) {
@@ -269,16 +273,16 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     int32_t *nval = o.n_valid ? o.n_valid + q0 : cv.take<int32_t>((size_t)nb);
     int32_t *fhat = stop >= STOP_FULL ? cv.take<int32_t>((size_t)nb * ncand) : nullptr;
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
-    stage_mark(idx, s);
+    stage_mark(idx, s, mark);
     launch_select(mask, fp, nb, TQP, idx->ndocs, ncand, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
-    stage_mark(idx, s);
+    stage_mark(idx, s, mark);
     launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
                           idx->h_weights, cand, nval, ncand, fhat, s);
-    stage_mark(idx, s);
+    stage_mark(idx, s, mark);
     launch_topk(fhat, cand, nval, nb, ncand, k, o.ids + q0 * k, o.scores + q0 * k, s);
-    stage_mark(idx, s);
+    stage_mark(idx, s, mark);
     CHIMERA_HIP(hipGetLastError());
   }
   CHIMERA_HIP(hipEventRecord(idx->scratch_done, s));
@@ -417,13 +421,13 @@ int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, in
   return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_PRUNE, o, (hipStream_t)hip_stream);
 }
 
-int chimera_stage_times(const chimera_index *idx, float *ms6) {
+int chimera_stage_times(chimera_index *idx, float *ms6) {
   if (!idx || !ms6) return fail(CHIMERA_E_INVAL, "null argument");
   if (!idx->timing) return fail(CHIMERA_E_INVAL, "stage timing is off (set CHIMERA_STAGE_TIMING=1 before load)");
-  for (int i = 0; i < 6; ++i) ms6[i] = 0.f;
-  // events per full sub-batch: round, probe, walk, select, score, topk, end
+  for (int i = 0; i < 7; ++i) ms6[i] = 0.f;
+  // events per sub-batch of a search: round, probe, walk, select, score, top-k, end
   const int per = 7;
-  if (idx->ev_used % per != 0 || idx->ev_used == 0) return fail(CHIMERA_E_INVAL, "no full search recorded");
+  if (idx->ev_used == 0 || idx->ev_used % per != 0) return fail(CHIMERA_E_INVAL, "no search recorded");
   CHIMERA_HIP(hipEventSynchronize(idx->ev[idx->ev_used - 1]));
   for (int b = 0; b + per <= idx->ev_used; b += per)
     for (int i = 0; i < 6; ++i) {
@@ -431,6 +435,8 @@ int chimera_stage_times(const chimera_index *idx, float *ms6) {
       CHIMERA_HIP(hipEventElapsedTime(&ms, idx->ev[b + i], idx->ev[b + i + 1]));
       ms6[i] += ms;
     }
+  ms6[6] = (float)(idx->ev_used / per);
+  idx->ev_used = 0;
   return CHIMERA_OK;
 }
 

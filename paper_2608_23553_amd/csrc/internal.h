@@ -47,6 +47,9 @@ int save_index(const HostIndex &h, const char *path);
 const HostIndex *builder_host(const chimera_builder *b);  // builds the lists on first use
 int load_index(const char *path, HostIndex &h);
 
+// Zeroed tokens appended to the device copies of cid and codes.
+constexpr int kTokenPad = 64;
+
 // ---- kernel launchers (one translation unit per pipeline step) -----------
 // Rounds Q [nq][Tq][128] (f32 or bf16) onto the grid as bf16, padding each
 // query to TQP rows with zeros: Qs [nq][TQP][128].
@@ -67,7 +70,7 @@ void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const
                         int32_t *cent_ids, int32_t *cent_keys, hipStream_t s);
 
 // Candidate walk: mask [nq][ndocs] (u32 words when TQP == 32, u64 when 64),
-// fp [nq][ndocs] i32; both must be zero on entry.
+// fp [nq][ndocs] i32; every entry is written.
 void launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, void *mask,

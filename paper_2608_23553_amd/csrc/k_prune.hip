@@ -9,7 +9,8 @@
 // detects the first hit and one integer atomic add accumulates F'.  Integer
 // atomics make the result independent of scheduling.  This plays the role of
 // the paper's fused atomic aggregation (Sec. 4.2, Alg. 4) with one update
-// per (doc, query token) instead of an atomic max per retrieved token.
+// per (doc, query token) instead of an atomic max per retrieved token, and
+// with the score table held in LDS one document range at a time.
 #include "device_common.h"
 #include "internal.h"
 
@@ -29,45 +30,92 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
   hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, s, (uint4 *)p, n16);
 }
 
-// One workgroup per (query, query token j).
+// Workgroup (query q, doc range [d0, d0 + WALK_RANGE)): the state of the
+// range lives in LDS, so the atomics are LDS atomics and each document's
+// state is written to HBM once.  For each rank r (in order, one barrier per
+// rank) every query token j clips its rank-r posting list to the range by
+// binary search (lists are ascending) and walks the clipped part.  Workgroup
+// b runs on XCD b % 8; all ranges of query q run on XCD q % 8.
+constexpr int WALK_THREADS = 512;
+constexpr int WALK_RANGE = 8192;
+
+__device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a, int64_t lo, int64_t hi, int64_t x) {
+  while (lo < hi) {
+    const int64_t mid = lo + ((hi - lo) >> 1);
+    if ((int64_t)a[mid] < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
 template <typename MaskT>
-__global__ __launch_bounds__(256) void k_cand_walk(const int32_t *__restrict__ cent_ids,
-                                                   const int32_t *__restrict__ cent_keys, int Tq, int TQP, int nprobe,
-                                                   const int64_t *__restrict__ ivf_off,
-                                                   const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
-                                                   MaskT *__restrict__ mask, int32_t *__restrict__ fp) {
-  const int64_t q = blockIdx.x / Tq;
-  const int j = (int)(blockIdx.x - q * Tq);
-  const MaskT bit = (MaskT)1 << j;
-  MaskT *m = mask + q * ndocs;
-  int32_t *f = fp + q * ndocs;
-  const int32_t *ci = cent_ids + (q * TQP + j) * nprobe;
-  const int32_t *ck = cent_keys + (q * TQP + j) * nprobe;
+__global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
+    const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, int64_t nq, int Tq, int TQP,
+    int nprobe, const int64_t *__restrict__ ivf_off, const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
+    int nranges, MaskT *__restrict__ mask, int32_t *__restrict__ fp) {
+  __shared__ MaskT smask[WALK_RANGE];
+  __shared__ int32_t sfp[WALK_RANGE];
+  __shared__ int64_t lo_s[64], hi_s[64];
+  __shared__ int32_t key_s[64];
+  const int b = blockIdx.x;
+  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / nranges);
+  const int range = (b >> 3) % nranges;
+  if (q >= nq) return;
+  const int64_t d0 = (int64_t)range * WALK_RANGE;
+  const int64_t d1 = min(ndocs, d0 + WALK_RANGE);
+  const int nd = (int)(d1 - d0);
+  for (int v = threadIdx.x; v < WALK_RANGE; v += WALK_THREADS) {
+    smask[v] = 0;
+    sfp[v] = 0;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = WALK_THREADS / 64;
   for (int r = 0; r < nprobe; ++r) {
-    const int32_t c = ci[r];
-    const int32_t key = ck[r];
-    if ((uint32_t)c >= (uint32_t)ncent) continue;  // block-uniform; cannot happen for nprobe <= ncent
-    const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
-    for (int64_t p = beg + threadIdx.x; p < end; p += 256) {
-      const int32_t v = ivf_doc[p];
-      const MaskT old = atomicOr(&m[v], bit);
-      if (!(old & bit)) atomicAdd(&f[v], key);
+    if (threadIdx.x < Tq) {
+      const int j = threadIdx.x;
+      const int32_t c = cent_ids[(q * TQP + j) * nprobe + r];
+      int64_t lo = 0, hi = 0;
+      if ((uint32_t)c < (uint32_t)ncent) {
+        const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
+        lo = lower_bound_i32(ivf_doc, beg, end, d0);
+        hi = lower_bound_i32(ivf_doc, lo, end, d1);
+      }
+      lo_s[j] = lo;
+      hi_s[j] = hi;
+      key_s[j] = cent_keys[(q * TQP + j) * nprobe + r];
     }
-    // every OR of rank r has returned before any OR of rank r+1 issues
+    __syncthreads();  // also orders rank r-1's LDS atomics before rank r's
+    for (int j = wave; j < Tq; j += nwaves) {
+      const MaskT bit = (MaskT)1 << j;
+      const int32_t key = key_s[j];
+      const int64_t hi = hi_s[j];
+      for (int64_t p = lo_s[j] + lane; p < hi; p += 64) {
+        const int v = (int)(ivf_doc[p] - d0);
+        const MaskT old = atomicOr(&smask[v], bit);
+        if (!(old & bit)) atomicAdd(&sfp[v], key);
+      }
+    }
     __syncthreads();
+  }
+  MaskT *m = mask + q * ndocs + d0;
+  int32_t *f = fp + q * ndocs + d0;
+  for (int v = threadIdx.x; v < nd; v += WALK_THREADS) {
+    m[v] = smask[v];
+    f[v] = sfp[v];
   }
 }
 
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, void *mask,
                       int32_t *fp, hipStream_t s) {
-  dim3 grid((unsigned)(nq * Tq));
+  const int nranges = (int)((ndocs + WALK_RANGE - 1) / WALK_RANGE);
+  const int64_t blocks = (nq + 7) / 8 * 8 * nranges;
+  if (blocks == 0) return;
   if (TQP == 32)
-    hipLaunchKernelGGL(k_cand_walk<uint32_t>, grid, dim3(256), 0, s, cent_ids, cent_keys, Tq, TQP, nprobe, ivf_off,
-                       ivf_doc, ndocs, ncent, (uint32_t *)mask, fp);
+    hipLaunchKernelGGL(k_cand_walk<uint32_t>, dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s, cent_ids, cent_keys,
+                       nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, (uint32_t *)mask, fp);
   else
-    hipLaunchKernelGGL(k_cand_walk<unsigned long long>, grid, dim3(256), 0, s, cent_ids, cent_keys, Tq, TQP, nprobe,
-                       ivf_off, ivf_doc, ndocs, ncent, (unsigned long long *)mask, fp);
+    hipLaunchKernelGGL(k_cand_walk<unsigned long long>, dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s, cent_ids,
+                       cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges,
+                       (unsigned long long *)mask, fp);
 }
 
 // ------------------------------------------------------- block helpers

@@ -26,18 +26,127 @@ namespace chimera {
 //   B: lane l holds col l%16, contraction slots 8(l/16) .. +7
 //   D: lane l, register v holds row 4(l/16) + v, col l%16
 // Contraction slot (step s, lane group g, element i) is dimension 32g + 8s + i
-// for both operands: group g of the A side reads bytes of dimensions
+// for both operands: group g of the A side reads the bytes of dimensions
 // 32g .. 32g+31 of its token, a contiguous piece of the packed code.
+// Column n of column block cb is query token j = NCB*n + cb, so the NCB
+// S^T values a lane needs for one doc token are adjacent in memory.
+//
+// Work split: a workgroup scores 64 candidates of one query, each wave 16 of
+// them as one flat stream of 16-token tiles.  The loop is software
+// pipelined: while tile t is decoded and multiplied, the centroid ids of
+// tile t+2, the codes of tile t+1 and the S^T rows of tile t+1 (whose
+// addresses need tile t+1's ids) are in flight.  The loop is unrolled by two
+// so that no register that is still being loaded is ever copied.
+//
+// Vector-ALU economy (the kernel is otherwise issue bound): addresses are a
+// wave-uniform 64-bit base (scalar registers) plus a small 32-bit lane
+// offset; loads are never predicated: a tile may read up to 15 tokens past
+// its document, which the index pads at the end of the token arrays, and
+// those rows are masked only in a document's last, partial tile.
+// Workgroup b runs on XCD b % 8; all workgroups of a query are given the
+// same XCD so that the query's S^T table stays in that XCD's L2.
+constexpr int RS_DOCS_PER_BLOCK = 64;
+
+template <int NBITS>
+struct RsCodes {
+  uint32_t w[NBITS == 2 ? 2 : 4];
+};
+struct RsIds {
+  int32_t c[4];
+};
+// Wave-uniform tile cursor: document slot u, first token base, and that
+// document's token offset and length (kept in scalar registers).
+struct RsCur {
+  int u, base, len;
+  int64_t beg;
+};
+
+// Buffer resource (gfx9 family word 3) over [p, p + bytes): loads take a
+// scalar base and a 32-bit lane offset, and read 0 past the range.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rs_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+template <int NBITS, int NCB>
+struct RsWave {
+  static constexpr int TQP = NCB * 16;
+  static constexpr int CB = 16 * NBITS;
+  const uint8_t *__restrict__ codes;
+  const int32_t *__restrict__ cid;
+  __amdgpu_buffer_rsrc_t st_rsrc;
+  int64_t my_beg, beg0;
+  int my_len, ndw, n, g;
+
+  __device__ __forceinline__ void set_doc(RsCur &c, int u) const {
+    c.u = __builtin_amdgcn_readfirstlane(u);
+    c.base = 0;
+    if (c.u < ndw) {
+      c.len = __builtin_amdgcn_readlane(my_len, c.u);
+      const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)my_beg, c.u);
+      const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)my_beg >> 32), c.u);
+      c.beg = (int64_t)(((uint64_t)hi << 32) | lo);
+    } else {
+      c.len = 0;
+      c.beg = beg0;  // past the wave's last tile: read (and ignore) a valid tile
+    }
+  }
+  // next 16-token tile of the wave's document stream
+  __device__ __forceinline__ void advance(RsCur &c) const {
+    if (c.u < ndw) {
+      const int nb = c.base + 16;
+      if (nb >= c.len) set_doc(c, c.u + 1);
+      else c.base = __builtin_amdgcn_readfirstlane(nb);
+    }
+  }
+  __device__ __forceinline__ void load_ids(RsIds &I, const RsCur &c) const {
+    const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + c.beg + c.base, 64);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)(16 * g), 0, 0);
+    I.c[0] = (int32_t)v[0]; I.c[1] = (int32_t)v[1]; I.c[2] = (int32_t)v[2]; I.c[3] = (int32_t)v[3];
+  }
+  __device__ __forceinline__ void load_codes(RsCodes<NBITS> &K, const RsCur &c) const {
+    const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (c.beg + c.base) * CB, 16 * CB);
+    const uint32_t off = (uint32_t)(n * CB + (CB / 4) * g);
+    if (NBITS == 2) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+      K.w[0] = v[0]; K.w[1] = v[1];
+    } else {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+      K.w[0] = v[0]; K.w[1] = v[1]; K.w[2 % (NBITS == 2 ? 2 : 4)] = v[2]; K.w[3 % (NBITS == 2 ? 2 : 4)] = v[3];
+    }
+  }
+  __device__ __forceinline__ void gather(float (&st)[4][NCB], const RsIds &I) const {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const uint32_t off = ((uint32_t)I.c[v] * TQP + NCB * n) * 4;
+      if (NCB == 2) {
+        const auto x = __builtin_amdgcn_raw_buffer_load_b64(st_rsrc, off, 0, 0);
+        st[v][0] = __uint_as_float(x[0]); st[v][1 % NCB] = __uint_as_float(x[1]);
+      } else {
+        const auto x = __builtin_amdgcn_raw_buffer_load_b128(st_rsrc, off, 0, 0);
+        st[v][0] = __uint_as_float(x[0]); st[v][1 % NCB] = __uint_as_float(x[1]);
+        st[v][2 % NCB] = __uint_as_float(x[2]); st[v][3 % NCB] = __uint_as_float(x[3]);
+      }
+    }
+  }
+};
+
 template <int NBITS, int NCB>
 __global__ __launch_bounds__(256) void k_residual_score(
-    const uint16_t *__restrict__ Qs, int Tq, const float *__restrict__ ST, int ncent,
+    const uint16_t *__restrict__ Qs, int64_t nq, int Tq, const float *__restrict__ ST, int ncent,
     const int64_t *__restrict__ doc_off, const int32_t *__restrict__ cid, const uint8_t *__restrict__ codes,
     uint4 w_lo, uint4 w_hi, const int32_t *__restrict__ cand_ids, const int32_t *__restrict__ n_valid, int ncand,
-    int docs_per_block, int32_t *__restrict__ fhat) {
+    int nchunks, int32_t *__restrict__ fhat) {
   constexpr int TQP = NCB * 16;
-  constexpr int CODE_BYTES = 16 * NBITS;  // per token
+  const int b = blockIdx.x;
+  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / nchunks);
+  const int chunk = (b >> 3) % nchunks;
+  if (q >= nq) return;
+  const int nv = n_valid[q];
+  if (chunk * RS_DOCS_PER_BLOCK >= nv) return;  // uniform: before the only barrier
+
   // 2-bit: byte -> 4 weights (two bf16x2 words); 4-bit: byte -> 2 weights
-  __shared__ uint32_t lut[NBITS == 2 ? 512 : 256];
+  __shared__ uint2 lut2[NBITS == 2 ? 256 : 1];
+  __shared__ uint32_t lut4[NBITS == 4 ? 256 : 1];
   {
     const uint16_t w[16] = {
         (uint16_t)w_lo.x, (uint16_t)(w_lo.x >> 16), (uint16_t)w_lo.y, (uint16_t)(w_lo.y >> 16),
@@ -45,110 +154,146 @@ __global__ __launch_bounds__(256) void k_residual_score(
         (uint16_t)w_hi.x, (uint16_t)(w_hi.x >> 16), (uint16_t)w_hi.y, (uint16_t)(w_hi.y >> 16),
         (uint16_t)w_hi.z, (uint16_t)(w_hi.z >> 16), (uint16_t)w_hi.w, (uint16_t)(w_hi.w >> 16)};
     const int e = threadIdx.x;  // 256 threads, one table entry each
-    if (NBITS == 2) {
-      lut[2 * e] = (uint32_t)w[e & 3] | ((uint32_t)w[(e >> 2) & 3] << 16);
-      lut[2 * e + 1] = (uint32_t)w[(e >> 4) & 3] | ((uint32_t)w[(e >> 6) & 3] << 16);
-    } else {
-      lut[e] = (uint32_t)w[e & 15] | ((uint32_t)w[e >> 4] << 16);
-    }
+    if (NBITS == 2)
+      lut2[e] = make_uint2((uint32_t)w[e & 3] | ((uint32_t)w[(e >> 2) & 3] << 16),
+                           (uint32_t)w[(e >> 4) & 3] | ((uint32_t)w[(e >> 6) & 3] << 16));
+    else
+      lut4[e] = (uint32_t)w[e & 15] | ((uint32_t)w[e >> 4] << 16);
   }
   __syncthreads();
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = lane & 15, g = lane >> 4;
-  const int64_t q = blockIdx.y;
-  const int nv = n_valid[q];
-  const int i_end = min(nv, (int)(blockIdx.x + 1) * docs_per_block);
+  // this wave's documents: candidates chunk*64 + wave + 4u, u < 16; lane u holds doc u
+  const int first = chunk * RS_DOCS_PER_BLOCK + wave;
+  const int rem = nv - first;
+  RsWave<NBITS, NCB> W;
+  W.ndw = __builtin_amdgcn_readfirstlane(rem <= 0 ? 0 : min(16, (rem + 3) >> 2));
+  if (W.ndw == 0) return;
+  W.codes = codes;
+  W.cid = cid;
+  W.st_rsrc = rs_rsrc(ST + q * (int64_t)ncent * TQP, (uint32_t)ncent * TQP * 4);
+  W.n = lane & 15;
+  W.g = lane >> 4;
+  W.my_beg = 0;
+  W.my_len = 0;
+  if (lane < W.ndw) {
+    const int32_t V = cand_ids[q * ncand + first + 4 * lane];
+    W.my_beg = doc_off[V];
+    W.my_len = (int)(doc_off[V + 1] - W.my_beg);
+  }
+  {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)W.my_beg, 0);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)W.my_beg >> 32), 0);
+    W.beg0 = (int64_t)(((uint64_t)hi << 32) | lo);
+  }
+  const int n = W.n, g = W.g;
 
   bf16x8 bq[NCB][4];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
-    const uint4 *qp = (const uint4 *)(Qs + ((q * TQP) + 16 * cb + n) * 128 + 32 * g);
+    const uint4 *qp = (const uint4 *)(Qs + ((q * TQP) + NCB * n + cb) * 128 + 32 * g);
 #pragma unroll
     for (int s = 0; s < 4; ++s) bq[cb][s] = as_bf16x8(qp[s]);
   }
-  const float *STq = ST + q * (int64_t)ncent * TQP;
 
-  for (int i = blockIdx.x * docs_per_block + wave; i < i_end; i += 4) {
-    const int32_t V = cand_ids[q * ncand + i];
-    const int64_t t0 = doc_off[V];
-    const int len = (int)(doc_off[V + 1] - t0);
-    float mx[NCB];
+  // cursors of tiles t (c), t+1 (nx) and t+2 (m)
+  RsCur cc, nx, mm;
+  W.set_doc(cc, 0);
+  nx = cc;
+  W.advance(nx);
+  mm = nx;
+  W.advance(mm);
+
+  RsIds id0, id1;          // ids of tiles t+1 and t+2 (ring of 2)
+  RsCodes<NBITS> k0, k1;   // codes of tiles t and t+1 (ring of 2)
+  float st0[4][NCB], st1[4][NCB];  // S^T rows of tiles t and t+1 (ring of 2)
+  {
+    RsIds idc;
+    W.load_ids(idc, cc);
+    W.load_codes(k0, cc);
+    W.load_ids(id0, nx);
+    W.gather(st0, idc);
+  }
+
+  float mx[NCB];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) mx[cb] = -INFINITY;
+  for (int cb = 0; cb < NCB; ++cb) mx[cb] = -INFINITY;
 
-    for (int base = 0; base < len; base += 16) {
-      // ---- A operand: token base + n, dimensions 32g .. 32g+31
-      const int tA = base + n;
-      uint32_t cw[NBITS == 2 ? 2 : 4];
-      if (tA < len) {
-        const uint8_t *cp = codes + (t0 + tA) * CODE_BYTES + (CODE_BYTES / 4) * g;
-        if (NBITS == 2) {
-          const uint2 v = *(const uint2 *)cp;
-          cw[0] = v.x; cw[1] = v.y;
-        } else {
-          const uint4 v = *(const uint4 *)cp;
-          cw[0] = v.x; cw[1] = v.y; cw[2] = v.z; cw[3] = v.w;
-        }
+  // One pipeline step.  In: kc/stc hold tile t; idn holds the ids of t+1.
+  // Out: kn/stn hold tile t+1; idm holds the ids of t+2.
+  auto step = [&](RsCodes<NBITS> &kc, float (&stc)[4][NCB], RsIds &idn, RsCodes<NBITS> &kn, float (&stn)[4][NCB],
+                  RsIds &idm) {
+    W.load_ids(idm, mm);
+    W.load_codes(kn, nx);
+    W.gather(stn, idn);
+    const int len = cc.len, cbase = cc.base;
+    bf16x8 a[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 u;
+      if (NBITS == 2) {
+        // step s covers code bytes 2s and 2s+1 of this lane's 8 bytes
+        const uint32_t word = kc.w[s >> 1];
+        const uint2 lo = lut2[(word >> (16 * (s & 1))) & 255u];
+        const uint2 hi = lut2[(word >> (16 * (s & 1) + 8)) & 255u];
+        u = make_uint4(lo.x, lo.y, hi.x, hi.y);
       } else {
-#pragma unroll
-        for (int w = 0; w < (NBITS == 2 ? 2 : 4); ++w) cw[w] = 0;
+        // step s covers code bytes 4s .. 4s+3 (word s)
+        const uint32_t word = kc.w[s % (NBITS == 2 ? 2 : 4)];
+        u = make_uint4(lut4[word & 255u], lut4[(word >> 8) & 255u], lut4[(word >> 16) & 255u], lut4[word >> 24]);
       }
-      bf16x8 a[4];
+      a[s] = as_bf16x8(u);
+    }
+    f32x4 acc[NCB];
+    const bool partial = cbase + 16 > len;  // wave-uniform
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        uint4 u;
-        if (NBITS == 2) {
-          // step s covers code bytes 2s and 2s+1 of this lane's 8 bytes
-          const uint32_t word = cw[s >> 1];
-          const uint32_t b0 = (word >> (16 * (s & 1))) & 255u, b1 = (word >> (16 * (s & 1) + 8)) & 255u;
-          u.x = lut[2 * b0]; u.y = lut[2 * b0 + 1];
-          u.z = lut[2 * b1]; u.w = lut[2 * b1 + 1];
-        } else {
-          // step s covers code bytes 4s .. 4s+3 (word s)
-          const uint32_t word = cw[s];
-          u.x = lut[word & 255u]; u.y = lut[(word >> 8) & 255u];
-          u.z = lut[(word >> 16) & 255u]; u.w = lut[word >> 24];
-        }
-        a[s] = as_bf16x8(u);
-      }
-      // ---- accumulator init: S[j][cid(t)] for D rows t = base + 4g + v
-      f32x4 acc[NCB];
+    for (int v = 0; v < 4; ++v) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int tC = base + 4 * g + v;
-        if (tC < len) {
-          const float *row = STq + (int64_t)cid[t0 + tC] * TQP + n;
+      for (int cb = 0; cb < NCB; ++cb) acc[cb][v] = stc[v][cb];
+    }
+    if (partial) {
+      // rows past the document start at -inf and never win the maximum
 #pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) acc[cb][v] = row[16 * cb];
-        } else {
+      for (int v = 0; v < 4; ++v)
+        if (cbase + 4 * g + v >= len)
 #pragma unroll
           for (int cb = 0; cb < NCB; ++cb) acc[cb][v] = -INFINITY;
-        }
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], bq[cb][s], acc[cb], 0, 0, 0);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+      mx[cb] = fmaxf(mx[cb], fmaxf(fmaxf(acc[cb][0], acc[cb][1]), fmaxf(acc[cb][2], acc[cb][3])));
+    if (cbase + 16 >= len) {
+      // last tile of document cu: segmented max across the four lane groups,
+      // then the exact integer sum over query tokens
+      int key = 0;
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) {
+        float m = mx[cb];
+        m = fmaxf(m, shfl_xor(m, 16));
+        m = fmaxf(m, shfl_xor(m, 32));
+        if (NCB * n + cb < Tq) key += to_key(m);
+        mx[cb] = -INFINITY;
       }
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], bq[cb][s], acc[cb], 0, 0, 0);
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-        mx[cb] = fmaxf(mx[cb], fmaxf(fmaxf(acc[cb][0], acc[cb][1]), fmaxf(acc[cb][2], acc[cb][3])));
+      key += shfl_xor(key, 1);
+      key += shfl_xor(key, 2);
+      key += shfl_xor(key, 4);
+      key += shfl_xor(key, 8);
+      if (lane == 0) fhat[q * ncand + first + 4 * cc.u] = key;
     }
-    // segmented max: the four lane groups hold different doc tokens
-    int key = 0;
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      float m = mx[cb];
-      m = fmaxf(m, shfl_xor(m, 16));
-      m = fmaxf(m, shfl_xor(m, 32));
-      if (16 * cb + n < Tq) key += to_key(m);
-    }
-    // sum over query tokens: integer, exact
-    key += shfl_xor(key, 1);
-    key += shfl_xor(key, 2);
-    key += shfl_xor(key, 4);
-    key += shfl_xor(key, 8);
-    if (lane == 0) fhat[q * ncand + i] = key;
+    cc = nx;
+    nx = mm;
+    W.advance(mm);
+  };
+
+  while (true) {
+    step(k0, st0, id0, k1, st1, id1);
+    if (cc.u >= W.ndw) break;
+    step(k1, st1, id1, k0, st0, id0);
+    if (cc.u >= W.ndw) break;
   }
 }
 
@@ -160,12 +305,13 @@ void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, cons
   const int B = 1 << nbits;
   for (int u = 0; u < B; ++u) w[u >> 1] |= (uint32_t)weights_host[u] << (16 * (u & 1));
   const uint4 w_lo = make_uint4(w[0], w[1], w[2], w[3]), w_hi = make_uint4(w[4], w[5], w[6], w[7]);
-  const int docs_per_block = 64;
-  dim3 grid((unsigned)((ncand + docs_per_block - 1) / docs_per_block), (unsigned)nq);
-  if (grid.x == 0) return;
-#define CHIMERA_RS(NB, NC)                                                                                        \
-  hipLaunchKernelGGL((k_residual_score<NB, NC>), grid, dim3(256), 0, s, Qs, Tq, ST, ncent, doc_off, cid, codes, \
-                     w_lo, w_hi, cand_ids, n_valid, ncand, docs_per_block, fhat)
+  const int nchunks = (ncand + RS_DOCS_PER_BLOCK - 1) / RS_DOCS_PER_BLOCK;
+  const int64_t nq8 = (nq + 7) / 8 * 8;
+  const int64_t blocks = nq8 * nchunks;
+  if (blocks == 0) return;
+#define CHIMERA_RS(NB, NC)                                                                                          \
+  hipLaunchKernelGGL((k_residual_score<NB, NC>), dim3((unsigned)blocks), dim3(256), 0, s, Qs, nq, Tq, ST, ncent, \
+                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, nchunks, fhat)
   if (nbits == 2 && TQP == 32) CHIMERA_RS(2, 2);
   else if (nbits == 2) CHIMERA_RS(2, 4);
   else if (TQP == 32) CHIMERA_RS(4, 2);
