@@ -152,8 +152,8 @@ static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int npr
   b += 2 * align_up((size_t)rows * nprobe * 4);                // cent ids / keys
   if (stop >= STOP_FULL) b += align_up((size_t)nb * idx->ncent * TQP * 4);  // S^T
   if (stop >= STOP_CANDIDATES) {
-    b += align_up((size_t)nb * idx->ndocs * (TQP == 32 ? 4 : 8));  // mask
-    b += align_up((size_t)nb * idx->ndocs * 4);                     // F'
+    b += align_up((size_t)nb * idx->ndocs * 4);  // F'
+    b += align_up((size_t)nb * 4096 * 4);        // select histogram
   }
   if (stop == STOP_CANDIDATES) b += align_up((size_t)(nb + 1) * 8);  // counts
   if (stop >= STOP_PRUNE) b += 3 * align_up((size_t)nb * ncand * 4) + align_up((size_t)nb * 4);  // cand, keys, F^, n
@@ -213,7 +213,6 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
 
   std::vector<int64_t> host_counts;
   int64_t total_hits = 0;
-  const size_t mask_word = TQP == 32 ? 4 : 8;
 
   for (int64_t q0 = 0; q0 < nq; q0 += B) {
     const int64_t nb = std::min<int64_t>(B, nq - q0);
@@ -242,16 +241,17 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
                                    (size_t)TQP * nprobe * 4, (size_t)Tq * nprobe * 4, nb, hipMemcpyDeviceToDevice, s));
       continue;
     }
-    void *mask = cv.take<char>((size_t)nb * idx->ndocs * mask_word);
     int32_t *fp = cv.take<int32_t>((size_t)nb * idx->ndocs);
+    uint32_t *hist = cv.take<uint32_t>((size_t)nb * 4096);
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
-    launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, mask, fp, s);
+    launch_fill_zero(hist, (size_t)nb * 4096 * 4, s);
+    launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, fp, hist, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_CANDIDATES) {
       int64_t *cnt = cv.take<int64_t>((size_t)nb + 1);
       if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
-      launch_count_hits(mask, nb, TQP, idx->ndocs, cnt, s);
+      launch_count_hits(fp, nb, idx->ndocs, cnt, s);
       std::vector<int64_t> hc(nb);
       CHIMERA_HIP(hipMemcpyAsync(hc.data(), cnt, nb * 8, hipMemcpyDeviceToHost, s));
       CHIMERA_HIP(hipStreamSynchronize(s));
@@ -261,7 +261,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
       bool fits = offs[nb] <= o.capacity;
       if (fits && offs[nb] > total_hits) {
         CHIMERA_HIP(hipMemcpyAsync(cnt, offs.data(), (nb + 1) * 8, hipMemcpyHostToDevice, s));
-        launch_list_hits(mask, nb, TQP, idx->ndocs, cnt, o.doc_ids, s);
+        launch_list_hits(fp, nb, idx->ndocs, cnt, o.doc_ids, s);
         CHIMERA_HIP(hipStreamSynchronize(s));
       }
       for (int64_t i = 0; i < nb; ++i) host_counts.push_back(hc[i]);
@@ -274,7 +274,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     int32_t *fhat = stop >= STOP_FULL ? cv.take<int32_t>((size_t)nb * ncand) : nullptr;
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
-    launch_select(mask, fp, nb, TQP, idx->ndocs, ncand, cand, candk, nval, s);
+    launch_select(fp, hist, nb, idx->ndocs, ncand, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
     stage_mark(idx, s, mark);

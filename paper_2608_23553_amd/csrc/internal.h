@@ -69,21 +69,23 @@ void launch_probe(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cen
 void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const ProbePlan &p, int nprobe,
                         int32_t *cent_ids, int32_t *cent_keys, hipStream_t s);
 
-// Candidate walk: mask [nq][ndocs] (u32 words when TQP == 32, u64 when 64),
-// fp [nq][ndocs] i32; every entry is written.
+// Candidate walk: fp [nq][ndocs] i32 receives F' of every document, or
+// INT32_MIN for documents outside S_Q (every entry is written); hist
+// [nq][4096] u32, zero on entry, receives the histogram of the top 12 bits of
+// F' ^ 0x80000000 over S_Q.
 void launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
-                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, void *mask,
-                      int32_t *fp, hipStream_t s);
+                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
+                      uint32_t *hist, hipStream_t s);
 
-// Refinement select: per query, the ncand best of {V : mask != 0} by
-// (fp desc, V asc), written in ascending V order; n_valid [nq].
-void launch_select(const void *mask, const int32_t *fp, int64_t nq, int TQP, int64_t ndocs, int ncand,
-                   int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s);
-// Candidate-set tap: counts [nq] of {V : mask != 0}; then ordered ids.
-void launch_count_hits(const void *mask, int64_t nq, int TQP, int64_t ndocs, int64_t *counts, hipStream_t s);
-void launch_list_hits(const void *mask, int64_t nq, int TQP, int64_t ndocs, const int64_t *offsets,
-                      int32_t *doc_ids, hipStream_t s);
+// Refinement select: per query, the ncand best of S_Q by (F' desc, V asc),
+// written in ascending V order; n_valid [nq].
+void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, int32_t *cand_ids,
+                   int32_t *cand_keys, int32_t *n_valid, hipStream_t s);
+// Candidate-set tap: counts [nq] of S_Q; then each S_Q in ascending order.
+void launch_count_hits(const int32_t *fp, int64_t nq, int64_t ndocs, int64_t *counts, hipStream_t s);
+void launch_list_hits(const int32_t *fp, int64_t nq, int64_t ndocs, const int64_t *offsets, int32_t *doc_ids,
+                      hipStream_t s);
 
 // Residual scoring: fhat [nq][ncand] i32 keys of the kept documents.
 void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,

@@ -30,14 +30,18 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
   hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, s, (uint4 *)p, n16);
 }
 
-// Workgroup (query q, doc range [d0, d0 + WALK_RANGE)): the state of the
-// range lives in LDS, so the atomics are LDS atomics and each document's
-// state is written to HBM once.  For each rank r (in order, one barrier per
-// rank) every query token j clips its rank-r posting list to the range by
-// binary search (lists are ascending) and walks the clipped part.  Workgroup
-// b runs on XCD b % 8; all ranges of query q run on XCD q % 8.
+// Workgroup (query q, doc range [d0, d0 + R)): the state of the range lives
+// in LDS, so the atomics are LDS atomics and each document's state is
+// written to HBM once.  For each rank r (in order, one barrier per rank)
+// every query token j clips its rank-r posting list to the range by binary
+// search (lists are ascending) and walks the clipped part.  The workgroup
+// then writes F' (or NO_HIT for documents outside S_Q) and adds the range's
+// histogram of the top 12 bits of the order key to the query's histogram,
+// the first pass of the refinement select.  Workgroup b runs on XCD b % 8;
+// all ranges of query q run on XCD q % 8.
 constexpr int WALK_THREADS = 512;
-constexpr int WALK_RANGE = 8192;
+constexpr int NO_HIT = (int)0x80000000;  // F' is never this small
+constexpr int SEL_BINS = 4096;
 
 __device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a, int64_t lo, int64_t hi, int64_t x) {
   while (lo < hi) {
@@ -47,23 +51,27 @@ __device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a
   return lo;
 }
 
-template <typename MaskT>
+// Unsigned order key of a partial score: larger F' <-> larger key.
+__device__ __forceinline__ uint32_t fp_key(int32_t f) { return (uint32_t)f ^ 0x80000000u; }
+
+template <typename MaskT, int R>
 __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, int64_t nq, int Tq, int TQP,
     int nprobe, const int64_t *__restrict__ ivf_off, const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
-    int nranges, MaskT *__restrict__ mask, int32_t *__restrict__ fp) {
-  __shared__ MaskT smask[WALK_RANGE];
-  __shared__ int32_t sfp[WALK_RANGE];
+    int nranges, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
+  static_assert(R * sizeof(MaskT) >= SEL_BINS * 4, "the histogram reuses the mask array");
+  __shared__ MaskT smask[R];
+  __shared__ int32_t sfp[R];
   __shared__ int64_t lo_s[64], hi_s[64];
   __shared__ int32_t key_s[64];
   const int b = blockIdx.x;
   const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / nranges);
   const int range = (b >> 3) % nranges;
   if (q >= nq) return;
-  const int64_t d0 = (int64_t)range * WALK_RANGE;
-  const int64_t d1 = min(ndocs, d0 + WALK_RANGE);
+  const int64_t d0 = (int64_t)range * R;
+  const int64_t d1 = min(ndocs, d0 + R);
   const int nd = (int)(d1 - d0);
-  for (int v = threadIdx.x; v < WALK_RANGE; v += WALK_THREADS) {
+  for (int v = threadIdx.x; v < R; v += WALK_THREADS) {
     smask[v] = 0;
     sfp[v] = 0;
   }
@@ -95,150 +103,189 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     }
     __syncthreads();
   }
-  MaskT *m = mask + q * ndocs + d0;
+  for (int v = threadIdx.x; v < nd; v += WALK_THREADS)
+    if (smask[v] == 0) sfp[v] = NO_HIT;
+  __syncthreads();
+  uint32_t *sh = (uint32_t *)smask;  // the masks are no longer needed
+  for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS) sh[i] = 0;
+  __syncthreads();
   int32_t *f = fp + q * ndocs + d0;
   for (int v = threadIdx.x; v < nd; v += WALK_THREADS) {
-    m[v] = smask[v];
-    f[v] = sfp[v];
+    const int32_t x = sfp[v];
+    f[v] = x;
+    if (x != NO_HIT) atomicAdd(&sh[fp_key(x) >> 20], 1u);
   }
+  __syncthreads();
+  uint32_t *hq = hist + q * SEL_BINS;
+  for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS)
+    if (sh[i]) atomicAdd(&hq[i], sh[i]);
 }
 
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
-                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, void *mask,
-                      int32_t *fp, hipStream_t s) {
-  const int nranges = (int)((ndocs + WALK_RANGE - 1) / WALK_RANGE);
+                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
+                      uint32_t *hist, hipStream_t s) {
+  const int R = TQP == 32 ? 8192 : 4096;
+  const int nranges = (int)((ndocs + R - 1) / R);
   const int64_t blocks = (nq + 7) / 8 * 8 * nranges;
   if (blocks == 0) return;
   if (TQP == 32)
-    hipLaunchKernelGGL(k_cand_walk<uint32_t>, dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s, cent_ids, cent_keys,
-                       nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, (uint32_t *)mask, fp);
+    hipLaunchKernelGGL((k_cand_walk<uint32_t, 8192>), dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s, cent_ids,
+                       cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, fp, hist);
   else
-    hipLaunchKernelGGL(k_cand_walk<unsigned long long>, dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s, cent_ids,
-                       cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges,
-                       (unsigned long long *)mask, fp);
+    hipLaunchKernelGGL((k_cand_walk<unsigned long long, 4096>), dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s,
+                       cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, fp, hist);
 }
 
 // ------------------------------------------------------- block helpers
+constexpr int SEL_THREADS = 1024;
+constexpr int SEL_ITEMS = 4;
+
 // Exclusive prefix sum over the block; thread 0 leaves the block total in
 // *total (shared), readable by every thread once the call returns.
-__device__ __forceinline__ int block_exclusive_scan(int x, int *wsum, int *total) {
+__device__ __forceinline__ long long block_exclusive_scan(long long x, long long *wsum, long long *total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int incl = x;
+  long long incl = x;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const int y = __shfl_up(incl, d, 64);
+    const long long y = __shfl_up(incl, d, 64);
     if (lane >= d) incl += y;
   }
   if (lane == 63) wsum[wave] = incl;
   __syncthreads();
   if (threadIdx.x == 0) {
-    int acc = 0;
+    long long acc = 0;
     for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
-      const int t = wsum[w];
+      const long long t = wsum[w];
       wsum[w] = acc;
       acc += t;
     }
     *total = acc;
   }
   __syncthreads();
-  const int res = wsum[wave] + incl - x;
+  const long long res = wsum[wave] + incl - x;
   __syncthreads();  // wsum is reused by the next call
   return res;
 }
 
-template <typename MaskT>
-__device__ __forceinline__ bool is_hit(const MaskT *m, int64_t v) {
-  return m[v] != 0;
+// Radix-select step: over bins[0..nbins) taken from the highest bin down,
+// find the bin b where the running count reaches rem.  Leaves b in *s_bin
+// and the count of the bins above b in *s_above.
+__device__ __forceinline__ void select_bin(const uint32_t *bins, int nbins, long long rem, long long *wsum,
+                                           long long *s_tot, int *s_bin, long long *s_above) {
+  const int per = (nbins + SEL_THREADS - 1) / SEL_THREADS;
+  const int top = nbins - 1 - threadIdx.x * per;  // this thread's bins: top, top-1, ... (descending)
+  long long local = 0;
+  for (int i = 0; i < per; ++i)
+    if (top - i >= 0) local += bins[top - i];
+  const long long excl = block_exclusive_scan(local, wsum, s_tot);
+  if (excl < rem && excl + local >= rem) {
+    long long cum = excl;
+    for (int i = 0; i < per; ++i) {
+      const int bb = top - i;
+      if (bb < 0) break;
+      if (cum + bins[bb] >= rem) {
+        *s_bin = bb;
+        *s_above = cum;
+        break;
+      }
+      cum += bins[bb];
+    }
+  }
+  __syncthreads();
 }
 
-// Per-query ordered compaction of hits.  mode 0: top-ncand refinement
-// (F' desc, doc asc) written in ascending doc order; mode 1: every hit.
-constexpr int SEL_THREADS = 1024;
-constexpr int SEL_ITEMS = 4;
-
-template <typename MaskT, int MODE>
-__global__ __launch_bounds__(SEL_THREADS) void k_select(const MaskT *__restrict__ mask, const int32_t *__restrict__ fp,
-                                                        int64_t ndocs, int ncand, const int64_t *__restrict__ offsets,
+// Per-query selection of the ncand best hits by (F' desc, doc asc), written
+// in ascending doc order.  The first radix pass (top 12 key bits) comes from
+// the walk's histogram; two more passes over F' (12 and 8 bits) give the
+// exact threshold key T and how many documents with key T to keep (the
+// lowest ids first).  MODE 1 lists every hit at offsets[q] (the candidate-set
+// tap).
+template <int MODE>
+__global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restrict__ fp,
+                                                        const uint32_t *__restrict__ hist1, int64_t ndocs, int ncand,
+                                                        const int64_t *__restrict__ offsets,
                                                         int32_t *__restrict__ out_ids, int32_t *__restrict__ out_keys,
                                                         int32_t *__restrict__ n_valid) {
-  __shared__ int hist[256];
-  __shared__ int wsum[16];
-  __shared__ int s_total;
-  __shared__ long long s_nhit;
-  __shared__ unsigned s_prefix, s_pmask;
-  __shared__ long long s_remaining;
+  __shared__ uint32_t hist[SEL_BINS];
+  __shared__ long long wsum[SEL_THREADS / 64];
+  __shared__ long long s_tot, s_above;
+  __shared__ int s_bin;
   const int64_t q = blockIdx.x;
-  const MaskT *m = mask + q * ndocs;
   const int32_t *f = fp + q * ndocs;
 
-  // --- threshold by radix selection on u = F' ^ 0x80000000 (order-preserving)
-  unsigned T = 0;
-  long long need = 0;  // hits with u == T still to take
+  uint32_t T = 0;
+  long long need = 0;  // hits with key == T still to take
   bool take_all = true;
   if (MODE == 0) {
-    if (threadIdx.x == 0) s_nhit = 0;
-    __syncthreads();
     long long local = 0;
-    for (int64_t v = threadIdx.x; v < ndocs; v += SEL_THREADS) local += is_hit(m, v);
-    atomicAdd((unsigned long long *)&s_nhit, (unsigned long long)local);
-    __syncthreads();
-    take_all = s_nhit <= ncand;
+    for (int i = threadIdx.x; i < SEL_BINS; i += SEL_THREADS) {
+      hist[i] = hist1[q * SEL_BINS + i];
+      local += hist[i];
+    }
+    block_exclusive_scan(local, wsum, &s_tot);
+    const long long nhit = s_tot;
+    take_all = nhit <= ncand;
     if (!take_all) {
-      if (threadIdx.x == 0) { s_prefix = 0; s_pmask = 0; s_remaining = ncand; }
-      for (int pass = 0; pass < 4; ++pass) {
-        const int shift = 24 - 8 * pass;
-        for (int b = threadIdx.x; b < 256; b += SEL_THREADS) hist[b] = 0;
-        __syncthreads();
-        const unsigned prefix = s_prefix, pmask = s_pmask;
-        for (int64_t v = threadIdx.x; v < ndocs; v += SEL_THREADS) {
-          if (!is_hit(m, v)) continue;
-          const unsigned u = (unsigned)f[v] ^ 0x80000000u;
-          if ((u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-          long long rem = s_remaining, cum = 0;
-          int sel = 0;
-          for (int b = 255; b >= 0; --b) {
-            if (cum + hist[b] >= rem) { sel = b; break; }
-            cum += hist[b];
-          }
-          s_remaining = rem - cum;
-          s_prefix = prefix | ((unsigned)sel << shift);
-          s_pmask = pmask | (255u << shift);
-        }
-        __syncthreads();
+      long long rem = ncand;
+      // pass 1 (histogram from the walk): key bits 31..20
+      select_bin(hist, SEL_BINS, rem, wsum, &s_tot, &s_bin, &s_above);
+      const uint32_t b1 = (uint32_t)s_bin;
+      rem -= s_above;
+      // pass 2: key bits 19..8 among keys with top bits b1
+      for (int i = threadIdx.x; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0;
+      __syncthreads();
+      for (int64_t v = threadIdx.x; v < ndocs; v += SEL_THREADS) {
+        const int32_t x = f[v];
+        if (x == NO_HIT) continue;
+        const uint32_t u = fp_key(x);
+        if ((u >> 20) == b1) atomicAdd(&hist[(u >> 8) & 4095u], 1u);
       }
-      T = s_prefix;
-      need = s_remaining;
+      __syncthreads();
+      select_bin(hist, SEL_BINS, rem, wsum, &s_tot, &s_bin, &s_above);
+      const uint32_t p2 = (b1 << 12) | (uint32_t)s_bin;
+      rem -= s_above;
+      // pass 3: key bits 7..0 among keys with top bits p2
+      for (int i = threadIdx.x; i < 256; i += SEL_THREADS) hist[i] = 0;
+      __syncthreads();
+      for (int64_t v = threadIdx.x; v < ndocs; v += SEL_THREADS) {
+        const int32_t x = f[v];
+        if (x == NO_HIT) continue;
+        const uint32_t u = fp_key(x);
+        if ((u >> 8) == p2) atomicAdd(&hist[u & 255u], 1u);
+      }
+      __syncthreads();
+      select_bin(hist, 256, rem, wsum, &s_tot, &s_bin, &s_above);
+      T = (p2 << 8) | (uint32_t)s_bin;
+      need = rem - s_above;
     }
   }
 
   // --- ordered compaction
-  int64_t base_out = MODE == 1 ? offsets[q] : q * (int64_t)ncand;
+  const int64_t base_out = MODE == 1 ? offsets[q] : q * (int64_t)ncand;
   long long written = 0, ties_seen = 0;
   const int64_t chunk = (int64_t)SEL_THREADS * SEL_ITEMS;
   for (int64_t c0 = 0; c0 < ndocs; c0 += chunk) {
     const int64_t v0 = c0 + (int64_t)threadIdx.x * SEL_ITEMS;
     int take_flags = 0, tie_flags = 0, ntie = 0;
+    int32_t xs[SEL_ITEMS];
 #pragma unroll
     for (int i = 0; i < SEL_ITEMS; ++i) {
       const int64_t v = v0 + i;
-      if (v < ndocs && is_hit(m, v)) {
+      xs[i] = v < ndocs ? f[v] : NO_HIT;
+      if (xs[i] != NO_HIT) {
         if (MODE == 1 || take_all) {
           take_flags |= 1 << i;
         } else {
-          const unsigned u = (unsigned)f[v] ^ 0x80000000u;
+          const uint32_t u = fp_key(xs[i]);
           if (u > T) take_flags |= 1 << i;
           else if (u == T) { tie_flags |= 1 << i; ++ntie; }
         }
       }
     }
-    int tie_total = 0;
-    int tie_rank = 0;
+    long long tie_total = 0, tie_rank = 0;
     if (MODE == 0 && !take_all) {
-      tie_rank = block_exclusive_scan(ntie, wsum, &s_total);
-      tie_total = s_total;
+      tie_rank = block_exclusive_scan(ntie, wsum, &s_tot);
+      tie_total = s_tot;
     }
 #pragma unroll
     for (int i = 0; i < SEL_ITEMS; ++i)
@@ -246,22 +293,19 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const MaskT *__restrict_
         if (ties_seen + tie_rank < need) take_flags |= 1 << i;
         ++tie_rank;
       }
-    const int ntake = __popc(take_flags);
-    int pos = block_exclusive_scan(ntake, wsum, &s_total);
-    const int take_total = s_total;
+    long long pos = block_exclusive_scan(__popc(take_flags), wsum, &s_tot);
+    const long long take_total = s_tot;
 #pragma unroll
     for (int i = 0; i < SEL_ITEMS; ++i)
       if (take_flags & (1 << i)) {
-        const int64_t v = v0 + i;
         if (MODE == 1 || written + pos < ncand) {
-          out_ids[base_out + written + pos] = (int32_t)v;
-          if (MODE == 0) out_keys[base_out + written + pos] = f[v];
+          out_ids[base_out + written + pos] = (int32_t)(v0 + i);
+          if (MODE == 0) out_keys[base_out + written + pos] = xs[i];
         }
         ++pos;
       }
     written += take_total;
     ties_seen += tie_total;
-    __syncthreads();
   }
   if (MODE == 0) {
     for (int64_t i = written + threadIdx.x; i < ncand; i += SEL_THREADS) {
@@ -272,50 +316,33 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const MaskT *__restrict_
   }
 }
 
-void launch_select(const void *mask, const int32_t *fp, int64_t nq, int TQP, int64_t ndocs, int ncand,
-                   int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s) {
-  dim3 grid((unsigned)nq);
-  if (TQP == 32)
-    hipLaunchKernelGGL((k_select<uint32_t, 0>), grid, dim3(SEL_THREADS), 0, s, (const uint32_t *)mask, fp, ndocs, ncand,
-                       (const int64_t *)nullptr, cand_ids, cand_keys, n_valid);
-  else
-    hipLaunchKernelGGL((k_select<unsigned long long, 0>), grid, dim3(SEL_THREADS), 0, s,
-                       (const unsigned long long *)mask, fp, ndocs, ncand, (const int64_t *)nullptr, cand_ids,
-                       cand_keys, n_valid);
+void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, int32_t *cand_ids,
+                   int32_t *cand_keys, int32_t *n_valid, hipStream_t s) {
+  hipLaunchKernelGGL((k_select<0>), dim3((unsigned)nq), dim3(SEL_THREADS), 0, s, fp, hist, ndocs, ncand,
+                     (const int64_t *)nullptr, cand_ids, cand_keys, n_valid);
 }
 
-template <typename MaskT>
-__global__ __launch_bounds__(256) void k_count_hits(const MaskT *__restrict__ mask, int64_t ndocs,
+__global__ __launch_bounds__(256) void k_count_hits(const int32_t *__restrict__ fp, int64_t ndocs,
                                                     int64_t *__restrict__ counts) {
   __shared__ unsigned long long acc;
   if (threadIdx.x == 0) acc = 0;
   __syncthreads();
-  const MaskT *m = mask + (int64_t)blockIdx.x * ndocs;
+  const int32_t *f = fp + (int64_t)blockIdx.x * ndocs;
   unsigned long long local = 0;
-  for (int64_t v = threadIdx.x; v < ndocs; v += 256) local += m[v] != 0;
+  for (int64_t v = threadIdx.x; v < ndocs; v += 256) local += f[v] != NO_HIT;
   atomicAdd(&acc, local);
   __syncthreads();
   if (threadIdx.x == 0) counts[blockIdx.x] = (int64_t)acc;
 }
 
-void launch_count_hits(const void *mask, int64_t nq, int TQP, int64_t ndocs, int64_t *counts, hipStream_t s) {
-  if (TQP == 32)
-    hipLaunchKernelGGL(k_count_hits<uint32_t>, dim3((unsigned)nq), dim3(256), 0, s, (const uint32_t *)mask, ndocs, counts);
-  else
-    hipLaunchKernelGGL(k_count_hits<unsigned long long>, dim3((unsigned)nq), dim3(256), 0, s,
-                       (const unsigned long long *)mask, ndocs, counts);
+void launch_count_hits(const int32_t *fp, int64_t nq, int64_t ndocs, int64_t *counts, hipStream_t s) {
+  hipLaunchKernelGGL(k_count_hits, dim3((unsigned)nq), dim3(256), 0, s, fp, ndocs, counts);
 }
 
-void launch_list_hits(const void *mask, int64_t nq, int TQP, int64_t ndocs, const int64_t *offsets, int32_t *doc_ids,
+void launch_list_hits(const int32_t *fp, int64_t nq, int64_t ndocs, const int64_t *offsets, int32_t *doc_ids,
                       hipStream_t s) {
-  dim3 grid((unsigned)nq);
-  if (TQP == 32)
-    hipLaunchKernelGGL((k_select<uint32_t, 1>), grid, dim3(SEL_THREADS), 0, s, (const uint32_t *)mask,
-                       (const int32_t *)nullptr, ndocs, 0, offsets, doc_ids, (int32_t *)nullptr, (int32_t *)nullptr);
-  else
-    hipLaunchKernelGGL((k_select<unsigned long long, 1>), grid, dim3(SEL_THREADS), 0, s,
-                       (const unsigned long long *)mask, (const int32_t *)nullptr, ndocs, 0, offsets, doc_ids,
-                       (int32_t *)nullptr, (int32_t *)nullptr);
+  hipLaunchKernelGGL((k_select<1>), dim3((unsigned)nq), dim3(SEL_THREADS), 0, s, fp, (const uint32_t *)nullptr, ndocs,
+                     0, offsets, doc_ids, (int32_t *)nullptr, (int32_t *)nullptr);
 }
 
 }  // namespace chimera

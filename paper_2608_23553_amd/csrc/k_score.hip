@@ -16,6 +16,8 @@
 // every lane issues one 64- or 128-bit load per 16-token tile.  The maximum
 // over the document's tokens stays in registers and the sum over query
 // tokens is an integer sum of exact keys.
+#include <cstdlib>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -31,8 +33,8 @@ namespace chimera {
 // Column n of column block cb is query token j = NCB*n + cb, so the NCB
 // S^T values a lane needs for one doc token are adjacent in memory.
 //
-// Work split: a workgroup scores 64 candidates of one query, each wave 16 of
-// them as one flat stream of 16-token tiles.  The loop is software
+// Work split: a workgroup scores 4*dpw candidates of one query, each wave dpw
+// (<= 64) of them as one flat stream of 16-token tiles.  The loop is software
 // pipelined: while tile t is decoded and multiplied, the centroid ids of
 // tile t+2, the codes of tile t+1 and the S^T rows of tile t+1 (whose
 // addresses need tile t+1's ids) are in flight.  The loop is unrolled by two
@@ -44,8 +46,11 @@ namespace chimera {
 // its document, which the index pads at the end of the token arrays, and
 // those rows are masked only in a document's last, partial tile.
 // Workgroup b runs on XCD b % 8; all workgroups of a query are given the
-// same XCD so that the query's S^T table stays in that XCD's L2.
-constexpr int RS_DOCS_PER_BLOCK = 64;
+// same XCD, and a query has about as many workgroups as an XCD holds at once,
+// so each XCD works on about one query at a time and that query's S^T table
+// stays in the XCD's L2.  Codes and ids are read once: their loads are marked
+// non-temporal so that they do not evict S^T rows.
+constexpr int RS_NT = 0;  // cache policy: default (non-temporal measured slower)
 
 template <int NBITS>
 struct RsCodes {
@@ -100,17 +105,17 @@ struct RsWave {
   }
   __device__ __forceinline__ void load_ids(RsIds &I, const RsCur &c) const {
     const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + c.beg + c.base, 64);
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)(16 * g), 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)(16 * g), 0, RS_NT);
     I.c[0] = (int32_t)v[0]; I.c[1] = (int32_t)v[1]; I.c[2] = (int32_t)v[2]; I.c[3] = (int32_t)v[3];
   }
   __device__ __forceinline__ void load_codes(RsCodes<NBITS> &K, const RsCur &c) const {
     const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (c.beg + c.base) * CB, 16 * CB);
     const uint32_t off = (uint32_t)(n * CB + (CB / 4) * g);
     if (NBITS == 2) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, RS_NT);
       K.w[0] = v[0]; K.w[1] = v[1];
     } else {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, RS_NT);
       K.w[0] = v[0]; K.w[1] = v[1]; K.w[2 % (NBITS == 2 ? 2 : 4)] = v[2]; K.w[3 % (NBITS == 2 ? 2 : 4)] = v[3];
     }
   }
@@ -135,14 +140,15 @@ __global__ __launch_bounds__(256) void k_residual_score(
     const uint16_t *__restrict__ Qs, int64_t nq, int Tq, const float *__restrict__ ST, int ncent,
     const int64_t *__restrict__ doc_off, const int32_t *__restrict__ cid, const uint8_t *__restrict__ codes,
     uint4 w_lo, uint4 w_hi, const int32_t *__restrict__ cand_ids, const int32_t *__restrict__ n_valid, int ncand,
-    int nchunks, int32_t *__restrict__ fhat) {
+    int nchunks, int dpw, int32_t *__restrict__ fhat) {
   constexpr int TQP = NCB * 16;
+  const int docs_per_block = 4 * dpw;
   const int b = blockIdx.x;
   const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / nchunks);
   const int chunk = (b >> 3) % nchunks;
   if (q >= nq) return;
   const int nv = n_valid[q];
-  if (chunk * RS_DOCS_PER_BLOCK >= nv) return;  // uniform: before the only barrier
+  if (chunk * docs_per_block >= nv) return;  // uniform: before the only barrier
 
   // 2-bit: byte -> 4 weights (two bf16x2 words); 4-bit: byte -> 2 weights
   __shared__ uint2 lut2[NBITS == 2 ? 256 : 1];
@@ -163,11 +169,11 @@ __global__ __launch_bounds__(256) void k_residual_score(
   __syncthreads();
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // this wave's documents: candidates chunk*64 + wave + 4u, u < 16; lane u holds doc u
-  const int first = chunk * RS_DOCS_PER_BLOCK + wave;
+  // this wave's documents: candidates chunk*4*dpw + wave + 4u, u < dpw; lane u holds doc u
+  const int first = chunk * docs_per_block + wave;
   const int rem = nv - first;
   RsWave<NBITS, NCB> W;
-  W.ndw = __builtin_amdgcn_readfirstlane(rem <= 0 ? 0 : min(16, (rem + 3) >> 2));
+  W.ndw = __builtin_amdgcn_readfirstlane(rem <= 0 ? 0 : min(dpw, (rem + 3) >> 2));
   if (W.ndw == 0) return;
   W.codes = codes;
   W.cid = cid;
@@ -305,13 +311,20 @@ void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, cons
   const int B = 1 << nbits;
   for (int u = 0; u < B; ++u) w[u >> 1] |= (uint32_t)weights_host[u] << (16 * (u & 1));
   const uint4 w_lo = make_uint4(w[0], w[1], w[2], w[3]), w_hi = make_uint4(w[4], w[5], w[6], w[7]);
-  const int nchunks = (ncand + RS_DOCS_PER_BLOCK - 1) / RS_DOCS_PER_BLOCK;
+  // documents per wave: about as many workgroups per query as one XCD holds
+  static const int dpw_env = [] {
+    const char *e = std::getenv("CHIMERA_RS_DPW");
+    const int v = e ? std::atoi(e) : 0;
+    return v >= 1 && v <= 64 ? v : 0;
+  }();
+  const int dpw = dpw_env ? dpw_env : 16;
+  const int nchunks = (ncand + 4 * dpw - 1) / (4 * dpw);
   const int64_t nq8 = (nq + 7) / 8 * 8;
   const int64_t blocks = nq8 * nchunks;
   if (blocks == 0) return;
 #define CHIMERA_RS(NB, NC)                                                                                          \
   hipLaunchKernelGGL((k_residual_score<NB, NC>), dim3((unsigned)blocks), dim3(256), 0, s, Qs, nq, Tq, ST, ncent, \
-                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, nchunks, fhat)
+                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, nchunks, dpw, fhat)
   if (nbits == 2 && TQP == 32) CHIMERA_RS(2, 2);
   else if (nbits == 2) CHIMERA_RS(2, 4);
   else if (TQP == 32) CHIMERA_RS(4, 2);
