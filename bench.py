@@ -255,11 +255,11 @@ def main():
         tk, cl = corpus.tokens()
         oi = oracle.OracleIndex(corpus.centroids_k, corpus.doc_off, cl, w.nbits, tok_k=tk)
         del tk
-        probe_n = min(w.nq, 8)
+        probe_n = min(w.nq, max(1, threads))  # one query per thread
         s = time.perf_counter()
         oi.search(q_k[:probe_n], w.nprobe, w.ncand, w.k, nthreads=threads)
         t_probe = time.perf_counter() - s
-        n_cpu = int(min(w.nq, max(probe_n, probe_n * args.cpu_seconds / max(t_probe, 1e-3))))
+        n_cpu = int(min(w.nq, max(probe_n, probe_n * args.cpu_seconds / max(t_probe, 1e-3) // probe_n * probe_n)))
         s = time.perf_counter()
         ref = oi.search(q_k[:n_cpu], w.nprobe, w.ncand, w.k, nthreads=threads)
         t_cpu = time.perf_counter() - s

@@ -16,7 +16,7 @@
 // every lane issues one 64- or 128-bit load per 16-token tile.  The maximum
 // over the document's tokens stays in registers and the sum over query
 // tokens is an integer sum of exact keys.
-#include <cstdlib>
+#include <algorithm>
 
 #include "device_common.h"
 #include "internal.h"
@@ -40,17 +40,20 @@ namespace chimera {
 // addresses need tile t+1's ids) are in flight.  The loop is unrolled by two
 // so that no register that is still being loaded is ever copied.
 //
-// Vector-ALU economy (the kernel is otherwise issue bound): addresses are a
-// wave-uniform 64-bit base (scalar registers) plus a small 32-bit lane
-// offset; loads are never predicated: a tile may read up to 15 tokens past
-// its document, which the index pads at the end of the token arrays, and
-// those rows are masked only in a document's last, partial tile.
-// Workgroup b runs on XCD b % 8; all workgroups of a query are given the
-// same XCD, and a query has about as many workgroups as an XCD holds at once,
-// so each XCD works on about one query at a time and that query's S^T table
-// stays in the XCD's L2.  Codes and ids are read once: their loads are marked
-// non-temporal so that they do not evict S^T rows.
-constexpr int RS_NT = 0;  // cache policy: default (non-temporal measured slower)
+// The limit is the texture address unit: it spends 16 cycles on every 64-lane
+// load of 64 or 128 bits (4 on a 32-bit one), and a tile takes six such loads
+// (ids, codes, four S^T gathers).  Each gather touches only 4 cache lines
+// (four full S^T rows): loads that touch more lines per instruction stall on
+// L1 tag lookups instead.  Addresses are a wave-uniform 64-bit base (scalar
+// registers) plus a small 32-bit lane offset; loads are never predicated: a
+// tile may read up to 15 tokens past its document, which the index pads at
+// the end of the token arrays, and those rows are masked only in a
+// document's last, partial tile.
+// Workgroup b runs on XCD b % 8; with 8 or more queries all workgroups of
+// query q are given XCD q % 8 and queries are issued in order, so an XCD works
+// on a few queries at a time and much of their S^T tables stays in its L2.
+// With fewer than 8 queries, every XCD takes chunks of every query.
+constexpr int RS_CACHE = 0;  // cache policy of every load (default)
 
 template <int NBITS>
 struct RsCodes {
@@ -105,17 +108,17 @@ struct RsWave {
   }
   __device__ __forceinline__ void load_ids(RsIds &I, const RsCur &c) const {
     const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + c.beg + c.base, 64);
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)(16 * g), 0, RS_NT);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)(16 * g), 0, RS_CACHE);
     I.c[0] = (int32_t)v[0]; I.c[1] = (int32_t)v[1]; I.c[2] = (int32_t)v[2]; I.c[3] = (int32_t)v[3];
   }
   __device__ __forceinline__ void load_codes(RsCodes<NBITS> &K, const RsCur &c) const {
     const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (c.beg + c.base) * CB, 16 * CB);
     const uint32_t off = (uint32_t)(n * CB + (CB / 4) * g);
     if (NBITS == 2) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, RS_NT);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, RS_CACHE);
       K.w[0] = v[0]; K.w[1] = v[1];
     } else {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, RS_NT);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, RS_CACHE);
       K.w[0] = v[0]; K.w[1] = v[1]; K.w[2 % (NBITS == 2 ? 2 : 4)] = v[2]; K.w[3 % (NBITS == 2 ? 2 : 4)] = v[3];
     }
   }
@@ -144,8 +147,8 @@ __global__ __launch_bounds__(256) void k_residual_score(
   constexpr int TQP = NCB * 16;
   const int docs_per_block = 4 * dpw;
   const int b = blockIdx.x;
-  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / nchunks);
-  const int chunk = (b >> 3) % nchunks;
+  const int64_t q = nq >= 8 ? (b & 7) + 8 * (int64_t)((b >> 3) / nchunks) : b / nchunks;
+  const int chunk = nq >= 8 ? (b >> 3) % nchunks : b % nchunks;
   if (q >= nq) return;
   const int nv = n_valid[q];
   if (chunk * docs_per_block >= nv) return;  // uniform: before the only barrier
@@ -311,16 +314,11 @@ void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, cons
   const int B = 1 << nbits;
   for (int u = 0; u < B; ++u) w[u >> 1] |= (uint32_t)weights_host[u] << (16 * (u & 1));
   const uint4 w_lo = make_uint4(w[0], w[1], w[2], w[3]), w_hi = make_uint4(w[4], w[5], w[6], w[7]);
-  // documents per wave: about as many workgroups per query as one XCD holds
-  static const int dpw_env = [] {
-    const char *e = std::getenv("CHIMERA_RS_DPW");
-    const int v = e ? std::atoi(e) : 0;
-    return v >= 1 && v <= 64 ? v : 0;
-  }();
-  const int dpw = dpw_env ? dpw_env : 16;
+  // documents per wave: 16, fewer for small batches so that the chip still
+  // gets about 2048 workgroups
+  const int dpw = (int)std::max<int64_t>(1, std::min<int64_t>(16, (int64_t)ncand * nq / (4 * 2048)));
   const int nchunks = (ncand + 4 * dpw - 1) / (4 * dpw);
-  const int64_t nq8 = (nq + 7) / 8 * 8;
-  const int64_t blocks = nq8 * nchunks;
+  const int64_t blocks = (nq >= 8 ? (nq + 7) / 8 * 8 : nq) * nchunks;
   if (blocks == 0) return;
 #define CHIMERA_RS(NB, NC)                                                                                          \
   hipLaunchKernelGGL((k_residual_score<NB, NC>), dim3((unsigned)blocks), dim3(256), 0, s, Qs, nq, Tq, ST, ncent, \
