@@ -150,7 +150,7 @@ static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int npr
   b += align_up((size_t)rows * 128 * 2);                       // Qs
   b += align_up(probe_part_bytes(plan, rows));                 // partial lists
   b += 2 * align_up((size_t)rows * nprobe * 4);                // cent ids / keys
-  if (stop >= STOP_FULL) b += align_up((size_t)nb * idx->ncent * TQP * 4);  // S^T
+  if (stop >= STOP_FULL) b += align_up((size_t)nb * (idx->ncent + 1) * TQP * 4);  // S^T + sentinel rows
   if (stop >= STOP_CANDIDATES) {
     b += align_up((size_t)nb * idx->ndocs * 4);  // F'
     b += align_up((size_t)nb * 4096 * 4);        // select histogram
@@ -223,7 +223,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     uint64_t *part = cv.take<uint64_t>(probe_part_bytes(plan, rows) / 8);
     int32_t *ci = cv.take<int32_t>((size_t)rows * nprobe);
     int32_t *ck = cv.take<int32_t>((size_t)rows * nprobe);
-    float *ST = stop >= STOP_FULL ? cv.take<float>((size_t)nb * idx->ncent * TQP) : nullptr;
+    float *ST = stop >= STOP_FULL ? cv.take<float>((size_t)nb * (idx->ncent + 1) * TQP) : nullptr;
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     const size_t qbytes = (size_t)Tq * 128 * (q_dtype == CHIMERA_F32 ? 4 : 2);
     const void *Qb = (const char *)Q + (size_t)q0 * qbytes;

@@ -88,7 +88,7 @@ void launch_list_hits(const int32_t *fp, int64_t nq, int64_t ndocs, const int64_
                       hipStream_t s);
 
 // Residual scoring: fhat [nq][ncand] i32 keys of the kept documents; ST is
-// [nq][ncent][TQP].
+// [nq][ncent + 1][TQP] (row ncent all -inf).
 void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,
                            const int64_t *doc_off, const int32_t *cid, const uint8_t *codes, int nbits,
                            const uint16_t *weights_host, const int32_t *cand_ids, const int32_t *n_valid,

@@ -85,7 +85,10 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
   const int ntiles = (ncent + 31) >> 5;
   const int t0 = split * tiles_per_split;
   const int t1 = min(ntiles, t0 + tiles_per_split);
-  const int64_t st_base = (qrow / TQP) * (int64_t)ncent * TQP + (qrow % TQP);
+  // S^T of query qrow / TQP has ncent + 1 rows; the last, all -inf, is the
+  // sentinel that the document scorer reads for token slots past a document
+  const int64_t st_base = (qrow / TQP) * (int64_t)(ncent + 1) * TQP + (qrow % TQP);
+  if (WRITE_ST && split == 0 && wave == 0 && h == 0) ST[st_base + (int64_t)ncent * TQP] = -INFINITY;
 
   for (int t = t0 + wave; t < t1; t += 4) {
     const int crow = t * 32 + col;

@@ -7,15 +7,16 @@
 // decoded token c_cid(t) + w[code_t]):
 //     s[j][t] = S[j][cid(t)] + sum_d Q_j[d] * w[code_t[d]]
 // The first term is read from the per-query S^T table written by the probe;
-// the second is a [16 doc tokens x 128] x [128 x Tq] bf16 MFMA product whose
-// doc-token operand is decoded in registers from the packed codes through an
-// LDS lookup table indexed by code byte (the bucket-weight counterpart of the
-// LUT inner product of Sec. 4.1: one lookup yields 4 (2-bit) or 2 (4-bit)
-// bf16 weights).  The S term enters as the MFMA accumulator's initial value.
-// Each document's codes are one contiguous span (document-major layout), so
-// every lane issues one 64- or 128-bit load per 16-token tile.  The maximum
-// over the document's tokens stays in registers and the sum over query
-// tokens is an integer sum of exact keys.
+// the second is a [32 doc tokens x 128] x [128 x 32 query tokens] bf16 MFMA
+// product whose doc-token operand is decoded in registers from the packed
+// codes through an LDS lookup table indexed by code byte (the bucket-weight
+// counterpart of the LUT inner product of Sec. 4.1: one lookup yields 4
+// (2-bit) or 2 (4-bit) bf16 weights).  The S term enters as the MFMA
+// accumulator's initial value.  Each document's codes are one contiguous span
+// (document-major layout).  The maximum over the document's tokens stays in
+// registers and the sum over query tokens is an integer sum of exact keys.
+#include <hip/hip_runtime.h>
+
 #include <algorithm>
 
 #include "device_common.h"
@@ -23,44 +24,51 @@
 
 namespace chimera {
 
-// 16x16x32 MFMA operand layout (A: 16 x 32, B: 32 x 16, D: 16 x 16):
-//   A: lane l holds row l%16, contraction slots 8(l/16) .. +7
-//   B: lane l holds col l%16, contraction slots 8(l/16) .. +7
-//   D: lane l, register v holds row 4(l/16) + v, col l%16
-// Contraction slot (step s, lane group g, element i) is dimension 32g + 8s + i
-// for both operands: group g of the A side reads the bytes of dimensions
-// 32g .. 32g+31 of its token, a contiguous piece of the packed code.
-// Column n of column block cb is query token j = NCB*n + cb, so the NCB
-// S^T values a lane needs for one doc token are adjacent in memory.
+// 32x32x16 MFMA operand layout (A: 32 x 16, B: 16 x 32, D: 32 x 32):
+//   A: lane l holds row l%32, contraction slots 8(l/32) .. +7
+//   B: lane l holds col l%32, contraction slots 8(l/32) .. +7
+//   D: lane l, register v holds row 8(v/4) + 4(l/32) + v%4, col l%32
+// Rows are the 32 doc tokens of a tile, columns query tokens (column block
+// cb: tokens 32cb .. 32cb+31).  Contraction slot (step s, half h, element i)
+// is dimension 64h + 8s + i on both sides, so half h of the doc side decodes
+// one contiguous half of its token's packed code.
 //
-// Work split: a workgroup scores 4*dpw candidates of one query, each wave dpw
-// (<= 64) of them as one flat stream of 16-token tiles.  The loop is software
-// pipelined: while tile t is decoded and multiplied, the centroid ids of
-// tile t+2, the codes of tile t+1 and the S^T rows of tile t+1 (whose
-// addresses need tile t+1's ids) are in flight.  The loop is unrolled by two
-// so that no register that is still being loaded is ever copied.
+// The limit of this kernel is the vector memory front end: the texture
+// address unit spends 4 cycles on a 64-lane 32-bit load and 16 on a 64- or
+// 128-bit one, and one load instruction that touches many cache lines
+// serialises on L1 tag lookups.  The loads are shaped for both:
+//   S^T:   D register v holds two doc tokens (one per half wave) for 32 query
+//          tokens, so its initial value is one 32-bit gather of two full
+//          128-byte S^T rows (2 cache lines, 4 cycles)
+//   codes: one 128-bit load per 32-token tile (the tile's contiguous codes)
+//   ids:   one 32-bit load per tile; lane l reads the id of the row that D
+//          register l%16 holds in its half, so DPP row_newbcast:v hands
+//          every lane the id of its row in register v
 //
-// The limit is the texture address unit: it spends 16 cycles on every 64-lane
-// load of 64 or 128 bits (4 on a 32-bit one), and a tile takes six such loads
-// (ids, codes, four S^T gathers).  Each gather touches only 4 cache lines
-// (four full S^T rows): loads that touch more lines per instruction stall on
-// L1 tag lookups instead.  Addresses are a wave-uniform 64-bit base (scalar
-// registers) plus a small 32-bit lane offset; loads are never predicated: a
-// tile may read up to 15 tokens past its document, which the index pads at
-// the end of the token arrays, and those rows are masked only in a
-// document's last, partial tile.
-// Workgroup b runs on XCD b % 8; with 8 or more queries all workgroups of
-// query q are given XCD q % 8 and queries are issued in order, so an XCD works
-// on a few queries at a time and much of their S^T tables stays in its L2.
-// With fewer than 8 queries, every XCD takes chunks of every query.
-constexpr int RS_CACHE = 0;  // cache policy of every load (default)
+// Work split: a workgroup scores 4 * dpw candidates of one query, each wave
+// dpw contiguous ones.  Workgroup b runs on XCD b % 8; with 8 or more
+// queries, all workgroups of query q are given XCD q % 8 and queries are
+// issued in order, so an XCD works on a few queries at a time and much of
+// their S^T tables stays in its L2.  With fewer than 8 queries, every XCD
+// takes chunks of every query.
+//
+// A wave's documents form one flat stream of 32-token tiles, software
+// pipelined: while tile t is decoded and multiplied, the ids of tile t+2 and
+// the codes and S^T rows of tile t+1 (whose addresses need tile t+1's ids,
+// loaded one step earlier) are in flight.  Registers that are still being
+// loaded alternate between two slots, so the loop is unrolled by two, and it
+// has one exit (exits between the steps make the compiler drain every load
+// in flight at the loop head).
+//
+// Addresses are a wave-uniform 64-bit base (scalar registers) plus a small
+// 32-bit lane offset; loads are never predicated: a tile may read up to 31
+// tokens past its document, which the index pads at the end of the token
+// arrays.  Rows past the document read the S^T sentinel row ncent, which
+// holds -inf, so they never win the maximum.
 
 template <int NBITS>
 struct RsCodes {
-  uint32_t w[NBITS == 2 ? 2 : 4];
-};
-struct RsIds {
-  int32_t c[4];
+  uint32_t w[NBITS == 2 ? 4 : 8];
 };
 // Wave-uniform tile cursor: document slot u, first token base, and that
 // document's token offset and length (kept in scalar registers).
@@ -75,66 +83,77 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rs_rsrc(const void *p, uint32_
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
 
+// value of lane 16*(l/16) + K for every lane l (DPP row_newbcast)
+template <int K>
+__device__ __forceinline__ int rs_row_bcast(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, 0x150 + K, 0xF, 0xF, false);
+}
+// sum over the 32 lanes of each half wave, in lanes 31 and 63
+__device__ __forceinline__ int rs_half_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);  // row_mirror
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1, 3
+  return v;
+}
+
 template <int NBITS, int NCB>
 struct RsWave {
-  static constexpr int TQP = NCB * 16;
-  static constexpr int CB = 16 * NBITS;
+  static constexpr int TQP = NCB * 32;
+  static constexpr int CB = 16 * NBITS;  // code bytes per token
   const uint8_t *__restrict__ codes;
   const int32_t *__restrict__ cid;
   __amdgpu_buffer_rsrc_t st_rsrc;
-  int64_t my_beg, beg0;
-  int my_len, ndw, n, g;
+  int64_t my_beg;
+  int my_len, ndw, c, h, idrow, sentinel;
 
-  __device__ __forceinline__ void set_doc(RsCur &c, int u) const {
-    c.u = __builtin_amdgcn_readfirstlane(u);
-    c.base = 0;
-    if (c.u < ndw) {
-      c.len = __builtin_amdgcn_readlane(my_len, c.u);
-      const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)my_beg, c.u);
-      const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)my_beg >> 32), c.u);
-      c.beg = (int64_t)(((uint64_t)hi << 32) | lo);
-    } else {
-      c.len = 0;
-      c.beg = beg0;  // past the wave's last tile: read (and ignore) a valid tile
-    }
+  // Cursor on document u of the wave (u >= ndw: past the end; those lanes
+  // hold an empty document at token 0, so the cursor keeps reading valid,
+  // ignored tiles).
+  __device__ __forceinline__ void set_doc(RsCur &cu, int u) const {
+    cu.u = u;
+    cu.base = 0;
+    cu.len = __builtin_amdgcn_readlane(my_len, u & 63);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)my_beg, u & 63);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)my_beg >> 32), u & 63);
+    cu.beg = (int64_t)(((uint64_t)hi << 32) | lo);
   }
-  // next 16-token tile of the wave's document stream
-  __device__ __forceinline__ void advance(RsCur &c) const {
-    if (c.u < ndw) {
-      const int nb = c.base + 16;
-      if (nb >= c.len) set_doc(c, c.u + 1);
-      else c.base = __builtin_amdgcn_readfirstlane(nb);
-    }
+  // next 32-token tile of the wave's document stream
+  __device__ __forceinline__ void advance(RsCur &cu) const {
+    const int nb = cu.base + 32;
+    if (nb >= cu.len) set_doc(cu, cu.u + 1);
+    else cu.base = nb;
   }
-  __device__ __forceinline__ void load_ids(RsIds &I, const RsCur &c) const {
-    const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + c.beg + c.base, 64);
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (uint32_t)(16 * g), 0, RS_CACHE);
-    I.c[0] = (int32_t)v[0]; I.c[1] = (int32_t)v[1]; I.c[2] = (int32_t)v[2]; I.c[3] = (int32_t)v[3];
+  // id of tile row idrow (the row D register l%16 holds in this lane's half)
+  __device__ __forceinline__ int32_t load_id(const RsCur &cu) const {
+    const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + cu.beg + cu.base, 128);
+    return (int32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (uint32_t)(4 * idrow), 0, 0);
   }
-  __device__ __forceinline__ void load_codes(RsCodes<NBITS> &K, const RsCur &c) const {
-    const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (c.beg + c.base) * CB, 16 * CB);
-    const uint32_t off = (uint32_t)(n * CB + (CB / 4) * g);
-    if (NBITS == 2) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, RS_CACHE);
-      K.w[0] = v[0]; K.w[1] = v[1];
-    } else {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, RS_CACHE);
-      K.w[0] = v[0]; K.w[1] = v[1]; K.w[2 % (NBITS == 2 ? 2 : 4)] = v[2]; K.w[3 % (NBITS == 2 ? 2 : 4)] = v[3];
-    }
-  }
-  __device__ __forceinline__ void gather(float (&st)[4][NCB], const RsIds &I) const {
+  // this lane's half of token c's code: bytes CB/2 * h .. +CB/2
+  __device__ __forceinline__ void load_codes(RsCodes<NBITS> &K, const RsCur &cu) const {
+    const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (cu.beg + cu.base) * CB, 32 * CB);
+    const uint32_t off = (uint32_t)(c * CB + (CB / 2) * h);
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const uint32_t off = ((uint32_t)I.c[v] * TQP + NCB * n) * 4;
-      if (NCB == 2) {
-        const auto x = __builtin_amdgcn_raw_buffer_load_b64(st_rsrc, off, 0, 0);
-        st[v][0] = __uint_as_float(x[0]); st[v][1 % NCB] = __uint_as_float(x[1]);
-      } else {
-        const auto x = __builtin_amdgcn_raw_buffer_load_b128(st_rsrc, off, 0, 0);
-        st[v][0] = __uint_as_float(x[0]); st[v][1 % NCB] = __uint_as_float(x[1]);
-        st[v][2 % NCB] = __uint_as_float(x[2]); st[v][3 % NCB] = __uint_as_float(x[3]);
-      }
+    for (int p = 0; p < NBITS / 2; ++p) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * p, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) K.w[4 * p + e] = v[e];
     }
+  }
+  // S^T[id(row of register v)][32cb + c]; rows past the document take the
+  // sentinel row
+  __device__ __forceinline__ void gather(float (&st)[NCB][16], int32_t x, const RsCur &cu) const {
+    x = cu.base + idrow < cu.len ? x : sentinel;
+#define CHIMERA_G(V)                                                                                  \
+  {                                                                                                   \
+    const uint32_t off = ((uint32_t)rs_row_bcast<V>(x) * TQP + c) * 4;                                \
+    _Pragma("unroll") for (int cb = 0; cb < NCB; ++cb) st[cb][V] =                                    \
+        __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(st_rsrc, off + 128 * cb, 0, 0));         \
+  }
+    CHIMERA_G(0) CHIMERA_G(1) CHIMERA_G(2) CHIMERA_G(3) CHIMERA_G(4) CHIMERA_G(5) CHIMERA_G(6) CHIMERA_G(7)
+    CHIMERA_G(8) CHIMERA_G(9) CHIMERA_G(10) CHIMERA_G(11) CHIMERA_G(12) CHIMERA_G(13) CHIMERA_G(14) CHIMERA_G(15)
+#undef CHIMERA_G
   }
 };
 
@@ -143,16 +162,8 @@ __global__ __launch_bounds__(256) void k_residual_score(
     const uint16_t *__restrict__ Qs, int64_t nq, int Tq, const float *__restrict__ ST, int ncent,
     const int64_t *__restrict__ doc_off, const int32_t *__restrict__ cid, const uint8_t *__restrict__ codes,
     uint4 w_lo, uint4 w_hi, const int32_t *__restrict__ cand_ids, const int32_t *__restrict__ n_valid, int ncand,
-    int nchunks, int dpw, int32_t *__restrict__ fhat) {
-  constexpr int TQP = NCB * 16;
-  const int docs_per_block = 4 * dpw;
-  const int b = blockIdx.x;
-  const int64_t q = nq >= 8 ? (b & 7) + 8 * (int64_t)((b >> 3) / nchunks) : b / nchunks;
-  const int chunk = nq >= 8 ? (b >> 3) % nchunks : b % nchunks;
-  if (q >= nq) return;
-  const int nv = n_valid[q];
-  if (chunk * docs_per_block >= nv) return;  // uniform: before the only barrier
-
+    int dpw, int nchunks, int32_t *__restrict__ fhat) {
+  constexpr int TQP = NCB * 32;
   // 2-bit: byte -> 4 weights (two bf16x2 words); 4-bit: byte -> 2 weights
   __shared__ uint2 lut2[NBITS == 2 ? 256 : 1];
   __shared__ uint32_t lut4[NBITS == 4 ? 256 : 1];
@@ -169,164 +180,157 @@ __global__ __launch_bounds__(256) void k_residual_score(
     else
       lut4[e] = (uint32_t)w[e & 15] | ((uint32_t)w[e >> 4] << 16);
   }
-  __syncthreads();
+  __syncthreads();  // the only barrier
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // this wave's documents: candidates chunk*4*dpw + wave + 4u, u < dpw; lane u holds doc u
-  const int first = chunk * docs_per_block + wave;
-  const int rem = nv - first;
+  // workgroup b runs on XCD b % 8: with 8 or more queries, the chunks of
+  // query q go to XCD q % 8, queries in order
+  const int b = blockIdx.x;
+  const int64_t q = nq >= 8 ? (b & 7) + 8 * (int64_t)((b >> 3) / nchunks) : b / nchunks;
+  const int chunk = nq >= 8 ? (b >> 3) % nchunks : b % nchunks;
+  if (q >= nq) return;
+  const int nv = n_valid[q];
+  // this wave's documents: candidates d0 .. d0 + nd - 1
+  const int d0 = (chunk * 4 + wave) * dpw;
+  const int nd = min(dpw, nv - d0);
+  if (nd <= 0) return;
+
   RsWave<NBITS, NCB> W;
-  W.ndw = __builtin_amdgcn_readfirstlane(rem <= 0 ? 0 : min(dpw, (rem + 3) >> 2));
-  if (W.ndw == 0) return;
   W.codes = codes;
   W.cid = cid;
-  W.st_rsrc = rs_rsrc(ST + q * (int64_t)ncent * TQP, (uint32_t)ncent * TQP * 4);
-  W.n = lane & 15;
-  W.g = lane >> 4;
+  W.c = lane & 31;
+  W.h = lane >> 5;
+  // the row that D register k = l%16 holds in this lane's half
+  W.idrow = 8 * ((lane & 15) >> 2) + 4 * W.h + (lane & 3);
+  W.sentinel = ncent;
+  W.ndw = nd;
+  const int c = W.c, h = W.h;
+  W.st_rsrc = rs_rsrc(ST + q * (int64_t)(ncent + 1) * TQP, (uint32_t)(ncent + 1) * TQP * 4);
   W.my_beg = 0;
   W.my_len = 0;
-  if (lane < W.ndw) {
-    const int32_t V = cand_ids[q * ncand + first + 4 * lane];
+  if (lane < nd) {
+    const int32_t V = cand_ids[q * ncand + d0 + lane];
     W.my_beg = doc_off[V];
     W.my_len = (int)(doc_off[V + 1] - W.my_beg);
   }
-  {
-    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)W.my_beg, 0);
-    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)W.my_beg >> 32), 0);
-    W.beg0 = (int64_t)(((uint64_t)hi << 32) | lo);
-  }
-  const int n = W.n, g = W.g;
-
-  bf16x8 bq[NCB][4];
+  // query operand: column 32cb + c, dimensions 64h + 8s .. +7
+  bf16x8 bq[NCB][8];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
-    const uint4 *qp = (const uint4 *)(Qs + ((q * TQP) + NCB * n + cb) * 128 + 32 * g);
+    const uint4 *qp = (const uint4 *)(Qs + (q * TQP + 32 * cb + c) * 128 + 64 * h);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) bq[cb][s] = as_bf16x8(qp[s]);
+    for (int s = 0; s < 8; ++s) bq[cb][s] = as_bf16x8(qp[s]);
   }
+  int32_t *fout = fhat + q * ncand + d0;
 
-  // cursors of tiles t (c), t+1 (nx) and t+2 (m)
-  RsCur cc, nx, mm;
-  W.set_doc(cc, 0);
-  nx = cc;
-  W.advance(nx);
-  mm = nx;
-  W.advance(mm);
+  // cursors of tiles t (c0), t+1 (c1), t+2 (c2)
+  RsCur c0, c1, c2;
+  W.set_doc(c0, 0);
+  c1 = c0;
+  W.advance(c1);
+  c2 = c1;
+  W.advance(c2);
 
-  RsIds id0, id1;          // ids of tiles t+1 and t+2 (ring of 2)
-  RsCodes<NBITS> k0, k1;   // codes of tiles t and t+1 (ring of 2)
-  float st0[4][NCB], st1[4][NCB];  // S^T rows of tiles t and t+1 (ring of 2)
+  int32_t id0, id1;                      // ids of tiles t+1 and t+2 (ring of 2)
+  RsCodes<NBITS> k0, k1;                 // codes of tiles t and t+1 (ring of 2)
+  float st0[NCB][16], st1[NCB][16];      // S^T values of tiles t and t+1 (ring of 2)
   {
-    RsIds idc;
-    W.load_ids(idc, cc);
-    W.load_codes(k0, cc);
-    W.load_ids(id0, nx);
-    W.gather(st0, idc);
+    const int32_t idc = W.load_id(c0);
+    W.load_codes(k0, c0);
+    id0 = W.load_id(c1);
+    W.gather(st0, idc, c0);
   }
-
   float mx[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) mx[cb] = -INFINITY;
 
   // One pipeline step.  In: kc/stc hold tile t; idn holds the ids of t+1.
   // Out: kn/stn hold tile t+1; idm holds the ids of t+2.
-  auto step = [&](RsCodes<NBITS> &kc, float (&stc)[4][NCB], RsIds &idn, RsCodes<NBITS> &kn, float (&stn)[4][NCB],
-                  RsIds &idm) {
-    W.load_ids(idm, mm);
-    W.load_codes(kn, nx);
-    W.gather(stn, idn);
-    const int len = cc.len, cbase = cc.base;
-    bf16x8 a[4];
+  auto step = [&](RsCodes<NBITS> &kc, float (&stc)[NCB][16], int32_t &idn, RsCodes<NBITS> &kn,
+                  float (&stn)[NCB][16], int32_t &idm) {
+    const int32_t x = idn;
+    idm = W.load_id(c2);
+    W.load_codes(kn, c1);
+    W.gather(stn, x, c1);
+    const int len = c0.len, cbase = c0.base;
+    f32x16 acc[NCB];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[cb][v] = stc[cb][v];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
       uint4 u;
       if (NBITS == 2) {
-        // step s covers code bytes 2s and 2s+1 of this lane's 8 bytes
+        // step s covers code bytes 2s and 2s+1 of this lane's 16 bytes
         const uint32_t word = kc.w[s >> 1];
         const uint2 lo = lut2[(word >> (16 * (s & 1))) & 255u];
         const uint2 hi = lut2[(word >> (16 * (s & 1) + 8)) & 255u];
         u = make_uint4(lo.x, lo.y, hi.x, hi.y);
       } else {
         // step s covers code bytes 4s .. 4s+3 (word s)
-        const uint32_t word = kc.w[s % (NBITS == 2 ? 2 : 4)];
+        const uint32_t word = kc.w[s];
         u = make_uint4(lut4[word & 255u], lut4[(word >> 8) & 255u], lut4[(word >> 16) & 255u], lut4[word >> 24]);
       }
-      a[s] = as_bf16x8(u);
-    }
-    f32x4 acc[NCB];
-    const bool partial = cbase + 16 > len;  // wave-uniform
+      const bf16x8 a = as_bf16x8(u);
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) acc[cb][v] = stc[v][cb];
-    }
-    if (partial) {
-      // rows past the document start at -inf and never win the maximum
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (cbase + 4 * g + v >= len)
-#pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) acc[cb][v] = -INFINITY;
+      for (int cb = 0; cb < NCB; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq[cb][s], acc[cb], 0, 0, 0);
     }
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int cb = 0; cb < NCB; ++cb) {
+      float m = mx[cb];
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], bq[cb][s], acc[cb], 0, 0, 0);
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-      mx[cb] = fmaxf(mx[cb], fmaxf(fmaxf(acc[cb][0], acc[cb][1]), fmaxf(acc[cb][2], acc[cb][3])));
-    if (cbase + 16 >= len) {
-      // last tile of document cu: segmented max across the four lane groups,
-      // then the exact integer sum over query tokens
+      for (int v = 0; v < 16; ++v) m = fmaxf(m, acc[cb][v]);
+      mx[cb] = m;
+    }
+    if (cbase + 32 >= len && c0.u < W.ndw) {
+      // last tile of document c0.u: maximum over its tokens (the rows: the
+      // 16 registers and the two halves), then the exact integer sum over
+      // query tokens (the columns)
       int key = 0;
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb) {
-        float m = mx[cb];
-        m = fmaxf(m, shfl_xor(m, 16));
-        m = fmaxf(m, shfl_xor(m, 32));
-        if (NCB * n + cb < Tq) key += to_key(m);
+        const float m = fmaxf(mx[cb], shfl_xor(mx[cb], 32));
+        if (32 * cb + c < Tq) key += to_key(m);
         mx[cb] = -INFINITY;
       }
-      key += shfl_xor(key, 1);
-      key += shfl_xor(key, 2);
-      key += shfl_xor(key, 4);
-      key += shfl_xor(key, 8);
-      if (lane == 0) fhat[q * ncand + first + 4 * cc.u] = key;
+      key = rs_half_sum(key);
+      if (lane == 31) fout[c0.u] = key;
     }
-    cc = nx;
-    nx = mm;
-    W.advance(mm);
+    c0 = c1;
+    c1 = c2;
+    W.advance(c2);
   };
 
-  while (true) {
+  do {
     step(k0, st0, id0, k1, st1, id1);
-    if (cc.u >= W.ndw) break;
     step(k1, st1, id1, k0, st0, id0);
-    if (cc.u >= W.ndw) break;
-  }
+  } while (c0.u < W.ndw);
 }
 
 void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,
                            const int64_t *doc_off, const int32_t *cid, const uint8_t *codes, int nbits,
                            const uint16_t *weights_host, const int32_t *cand_ids, const int32_t *n_valid, int ncand,
                            int32_t *fhat, hipStream_t s) {
+  if (nq <= 0 || ncand <= 0) return;
   uint32_t w[8] = {0};
   const int B = 1 << nbits;
   for (int u = 0; u < B; ++u) w[u >> 1] |= (uint32_t)weights_host[u] << (16 * (u & 1));
   const uint4 w_lo = make_uint4(w[0], w[1], w[2], w[3]), w_hi = make_uint4(w[4], w[5], w[6], w[7]);
-  // documents per wave: 16, fewer for small batches so that the chip still
-  // gets about 2048 workgroups
-  const int dpw = (int)std::max<int64_t>(1, std::min<int64_t>(16, (int64_t)ncand * nq / (4 * 2048)));
+  // documents per wave: 8 (measured best at 4096 candidates per query: more
+  // documents per wave put more queries' S^T tables in flight per XCD, fewer
+  // add per-wave setup), fewer for small batches so that the chip still gets
+  // about 2048 workgroups
+  const int dpw = (int)std::max<int64_t>(1, std::min<int64_t>(8, (int64_t)ncand * nq / (4 * 2048)));
   const int nchunks = (ncand + 4 * dpw - 1) / (4 * dpw);
   const int64_t blocks = (nq >= 8 ? (nq + 7) / 8 * 8 : nq) * nchunks;
-  if (blocks == 0) return;
-#define CHIMERA_RS(NB, NC)                                                                                          \
+#define CHIMERA_RS(NB, NC)                                                                                        \
   hipLaunchKernelGGL((k_residual_score<NB, NC>), dim3((unsigned)blocks), dim3(256), 0, s, Qs, nq, Tq, ST, ncent, \
-                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, nchunks, dpw, fhat)
-  if (nbits == 2 && TQP == 32) CHIMERA_RS(2, 2);
-  else if (nbits == 2) CHIMERA_RS(2, 4);
-  else if (TQP == 32) CHIMERA_RS(4, 2);
-  else CHIMERA_RS(4, 4);
+                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, dpw, nchunks, fhat)
+  if (nbits == 2 && TQP == 32) CHIMERA_RS(2, 1);
+  else if (nbits == 2) CHIMERA_RS(2, 2);
+  else if (TQP == 32) CHIMERA_RS(4, 1);
+  else CHIMERA_RS(4, 2);
 #undef CHIMERA_RS
 }
 
