@@ -62,13 +62,35 @@ static inline void normal_pair(uint64_t key, uint64_t pair, double *z0, double *
   *z1 = r * sin(t);
 }
 
+/* The Box-Muller normals of pairs base .. base + np - 1 into z[2 np]
+ * (vectorised transform in synth_bm.c).  w is scratch of 4 np doubles
+ * following z: uniforms a, b, then the transform's r and t. */
+void synth_box_muller(const double *restrict a, const double *restrict b, double *restrict r,
+                      double *restrict t, double *restrict z, int n);
+static void normals(uint64_t key, uint64_t base, int np, double *z, double *w) {
+  double *a = w, *b = w + np;
+  for (int p = 0; p < np; ++p) {
+    a[p] = u01(key, 2 * (base + (uint64_t)p));
+    b[p] = u01(key, 2 * (base + (uint64_t)p) + 1);
+  }
+  synth_box_muller(a, b, w + 2 * np, w + 3 * np, z, np);
+}
+
 double synth_to_grid(double x) {
   double a = fabs(x);
-  if (a < 0.0625) return nearbyint(x * 2048.0) / 2048.0;
-  int e;
-  frexp(a, &e); /* a = m * 2^e, m in [0.5, 1): bf16 spacing is 2^(e-1-7) */
-  double q = ldexp(1.0, e - 8);
-  return nearbyint(x / q) * q;
+  /* below 2^-4 the grid spacing is 2^-11: adding and removing 1.5 * 2^41
+   * (whose ulp is 2^-11) rounds to it, ties to even, in the default rounding
+   * mode (this file is built without value-changing optimisations) */
+  if (a < 0.0625) return (x + 3298534883328.0) - 3298534883328.0;
+  /* bf16 spacing: keep 8 significant bits of the normal double x, rounding
+   * the 45 dropped significand bits to nearest, ties to even (a carry out of
+   * the significand correctly bumps the exponent) */
+  uint64_t b;
+  memcpy(&b, &x, sizeof b);
+  b += ((uint64_t)1 << 44) - 1 + ((b >> 45) & 1);
+  b &= ~(((uint64_t)1 << 45) - 1);
+  memcpy(&x, &b, sizeof x);
+  return x;
 }
 
 /* Unit-normalise v[dim] and write its grid integers to out. */
@@ -78,7 +100,7 @@ static void normalise_to_grid(const double *v, int dim, int16_t *out) {
   double inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
   for (int i = 0; i < dim; ++i) {
     double g = synth_to_grid(v[i] * inv);
-    out[i] = (int16_t)lrint(g * 2048.0);
+    out[i] = (int16_t)(g * 2048.0); /* exact: g is a multiple of 2^-11 */
   }
 }
 
@@ -93,11 +115,11 @@ synth_ctx *synth_create(const synth_cfg *cfg) {
   if (!ctx->cent) { synth_free(ctx); return NULL; }
 #pragma omp parallel
   {
-    double *v = (double *)malloc((size_t)dim * sizeof(double));
+    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
 #pragma omp for schedule(static)
     for (int c = 0; c < n; ++c) {
       uint64_t key = stream_key(cfg->seed, STREAM_CENT, (uint64_t)c);
-      for (int p = 0; p < dim / 2; ++p) normal_pair(key, (uint64_t)p, &v[2 * p], &v[2 * p + 1]);
+      normals(key, 0, dim / 2, v, v + dim);
       normalise_to_grid(v, dim, ctx->cent + (size_t)c * dim);
     }
     free(v);
@@ -175,7 +197,7 @@ static int32_t token_cluster(const synth_ctx *ctx, int64_t d, int64_t t) {
   return k >= c->ncent ? c->ncent - 1 : k;
 }
 
-/* Token t of doc d; v is dim doubles of scratch. */
+/* Token t of doc d; v is 4 dim doubles of scratch. */
 static void gen_token(const synth_ctx *ctx, int64_t d, int64_t t, double *v, int16_t *out_k, int32_t *out_cl) {
   const synth_cfg *c = &ctx->cfg;
   int dim = c->dim;
@@ -184,12 +206,9 @@ static void gen_token(const synth_ctx *ctx, int64_t d, int64_t t, double *v, int
   if (!out_k) return;
   const int16_t *cent = ctx->cent + (size_t)cl * dim;
   uint64_t key = stream_key(c->seed, STREAM_TOKNOISE, (uint64_t)d);
-  for (int p = 0; p < dim / 2; ++p) {
-    double z0, z1;
-    normal_pair(key, (uint64_t)t * (uint64_t)(dim / 2) + (uint64_t)p, &z0, &z1);
-    v[2 * p] = cent[2 * p] / 2048.0 + c->tok_sigma * z0;
-    v[2 * p + 1] = cent[2 * p + 1] / 2048.0 + c->tok_sigma * z1;
-  }
+  double *z = v + dim;
+  normals(key, (uint64_t)t * (uint64_t)(dim / 2), dim / 2, z, v + 2 * dim);
+  for (int i = 0; i < dim; ++i) v[i] = cent[i] / 2048.0 + c->tok_sigma * z[i];
   normalise_to_grid(v, dim, out_k);
 }
 
@@ -201,7 +220,7 @@ void synth_doc_tokens(const synth_ctx *ctx, int64_t d0, int64_t d1, const int64_
 #endif
 #pragma omp parallel num_threads(nthreads)
   {
-    double *v = (double *)malloc((size_t)dim * sizeof(double));
+    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
 #pragma omp for schedule(dynamic, 64)
     for (int64_t d = d0; d < d1; ++d) {
       int64_t row = tok_off[d - d0];
@@ -224,7 +243,7 @@ void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_
 #endif
 #pragma omp parallel num_threads(nthreads)
   {
-    double *v = (double *)malloc((size_t)dim * sizeof(double));
+    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
     int16_t *src_tok = (int16_t *)malloc((size_t)dim * sizeof(int16_t));
 #pragma omp for schedule(dynamic, 4)
     for (int64_t q = q0; q < q1; ++q) {
@@ -236,12 +255,9 @@ void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_
       uint64_t nkey = stream_key(qseed, STREAM_QNOISE, (uint64_t)q);
       for (int32_t j = 0; j < Tq; ++j) {
         gen_token(ctx, src, j % L, v, src_tok, NULL);
-        for (int p = 0; p < dim / 2; ++p) {
-          double z0, z1;
-          normal_pair(nkey, (uint64_t)j * (uint64_t)(dim / 2) + (uint64_t)p, &z0, &z1);
-          v[2 * p] = src_tok[2 * p] / 2048.0 + c->q_sigma * z0;
-          v[2 * p + 1] = src_tok[2 * p + 1] / 2048.0 + c->q_sigma * z1;
-        }
+        double *z = v + dim;
+        normals(nkey, (uint64_t)j * (uint64_t)(dim / 2), dim / 2, z, v + 2 * dim);
+        for (int i = 0; i < dim; ++i) v[i] = src_tok[i] / 2048.0 + c->q_sigma * z[i];
         normalise_to_grid(v, dim, out_k + ((size_t)(q - q0) * Tq + j) * dim);
       }
     }
