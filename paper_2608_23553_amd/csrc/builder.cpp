@@ -209,6 +209,10 @@ int load_index(const char *path, HostIndex &h) {
     if ((uint32_t)h.cid[t] >= (uint32_t)h.ncent) return fail(CHIMERA_E_FORMAT, "%s: centroid id out of range", path);
   for (int64_t p = 0; p < h.nnz; ++p)
     if ((uint64_t)h.ivf_doc[p] >= (uint64_t)h.ndocs) return fail(CHIMERA_E_FORMAT, "%s: posting doc out of range", path);
+  // the candidate walk relies on every list being strictly ascending
+  for (int32_t c = 0; c < h.ncent; ++c)
+    for (int64_t p = h.ivf_off[c] + 1; p < h.ivf_off[c + 1]; ++p)
+      if (h.ivf_doc[p] <= h.ivf_doc[p - 1]) return fail(CHIMERA_E_FORMAT, "%s: posting list %d not ascending", path, c);
   return CHIMERA_OK;
 }
 

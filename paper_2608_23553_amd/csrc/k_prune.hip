@@ -11,6 +11,9 @@
 // the paper's fused atomic aggregation (Sec. 4.2, Alg. 4) with one update
 // per (doc, query token) instead of an atomic max per retrieved token, and
 // with the score table held in LDS one document range at a time.
+#include <algorithm>
+#include <climits>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -30,15 +33,19 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
   hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, s, (uint4 *)p, n16);
 }
 
-// Workgroup (query q, doc range [d0, d0 + R)): the state of the range lives
-// in LDS, so the atomics are LDS atomics and each document's state is
-// written to HBM once.  For each rank r (in order, one barrier per rank)
-// every query token j clips its rank-r posting list to the range by binary
-// search (lists are ascending) and walks the clipped part.  The workgroup
-// then writes F' (or NO_HIT for documents outside S_Q) and adds the range's
-// histogram of the top 12 bits of the order key to the query's histogram,
-// the first pass of the refinement select.  Workgroup b runs on XCD b % 8;
-// all ranges of query q run on XCD q % 8.
+// Workgroup (query q, group g): the doc ranges [d0, d0 + R) of a contiguous
+// group of ranges, one after the other.  The state of a range lives in LDS,
+// so the atomics are LDS atomics and each document's state is written to HBM
+// once.  Every probed list (query token j, rank r) keeps a cursor in LDS
+// across the group's ranges: it is positioned once (by binary search, and
+// not at all for the first group) and then only moves forward, and a list
+// whose next document lies past the current range costs nothing there.  For
+// each rank r (in order, one barrier per rank) every list of that rank is
+// walked up to the range's end by one wave, 64 entries per step.  The
+// workgroup then writes F' (or NO_HIT for documents outside S_Q) and adds the
+// range's histogram of the top 12 bits of the order key to the query's
+// histogram, the first pass of the refinement select.  Workgroup b runs on
+// XCD b % 8; all groups of query q run on XCD q % 8.
 constexpr int WALK_THREADS = 512;
 constexpr int NO_HIT = (int)0x80000000;  // F' is never this small
 constexpr int SEL_BINS = 4096;
@@ -54,86 +61,167 @@ __device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a
 // Unsigned order key of a partial score: larger F' <-> larger key.
 __device__ __forceinline__ uint32_t fp_key(int32_t f) { return (uint32_t)f ^ 0x80000000u; }
 
+// Walk state of one probed list: entries ivf_doc[beg .. beg + len), cursor
+// pos, the document at the cursor (INT32_MAX past the end) and S[j][c].
+struct WalkList {
+  int64_t beg;
+  int32_t pos, len, next, key;
+};
+
+// One wave walks a list from pos up to the range's end d1, U blocks of 64
+// entries per step (entries past d1 are read but not applied; the next range
+// reads them again); leaves pos at the first entry >= d1 and next = its doc.
+template <int U, typename MaskT>
+__device__ __forceinline__ void walk_list(const int32_t *__restrict__ list, int32_t len, int64_t d0, int64_t d1,
+                                          MaskT bit, int32_t key, int lane, MaskT *smask, int32_t *sfp, int32_t &pos,
+                                          int32_t &next) {
+  bool done = false;
+  while (!done) {
+    int32_t doc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int32_t p = pos + 64 * u + lane;
+      doc[u] = p < len ? list[p] : INT32_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool in = doc[u] < d1;
+      if (in) {
+        const int v = (int)(doc[u] - d0);
+        const MaskT old = atomicOr(&smask[v], bit);
+        if (!(old & bit)) atomicAdd(&sfp[v], key);
+      }
+      const unsigned long long out = __ballot(!in);  // lanes at or past the range's end
+      if (out && !done) {
+        const int first = __ffsll((long long)out) - 1;
+        next = __shfl(doc[u], first, 64);
+        pos += 64 * u + first;
+        done = true;
+      }
+    }
+    if (!done) pos += 64 * U;
+  }
+}
+
 template <typename MaskT, int R>
 __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, int64_t nq, int Tq, int TQP,
     int nprobe, const int64_t *__restrict__ ivf_off, const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
-    int nranges, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
+    int nranges, int G, int M, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
   static_assert(R * sizeof(MaskT) >= SEL_BINS * 4, "the histogram reuses the mask array");
-  __shared__ MaskT smask[R];
-  __shared__ int32_t sfp[R];
-  __shared__ int64_t lo_s[64], hi_s[64];
-  __shared__ int32_t key_s[64];
+  extern __shared__ __align__(16) unsigned char walk_lds[];
+  MaskT *smask = (MaskT *)walk_lds;     // [R]
+  int32_t *sfp = (int32_t *)(smask + R);  // [R]
+  WalkList *L = (WalkList *)(sfp + R);  // [nprobe][Tq]
   const int b = blockIdx.x;
-  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / nranges);
-  const int range = (b >> 3) % nranges;
+  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / G);
+  const int g = (b >> 3) % G;
   if (q >= nq) return;
-  const int64_t d0 = (int64_t)range * R;
-  const int64_t d1 = min(ndocs, d0 + R);
-  const int nd = (int)(d1 - d0);
-  for (int v = threadIdx.x; v < R; v += WALK_THREADS) {
-    smask[v] = 0;
-    sfp[v] = 0;
+  const int rg0 = g * M, rg1 = min(nranges, rg0 + M);
+  if (rg0 >= rg1) return;  // uniform, before any barrier
+  const int64_t dstart = (int64_t)rg0 * R;
+  const int nl = nprobe * Tq;
+  for (int t = threadIdx.x; t < nl; t += WALK_THREADS) {
+    const int r = t / Tq, j = t - r * Tq;
+    const int64_t e = (q * TQP + j) * nprobe + r;
+    const int32_t c = cent_ids[e];
+    WalkList w;
+    w.beg = 0;
+    w.pos = 0;
+    w.len = 0;
+    w.key = cent_keys[e];
+    if ((uint32_t)c < (uint32_t)ncent) {
+      const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
+      const int64_t p = dstart > 0 ? lower_bound_i32(ivf_doc, beg, end, dstart) : beg;
+      w.beg = beg;
+      w.len = (int32_t)(end - beg);
+      w.pos = (int32_t)(p - beg);
+    }
+    w.next = w.pos < w.len ? ivf_doc[w.beg + w.pos] : INT32_MAX;
+    L[t] = w;
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = WALK_THREADS / 64;
-  for (int r = 0; r < nprobe; ++r) {
-    if (threadIdx.x < Tq) {
-      const int j = threadIdx.x;
-      const int32_t c = cent_ids[(q * TQP + j) * nprobe + r];
-      int64_t lo = 0, hi = 0;
-      if ((uint32_t)c < (uint32_t)ncent) {
-        const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
-        lo = lower_bound_i32(ivf_doc, beg, end, d0);
-        hi = lower_bound_i32(ivf_doc, lo, end, d1);
-      }
-      lo_s[j] = lo;
-      hi_s[j] = hi;
-      key_s[j] = cent_keys[(q * TQP + j) * nprobe + r];
+  for (int rg = rg0; rg < rg1; ++rg) {
+    const int64_t d0 = (int64_t)rg * R;
+    const int64_t d1 = min(ndocs, d0 + R);
+    const int nd = (int)(d1 - d0);
+    for (int v = threadIdx.x; v < R; v += WALK_THREADS) {
+      smask[v] = 0;
+      sfp[v] = 0;
     }
-    __syncthreads();  // also orders rank r-1's LDS atomics before rank r's
-    for (int j = wave; j < Tq; j += nwaves) {
-      const MaskT bit = (MaskT)1 << j;
-      const int32_t key = key_s[j];
-      const int64_t hi = hi_s[j];
-      for (int64_t p = lo_s[j] + lane; p < hi; p += 64) {
-        const int v = (int)(ivf_doc[p] - d0);
-        const MaskT old = atomicOr(&smask[v], bit);
-        if (!(old & bit)) atomicAdd(&sfp[v], key);
+    __syncthreads();  // the lists are set up; the previous range's reads are done
+    for (int r = 0; r < nprobe; ++r) {
+      // list j of rank r is always walked by wave j % nwaves
+      for (int j = wave; j < Tq; j += nwaves) {
+        WalkList *w = &L[r * Tq + j];
+        if (w->next >= d1) continue;  // wave-uniform: nothing of this list in the range
+        const MaskT bit = (MaskT)1 << j;
+        const int32_t key = w->key, len = w->len;
+        const int32_t *list = ivf_doc + w->beg;
+        int32_t pos = w->pos, next = INT32_MAX;
+        // lists expected to hold more than 64 entries per range keep 8 blocks
+        // of 64 entries in flight per step, others one
+        if ((int64_t)len * R > 64 * ndocs)
+          walk_list<8>(list, len, d0, d1, bit, key, lane, smask, sfp, pos, next);
+        else
+          walk_list<1>(list, len, d0, d1, bit, key, lane, smask, sfp, pos, next);
+        if (lane == 0) {
+          w->pos = pos;
+          w->next = next;
+        }
       }
+      __syncthreads();  // rank r's LDS atomics complete before rank r+1's
+    }
+    for (int v = threadIdx.x; v < nd; v += WALK_THREADS)
+      if (smask[v] == 0) sfp[v] = NO_HIT;
+    __syncthreads();
+    uint32_t *sh = (uint32_t *)smask;  // the masks are no longer needed
+    for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS) sh[i] = 0;
+    __syncthreads();
+    int32_t *f = fp + q * ndocs + d0;
+    for (int v = threadIdx.x; v < nd; v += WALK_THREADS) {
+      const int32_t x = sfp[v];
+      f[v] = x;
+      if (x != NO_HIT) atomicAdd(&sh[fp_key(x) >> 20], 1u);
     }
     __syncthreads();
+    uint32_t *hq = hist + q * SEL_BINS;
+    for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS)
+      if (sh[i]) atomicAdd(&hq[i], sh[i]);
+    __syncthreads();  // sh (the mask array) is cleared by the next range
   }
-  for (int v = threadIdx.x; v < nd; v += WALK_THREADS)
-    if (smask[v] == 0) sfp[v] = NO_HIT;
-  __syncthreads();
-  uint32_t *sh = (uint32_t *)smask;  // the masks are no longer needed
-  for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS) sh[i] = 0;
-  __syncthreads();
-  int32_t *f = fp + q * ndocs + d0;
-  for (int v = threadIdx.x; v < nd; v += WALK_THREADS) {
-    const int32_t x = sfp[v];
-    f[v] = x;
-    if (x != NO_HIT) atomicAdd(&sh[fp_key(x) >> 20], 1u);
-  }
-  __syncthreads();
-  uint32_t *hq = hist + q * SEL_BINS;
-  for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS)
-    if (sh[i]) atomicAdd(&hq[i], sh[i]);
+}
+
+template <typename MaskT, int R>
+static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
+                          const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
+                          uint32_t *hist, hipStream_t s) {
+  const int nranges = (int)((ndocs + R - 1) / R);
+  // ranges per workgroup: enough groups per query for about 4096 workgroups
+  int G = (int)std::min<int64_t>(nranges, std::max<int64_t>(1, (4096 + nq - 1) / nq));
+  const int M = (nranges + G - 1) / G;
+  G = (nranges + M - 1) / M;
+  const int64_t blocks = (nq + 7) / 8 * 8 * G;
+  if (blocks == 0 || nranges == 0) return;
+  const size_t lds = (size_t)R * (sizeof(MaskT) + 4) + (size_t)nprobe * Tq * sizeof(WalkList);
+  static bool attr = [] {
+    return hipFuncSetAttribute((const void *)k_cand_walk<MaskT, R>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               160 * 1024) == hipSuccess;
+  }();
+  (void)attr;
+  hipLaunchKernelGGL((k_cand_walk<MaskT, R>), dim3((unsigned)blocks), dim3(WALK_THREADS), lds, s, cent_ids, cent_keys,
+                     nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, G, M, fp, hist);
 }
 
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
                       uint32_t *hist, hipStream_t s) {
-  const int R = TQP == 32 ? 8192 : 4096;
-  const int nranges = (int)((ndocs + R - 1) / R);
-  const int64_t blocks = (nq + 7) / 8 * 8 * nranges;
-  if (blocks == 0) return;
   if (TQP == 32)
-    hipLaunchKernelGGL((k_cand_walk<uint32_t, 8192>), dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s, cent_ids,
-                       cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, fp, hist);
+    launch_walk_t<uint32_t, 8192>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, fp, hist,
+                                  s);
   else
-    hipLaunchKernelGGL((k_cand_walk<unsigned long long, 4096>), dim3((unsigned)blocks), dim3(WALK_THREADS), 0, s,
-                       cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, fp, hist);
+    launch_walk_t<unsigned long long, 4096>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
+                                            fp, hist, s);
 }
 
 // ------------------------------------------------------- block helpers

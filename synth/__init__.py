@@ -61,6 +61,7 @@ def _load():
     lib.synth_centroids.restype = ctypes.POINTER(ctypes.c_int16)
     lib.synth_doc_lengths.argtypes = [P, ctypes.c_int64, ctypes.c_int64, P]
     lib.synth_doc_tokens.argtypes = [P, ctypes.c_int64, ctypes.c_int64, P, P, P, P, ctypes.c_int]
+    lib.synth_docs_tokens.argtypes = [P, P, ctypes.c_int64, P, P, P, ctypes.c_int]
     lib.synth_queries.argtypes = [P, ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                   P, P, ctypes.c_int]
     lib.synth_splitmix64_at.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
@@ -149,15 +150,7 @@ class Corpus:
         rows = int(lens.sum())
         k = np.empty((rows, self.dim), dtype=np.int16)
         cl = np.empty(rows, dtype=np.int32)
-        # one contiguous doc at a time keeps the generator call simple
-        for i, d in enumerate(docs):
-            d = int(d)
-            off = np.zeros(1, dtype=np.int64)
-            ln = np.array([self.lengths[d]], dtype=np.int32)
-            r0 = int(begin[i])
-            _lib.synth_doc_tokens(self._ctx, d, d + 1, _ptr(off), _ptr(ln),
-                                  ctypes.c_void_p(k.ctypes.data + r0 * self.dim * 2),
-                                  ctypes.c_void_p(cl.ctypes.data + r0 * 4), 1)
+        _lib.synth_docs_tokens(self._ctx, _ptr(docs), len(docs), _ptr(begin), _ptr(k), _ptr(cl), self.nthreads)
         return k, cl, begin
 
     def queries(self, nq: int, Tq: int, query_seed: int = 0, q0: int = 0):

@@ -233,6 +233,27 @@ void synth_doc_tokens(const synth_ctx *ctx, int64_t d0, int64_t d1, const int64_
   }
 }
 
+void synth_docs_tokens(const synth_ctx *ctx, const int64_t *docs, int64_t n, const int64_t *row_off,
+                       int16_t *out_k, int32_t *out_cluster, int nthreads) {
+  int dim = ctx->cfg.dim;
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#endif
+#pragma omp parallel num_threads(nthreads)
+  {
+    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t i = 0; i < n; ++i) {
+      int64_t d = docs[i], row = row_off[i];
+      int32_t L = doc_length(ctx, d);
+      for (int32_t t = 0; t < L; ++t)
+        gen_token(ctx, d, t, v, out_k ? out_k + (size_t)(row + t) * dim : NULL,
+                  out_cluster ? out_cluster + row + t : NULL);
+    }
+    free(v);
+  }
+}
+
 void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_t q1, int32_t Tq,
                    int16_t *out_k, int64_t *out_src, int nthreads) {
   const synth_cfg *c = &ctx->cfg;

@@ -78,6 +78,10 @@ void synth_doc_tokens(const synth_ctx *ctx, int64_t d0, int64_t d1,
 /* Queries [q0, q1) with Tq tokens each: out_k is [q1-q0][Tq][dim] int16,
  * out_src[q1-q0] the source document (may be NULL).  query_seed separates
  * query sets drawn from one corpus. */
+/* Tokens of an arbitrary list of docs: doc docs[i] goes to rows
+ * row_off[i] .. row_off[i] + len - 1 of out_k [rows][dim] / out_cluster. */
+void synth_docs_tokens(const synth_ctx *ctx, const int64_t *docs, int64_t n, const int64_t *row_off,
+                       int16_t *out_k, int32_t *out_cluster, int nthreads);
 void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_t q1,
                    int32_t Tq, int16_t *out_k, int64_t *out_src, int nthreads);
 

@@ -90,3 +90,13 @@ def test_zipf_popularity_head():
     share = np.bincount(cl, minlength=w.ncent).max() / cl.size
     # Zipf(1.1) over 65,536 ranks: the head rank holds ~13.7% of the mass
     assert 0.12 < share < 0.155
+
+
+def test_docs_tokens_equals_per_range_generation():
+    c = synth.Corpus(synth.WORKLOADS["tiny"].corpus_spec())
+    docs = np.array([7, 999, 0, 7, 512], dtype=np.int64)
+    k, cl, begin = c.docs_tokens(docs)
+    for i, d in enumerate(docs):
+        kk, cc = c.tokens(int(d), int(d) + 1)
+        rows = slice(int(begin[i]), int(begin[i]) + len(cc))
+        assert np.array_equal(k[rows], kk) and np.array_equal(cl[rows], cc)
