@@ -41,7 +41,10 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
 // not at all for the first group) and then only moves forward, and a list
 // whose next document lies past the current range costs nothing there.  For
 // each rank r (in order, one barrier per rank) every list of that rank is
-// walked up to the range's end by one wave, 64 entries per step.  The
+// walked up to the range's end by one wave.  Query tokens that probe the same
+// centroid at the same rank share one walk of its list (on the Zipf-popular
+// corpora this halves the entries walked): one atomic OR of the group's token
+// mask tells which of them see the document for the first time.  The
 // workgroup then writes F' (or NO_HIT for documents outside S_Q) and adds the
 // range's histogram of the top 12 bits of the order key to the query's
 // histogram, the first pass of the refinement select.  Workgroup b runs on
@@ -61,11 +64,17 @@ __device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a
 // Unsigned order key of a partial score: larger F' <-> larger key.
 __device__ __forceinline__ uint32_t fp_key(int32_t f) { return (uint32_t)f ^ 0x80000000u; }
 
-// Walk state of one probed list: entries ivf_doc[beg .. beg + len), cursor
-// pos, the document at the cursor (INT32_MAX past the end) and S[j][c].
+// Walk state of one probed list (rank r, query token j): entries
+// ivf_doc[beg .. beg + len), cursor pos and the document at the cursor
+// (INT32_MAX past the end, or when another token's list stands for this one).
+// The query tokens whose rank-r centroid is the same form a group: the list
+// of the group's first token is walked once for all of them, with the
+// group's token mask and the sum of their scores S[j][c].
+template <typename MaskT>
 struct WalkList {
   int64_t beg;
-  int32_t pos, len, next, key;
+  MaskT mask;
+  int32_t pos, len, next, gsum;
 };
 
 // One wave walks a list from pos up to the range's end d1, U blocks of 64
@@ -73,8 +82,8 @@ struct WalkList {
 // reads them again); leaves pos at the first entry >= d1 and next = its doc.
 template <int U, typename MaskT>
 __device__ __forceinline__ void walk_list(const int32_t *__restrict__ list, int32_t len, int64_t d0, int64_t d1,
-                                          MaskT bit, int32_t key, int lane, MaskT *smask, int32_t *sfp, int32_t &pos,
-                                          int32_t &next) {
+                                          MaskT gmask, int32_t gsum, const int32_t *keys, int lane, MaskT *smask,
+                                          int32_t *sfp, int32_t &pos, int32_t &next) {
   bool done = false;
   while (!done) {
     int32_t doc[U];
@@ -88,8 +97,14 @@ __device__ __forceinline__ void walk_list(const int32_t *__restrict__ list, int3
       const bool in = doc[u] < d1;
       if (in) {
         const int v = (int)(doc[u] - d0);
-        const MaskT old = atomicOr(&smask[v], bit);
-        if (!(old & bit)) atomicAdd(&sfp[v], key);
+        const MaskT fresh = gmask & ~atomicOr(&smask[v], gmask);  // tokens for which this is the first hit
+        if (fresh == gmask) {
+          atomicAdd(&sfp[v], gsum);
+        } else if (fresh) {
+          int32_t add = 0;
+          for (MaskT m = fresh; m; m &= m - 1) add += keys[__builtin_ctzll((unsigned long long)m)];
+          atomicAdd(&sfp[v], add);
+        }
       }
       const unsigned long long out = __ballot(!in);  // lanes at or past the range's end
       if (out && !done) {
@@ -110,9 +125,11 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     int nranges, int G, int M, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
   static_assert(R * sizeof(MaskT) >= SEL_BINS * 4, "the histogram reuses the mask array");
   extern __shared__ __align__(16) unsigned char walk_lds[];
-  MaskT *smask = (MaskT *)walk_lds;     // [R]
-  int32_t *sfp = (int32_t *)(smask + R);  // [R]
-  WalkList *L = (WalkList *)(sfp + R);  // [nprobe][Tq]
+  MaskT *smask = (MaskT *)walk_lds;                        // [R]
+  int32_t *sfp = (int32_t *)(smask + R);                     // [R]
+  WalkList<MaskT> *L = (WalkList<MaskT> *)(sfp + R);         // [nprobe][Tq]
+  int32_t *skey = (int32_t *)(L + nprobe * Tq);              // [nprobe][Tq] S[j][c] keys
+  int32_t *scid = skey + nprobe * Tq;                        // [nprobe][Tq] centroid ids
   const int b = blockIdx.x;
   const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / G);
   const int g = (b >> 3) % G;
@@ -124,13 +141,33 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   for (int t = threadIdx.x; t < nl; t += WALK_THREADS) {
     const int r = t / Tq, j = t - r * Tq;
     const int64_t e = (q * TQP + j) * nprobe + r;
-    const int32_t c = cent_ids[e];
-    WalkList w;
+    scid[t] = cent_ids[e];
+    skey[t] = cent_keys[e];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < nl; t += WALK_THREADS) {
+    const int r = t / Tq, j = t - r * Tq;
+    const int32_t c = scid[t];
+    WalkList<MaskT> w;
     w.beg = 0;
     w.pos = 0;
     w.len = 0;
-    w.key = cent_keys[e];
-    if ((uint32_t)c < (uint32_t)ncent) {
+    w.mask = 0;
+    w.gsum = 0;
+    // one pass over the rank's centroids: is j the group's first token, and
+    // the group's mask and score sum
+    bool head = (uint32_t)c < (uint32_t)ncent;
+    MaskT gm = 0;
+    int32_t gs = 0;
+    for (int i = 0; i < Tq; ++i) {
+      const bool same = scid[r * Tq + i] == c;
+      head = head && !(same && i < j);
+      gm |= same ? (MaskT)1 << i : (MaskT)0;
+      gs += same ? skey[r * Tq + i] : 0;
+    }
+    if (head) {
+      w.mask = gm;
+      w.gsum = gs;
       const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
       const int64_t p = dstart > 0 ? lower_bound_i32(ivf_doc, beg, end, dstart) : beg;
       w.beg = beg;
@@ -153,18 +190,18 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     for (int r = 0; r < nprobe; ++r) {
       // list j of rank r is always walked by wave j % nwaves
       for (int j = wave; j < Tq; j += nwaves) {
-        WalkList *w = &L[r * Tq + j];
+        WalkList<MaskT> *w = &L[r * Tq + j];
         if (w->next >= d1) continue;  // wave-uniform: nothing of this list in the range
-        const MaskT bit = (MaskT)1 << j;
-        const int32_t key = w->key, len = w->len;
+        const MaskT gmask = w->mask;
+        const int32_t gsum = w->gsum, len = w->len;
         const int32_t *list = ivf_doc + w->beg;
         int32_t pos = w->pos, next = INT32_MAX;
         // lists expected to hold more than 64 entries per range keep 8 blocks
         // of 64 entries in flight per step, others one
         if ((int64_t)len * R > 64 * ndocs)
-          walk_list<8>(list, len, d0, d1, bit, key, lane, smask, sfp, pos, next);
+          walk_list<8>(list, len, d0, d1, gmask, gsum, skey + r * Tq, lane, smask, sfp, pos, next);
         else
-          walk_list<1>(list, len, d0, d1, bit, key, lane, smask, sfp, pos, next);
+          walk_list<1>(list, len, d0, d1, gmask, gsum, skey + r * Tq, lane, smask, sfp, pos, next);
         if (lane == 0) {
           w->pos = pos;
           w->next = next;
@@ -203,7 +240,7 @@ static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int
   G = (nranges + M - 1) / M;
   const int64_t blocks = (nq + 7) / 8 * 8 * G;
   if (blocks == 0 || nranges == 0) return;
-  const size_t lds = (size_t)R * (sizeof(MaskT) + 4) + (size_t)nprobe * Tq * sizeof(WalkList);
+  const size_t lds = (size_t)R * (sizeof(MaskT) + 4) + (size_t)nprobe * Tq * (sizeof(WalkList<MaskT>) + 8);
   static bool attr = [] {
     return hipFuncSetAttribute((const void *)k_cand_walk<MaskT, R>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                160 * 1024) == hipSuccess;
