@@ -156,7 +156,8 @@ static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int npr
     b += align_up((size_t)nb * 4096 * 4);        // select histogram
   }
   if (stop == STOP_CANDIDATES) b += align_up((size_t)(nb + 1) * 8);  // counts
-  if (stop >= STOP_PRUNE) b += 3 * align_up((size_t)nb * ncand * 4) + align_up((size_t)nb * 4);  // cand, keys, F^, n
+  if (stop >= STOP_PRUNE)  // cand, keys, F^, n, select state
+    b += 3 * align_up((size_t)nb * ncand * 4) + align_up((size_t)nb * 4) + align_up(select_scratch_bytes(nb, idx->ndocs));
   return b;
 }
 
@@ -274,7 +275,9 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     int32_t *fhat = stop >= STOP_FULL ? cv.take<int32_t>((size_t)nb * ncand) : nullptr;
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
-    launch_select(fp, hist, nb, idx->ndocs, ncand, cand, candk, nval, s);
+    char *selw = cv.take<char>(select_scratch_bytes(nb, idx->ndocs));
+    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    launch_select(fp, hist, nb, idx->ndocs, ncand, selw, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
     stage_mark(idx, s, mark);

@@ -79,9 +79,12 @@ void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t
                       uint32_t *hist, hipStream_t s);
 
 // Refinement select: per query, the ncand best of S_Q by (F' desc, V asc),
-// written in ascending V order; n_valid [nq].
-void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, int32_t *cand_ids,
-                   int32_t *cand_keys, int32_t *n_valid, hipStream_t s);
+// written in ascending V order; n_valid [nq].  scratch holds
+// select_scratch_bytes(nq, ndocs) bytes (no initial contents needed).
+int select_chunks(int64_t nq, int64_t ndocs);
+size_t select_scratch_bytes(int64_t nq, int64_t ndocs);
+void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, void *scratch,
+                   int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s);
 // Candidate-set tap: counts [nq] of S_Q; then each S_Q in ascending order.
 void launch_count_hits(const int32_t *fp, int64_t nq, int64_t ndocs, int64_t *counts, hipStream_t s);
 void launch_list_hits(const int32_t *fp, int64_t nq, int64_t ndocs, const int64_t *offsets, int32_t *doc_ids,

@@ -297,8 +297,8 @@ __device__ __forceinline__ long long block_exclusive_scan(long long x, long long
 // and the count of the bins above b in *s_above.
 __device__ __forceinline__ void select_bin(const uint32_t *bins, int nbins, long long rem, long long *wsum,
                                            long long *s_tot, int *s_bin, long long *s_above) {
-  const int per = (nbins + SEL_THREADS - 1) / SEL_THREADS;
-  const int top = nbins - 1 - threadIdx.x * per;  // this thread's bins: top, top-1, ... (descending)
+  const int per = (nbins + (int)blockDim.x - 1) / (int)blockDim.x;
+  const int top = nbins - 1 - (int)threadIdx.x * per;  // this thread's bins: top, top-1, ... (descending)
   long long local = 0;
   for (int i = 0; i < per; ++i)
     if (top - i >= 0) local += bins[top - i];
@@ -441,10 +441,252 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
   }
 }
 
-void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, int32_t *cand_ids,
-                   int32_t *cand_keys, int32_t *n_valid, hipStream_t s) {
-  hipLaunchKernelGGL((k_select<0>), dim3((unsigned)nq), dim3(SEL_THREADS), 0, s, fp, hist, ndocs, ncand,
-                     (const int64_t *)nullptr, cand_ids, cand_keys, n_valid);
+// ---------------------------------------------------------------------
+// Refinement select split over P chunks of documents per query, so that a
+// launch with few queries still fills the chip (with 128 queries or more,
+// k_select runs one workgroup per query instead).  A radix select on the order
+// key u = fp_key(F') finds the ncand-th largest key T and how many documents
+// with key T to keep (the lowest ids): bits 31..20 come from the walk's
+// histogram, bits 19..8 and 7..0 from two histogram passes over the chunks
+// (global atomics, only documents whose higher bits match count).  Then every
+// chunk counts what it keeps, the counts are scanned per query, and each
+// chunk writes its part of the candidate list in ascending doc order.
+// SelState per query: the bins found so far, the count still to place, T and
+// the ties to keep.
+struct SelState {
+  long long rem;     // candidates still to place below the bins fixed so far
+  uint32_t prefix;   // key bits fixed so far
+  uint32_t T;        // threshold key (0: keep every hit)
+  long long need;    // documents with key T to keep
+  long long total;   // candidates written
+};
+constexpr int SPLIT_THREADS = 256;
+
+// Per query: bin of bits 31..20 from the walk's histogram; clears the
+// histograms of the next passes.
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_first(const uint32_t *__restrict__ hist1, int ncand,
+                                                             uint32_t *__restrict__ hist2, uint32_t *__restrict__ hist3,
+                                                             SelState *__restrict__ st) {
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot, s_above;
+  __shared__ int s_bin;
+  const int64_t q = blockIdx.x;
+  const uint32_t *h = hist1 + q * SEL_BINS;
+  long long local = 0;
+  for (int i = threadIdx.x; i < SEL_BINS; i += SPLIT_THREADS) {
+    local += h[i];
+    hist2[q * SEL_BINS + i] = 0;
+  }
+  for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) hist3[q * 256 + i] = 0;
+  block_exclusive_scan(local, wsum, &s_tot);
+  const long long nhit = s_tot;
+  if (nhit <= ncand) {
+    if (threadIdx.x == 0) st[q] = SelState{0, 0, 0, 0, 0};
+    return;
+  }
+  select_bin(h, SEL_BINS, ncand, wsum, &s_tot, &s_bin, &s_above);
+  if (threadIdx.x == 0) st[q] = SelState{ncand - s_above, (uint32_t)s_bin, 1, 0, 0};
+}
+
+// Histogram pass over one chunk: keys whose top (32 - SHIFT - BITS) bits are
+// the state's prefix, binned by their next BITS bits.
+template <int SHIFT, int BITS>
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_hist(const int32_t *__restrict__ fp, int64_t ndocs, int P,
+                                                            const SelState *__restrict__ st,
+                                                            uint32_t *__restrict__ hout) {
+  __shared__ uint32_t h[1 << BITS];
+  const int64_t q = blockIdx.x / P;
+  const int c = blockIdx.x % P;
+  if (st[q].T == 0) return;  // uniform: every hit is kept
+  const uint32_t prefix = st[q].prefix;
+  for (int i = threadIdx.x; i < (1 << BITS); i += SPLIT_THREADS) h[i] = 0;
+  __syncthreads();
+  const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
+  const int32_t *f = fp + q * ndocs;
+  for (int64_t v = v0 + threadIdx.x; v < v1; v += SPLIT_THREADS) {
+    const int32_t x = f[v];
+    if (x == NO_HIT) continue;
+    const uint32_t u = fp_key(x);
+    if ((u >> (SHIFT + BITS)) == prefix) atomicAdd(&h[(u >> SHIFT) & ((1u << BITS) - 1)], 1u);
+  }
+  __syncthreads();
+  uint32_t *o = hout + q * (1 << BITS);
+  for (int i = threadIdx.x; i < (1 << BITS); i += SPLIT_THREADS)
+    if (h[i]) atomicAdd(&o[i], h[i]);
+}
+
+// Per query: the next bin from a pass's histogram; after the last pass, the
+// threshold key T and the ties to keep.
+template <int BITS, bool LAST>
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_next(const uint32_t *__restrict__ hin, SelState *__restrict__ st) {
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot, s_above;
+  __shared__ int s_bin;
+  const int64_t q = blockIdx.x;
+  const SelState s0 = st[q];
+  if (s0.T == 0) return;
+  select_bin(hin + q * (1 << BITS), 1 << BITS, s0.rem, wsum, &s_tot, &s_bin, &s_above);
+  if (threadIdx.x == 0) {
+    SelState s1 = s0;
+    s1.prefix = (s0.prefix << BITS) | (uint32_t)s_bin;
+    s1.rem = s0.rem - s_above;
+    if (LAST) {
+      s1.T = s1.prefix;
+      s1.need = s1.rem;
+    }
+    st[q] = s1;
+  }
+}
+
+// Per chunk: documents kept outright (key > T) and ties (key == T).
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_count(const int32_t *__restrict__ fp, int64_t ndocs, int P,
+                                                             const SelState *__restrict__ st,
+                                                             long long *__restrict__ counts) {
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot;
+  const int64_t q = blockIdx.x / P;
+  const int c = blockIdx.x % P;
+  const uint32_t T = st[q].T;
+  const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
+  const int32_t *f = fp + q * ndocs;
+  long long above = 0, ties = 0;
+  for (int64_t v = v0 + threadIdx.x; v < v1; v += SPLIT_THREADS) {
+    const int32_t x = f[v];
+    if (x == NO_HIT) continue;
+    const uint32_t u = fp_key(x);
+    above += u > T;
+    ties += u == T;
+  }
+  block_exclusive_scan(above, wsum, &s_tot);
+  const long long a = s_tot;
+  block_exclusive_scan(ties, wsum, &s_tot);
+  if (threadIdx.x == 0) {
+    counts[2 * (q * P + c)] = a;
+    counts[2 * (q * P + c) + 1] = s_tot;
+  }
+}
+
+// Per query: output offset and ties-before of every chunk (in place), the
+// number of candidates, and the padding of the unused slots.
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_scan(int P, int ncand, SelState *__restrict__ st,
+                                                            long long *__restrict__ counts, int32_t *__restrict__ out_ids,
+                                                            int32_t *__restrict__ out_keys,
+                                                            int32_t *__restrict__ n_valid) {
+  __shared__ long long total;
+  const int64_t q = blockIdx.x;
+  if (threadIdx.x == 0) {
+    const long long need = st[q].need;
+    long long off = 0, tb = 0;
+    for (int c = 0; c < P; ++c) {
+      long long *cc = counts + 2 * (q * P + c);
+      const long long a = cc[0], t = cc[1];
+      const long long take = a + max(0ll, min(t, need - tb));
+      cc[0] = off;
+      cc[1] = tb;
+      off += take;
+      tb += t;
+    }
+    const long long n = min(off, (long long)ncand);
+    st[q].total = n;
+    n_valid[q] = (int32_t)n;
+    total = n;
+  }
+  __syncthreads();
+  for (long long i = total + threadIdx.x; i < ncand; i += SPLIT_THREADS) {
+    out_ids[q * ncand + i] = -1;
+    out_keys[q * ncand + i] = 0;
+  }
+}
+
+// Per chunk: the ordered compaction of its kept documents.
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__restrict__ fp, int64_t ndocs, int P,
+                                                             int ncand, const SelState *__restrict__ st,
+                                                             const long long *__restrict__ counts,
+                                                             int32_t *__restrict__ out_ids,
+                                                             int32_t *__restrict__ out_keys) {
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot;
+  const int64_t q = blockIdx.x / P;
+  const int c = blockIdx.x % P;
+  const uint32_t T = st[q].T;
+  const long long need = st[q].need;
+  long long written = counts[2 * (q * P + c)], ties_seen = counts[2 * (q * P + c) + 1];
+  const int64_t per = (ndocs + P - 1) / P, vb = c * per, ve = min(ndocs, vb + per);
+  const int32_t *f = fp + q * ndocs;
+  const int64_t step = (int64_t)SPLIT_THREADS * SEL_ITEMS;
+  for (int64_t c0 = vb; c0 < ve; c0 += step) {
+    const int64_t v0 = c0 + (int64_t)threadIdx.x * SEL_ITEMS;
+    int take_flags = 0, tie_flags = 0, ntie = 0;
+    int32_t xs[SEL_ITEMS];
+#pragma unroll
+    for (int i = 0; i < SEL_ITEMS; ++i) {
+      const int64_t v = v0 + i;
+      xs[i] = v < ve ? f[v] : NO_HIT;
+      if (xs[i] != NO_HIT) {
+        const uint32_t u = fp_key(xs[i]);
+        if (u > T) take_flags |= 1 << i;
+        else if (u == T) { tie_flags |= 1 << i; ++ntie; }
+      }
+    }
+    long long tie_rank = block_exclusive_scan(ntie, wsum, &s_tot);
+    const long long tie_total = s_tot;
+#pragma unroll
+    for (int i = 0; i < SEL_ITEMS; ++i)
+      if (tie_flags & (1 << i)) {
+        if (ties_seen + tie_rank < need) take_flags |= 1 << i;
+        ++tie_rank;
+      }
+    long long pos = block_exclusive_scan(__popc(take_flags), wsum, &s_tot);
+    const long long take_total = s_tot;
+#pragma unroll
+    for (int i = 0; i < SEL_ITEMS; ++i)
+      if (take_flags & (1 << i)) {
+        if (written + pos < ncand) {
+          out_ids[q * ncand + written + pos] = (int32_t)(v0 + i);
+          out_keys[q * ncand + written + pos] = xs[i];
+        }
+        ++pos;
+      }
+    written += take_total;
+    ties_seen += tie_total;
+  }
+}
+
+int select_chunks(int64_t nq, int64_t ndocs) {
+  const int64_t by_q = (2048 + nq - 1) / std::max<int64_t>(1, nq);
+  const int64_t by_docs = (ndocs + 4095) / 4096;
+  return (int)std::max<int64_t>(1, std::min(by_q, by_docs));
+}
+
+size_t select_scratch_bytes(int64_t nq, int64_t ndocs) {
+  const int P = select_chunks(nq, ndocs);
+  return (size_t)nq * (sizeof(SelState) + (SEL_BINS + 256) * 4 + (size_t)P * 16) + 256;
+}
+
+void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, void *scratch,
+                   int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s) {
+  if (nq <= 0) return;
+  if (nq >= 128) {
+    // enough queries to fill the chip with one workgroup each (three passes
+    // over F' instead of four, and one launch)
+    hipLaunchKernelGGL((k_select<0>), dim3((unsigned)nq), dim3(SEL_THREADS), 0, s, fp, hist, ndocs, ncand,
+                       (const int64_t *)nullptr, cand_ids, cand_keys, n_valid);
+    return;
+  }
+  const int P = select_chunks(nq, ndocs);
+  SelState *st = (SelState *)scratch;
+  uint32_t *hist2 = (uint32_t *)(st + nq);
+  uint32_t *hist3 = hist2 + nq * SEL_BINS;
+  long long *counts = (long long *)(((uintptr_t)(hist3 + nq * 256) + 15) & ~(uintptr_t)15);
+  const dim3 gq((unsigned)nq), gc((unsigned)(nq * P)), tb(SPLIT_THREADS);
+  hipLaunchKernelGGL(k_sel_first, gq, tb, 0, s, hist, ncand, hist2, hist3, st);
+  hipLaunchKernelGGL((k_sel_hist<8, 12>), gc, tb, 0, s, fp, ndocs, P, st, hist2);
+  hipLaunchKernelGGL((k_sel_next<12, false>), gq, tb, 0, s, hist2, st);
+  hipLaunchKernelGGL((k_sel_hist<0, 8>), gc, tb, 0, s, fp, ndocs, P, st, hist3);
+  hipLaunchKernelGGL((k_sel_next<8, true>), gq, tb, 0, s, hist3, st);
+  hipLaunchKernelGGL(k_sel_count, gc, tb, 0, s, fp, ndocs, P, st, counts);
+  hipLaunchKernelGGL(k_sel_scan, gq, tb, 0, s, P, ncand, st, counts, cand_ids, cand_keys, n_valid);
+  hipLaunchKernelGGL(k_sel_write, gc, tb, 0, s, fp, ndocs, P, ncand, st, counts, cand_ids, cand_keys);
 }
 
 __global__ __launch_bounds__(256) void k_count_hits(const int32_t *__restrict__ fp, int64_t ndocs,

@@ -347,7 +347,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void k_topk(const int32_t *__restrict
   extern __shared__ uint64_t sk[];  // [kpow2]
   __shared__ int hist[256];
   __shared__ unsigned long long s_prefix, s_pmask;
-  __shared__ int s_remaining, s_count;
+  __shared__ int s_remaining, s_count, s_done;
   const int64_t q = blockIdx.x;
   const int n = n_valid[q];
   const int m = min(k, n);
@@ -356,7 +356,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void k_topk(const int32_t *__restrict
 
   unsigned long long T = 0;  // every key >= T is taken
   if (n > k) {
-    if (threadIdx.x == 0) { s_prefix = 0; s_pmask = 0; s_remaining = k; }
+    if (threadIdx.x == 0) { s_prefix = 0; s_pmask = 0; s_remaining = k; s_done = 0; }
     for (int pass = 0; pass < 8; ++pass) {
       const int shift = 56 - 8 * pass;
       for (int b = threadIdx.x; b < 256; b += TOPK_THREADS) hist[b] = 0;
@@ -367,19 +367,39 @@ __global__ __launch_bounds__(TOPK_THREADS) void k_topk(const int32_t *__restrict
         if ((K & pmask) == prefix) atomicAdd(&hist[(K >> shift) & 255], 1);
       }
       __syncthreads();
-      if (threadIdx.x == 0) {
-        int rem = s_remaining, cum = 0, sel = 0;
-        for (int b = 255; b >= 0; --b) {
-          if (cum + hist[b] >= rem) { sel = b; break; }
-          cum += hist[b];
+      if (threadIdx.x < 64) {
+        // wave 0 finds the bin holding the rem-th largest key: lane l covers
+        // bins 255 - 4l .. 252 - 4l, counts above it come from a lane scan
+        const int lane = threadIdx.x, rem = s_remaining;
+        int local = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) local += hist[255 - 4 * lane - i];
+        int incl = local;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const int y = __shfl_up(incl, d, 64);
+          if (lane >= d) incl += y;
         }
-        s_remaining = rem - cum;
-        s_prefix = prefix | ((unsigned long long)sel << shift);
-        s_pmask = pmask | (255ull << shift);
+        int cum = incl - local;
+        if (cum < rem && incl >= rem) {
+          for (int i = 0; i < 4; ++i) {
+            const int b = 255 - 4 * lane - i;
+            if (cum + hist[b] >= rem) {
+              s_remaining = rem - cum;
+              s_prefix = prefix | ((unsigned long long)b << shift);
+              s_pmask = pmask | (255ull << shift);
+              // the whole bin is needed: every key >= the bin's base is taken
+              s_done = hist[b] == rem - cum;
+              break;
+            }
+            cum += hist[b];
+          }
+        }
       }
       __syncthreads();
+      if (s_done) break;
     }
-    T = s_prefix;  // keys are distinct: exactly k keys are >= T
+    T = s_prefix;  // keys are distinct: exactly k keys are >= T (the base of the last bin)
   }
   for (int i = threadIdx.x; i < kpow2; i += TOPK_THREADS) sk[i] = 0;
   if (threadIdx.x == 0) s_count = 0;
