@@ -56,12 +56,17 @@ def build_corpus_index(w, threads):
     from paper_2608_23553_amd import build_index
     corpus = synth.Corpus(w.corpus_spec(), nthreads=threads)
 
+    passes = [0]
+
     def chunks():
         step = 50_000
+        passes[0] += 1
         for d0 in range(0, w.ndocs, step):
             d1 = min(w.ndocs, d0 + step)
             k, cl = corpus.tokens(d0, d1)
             yield synth.k_to_bf16_bits(k), cl, corpus.lengths[d0:d1]
+            if (d0 // step) % 20 == 19:
+                log(f"index build pass {passes[0]}/2: {d1}/{w.ndocs} docs")
 
     t = time.perf_counter()
     b = build_index(synth.k_to_bf16_bits(corpus.centroids_k), w.nbits, chunks)

@@ -56,7 +56,10 @@ enum {
 /* Element type of a query tensor. */
 enum { CHIMERA_F32 = 0, CHIMERA_BF16 = 1 };
 
-/* Limits of this build. */
+/* Limits of this build.  Besides these, the candidate walk keeps per-list
+ * state for all Tq x nprobe probed lists of a query on chip: with more than
+ * 32 query tokens, Tq * nprobe up to 2304 always fits (e.g. 64 x 32), and
+ * larger products may return CHIMERA_E_UNSUPPORTED. */
 #define CHIMERA_DIM 128
 #define CHIMERA_MAX_TQ 64
 #define CHIMERA_MAX_NPROBE 64

@@ -60,6 +60,12 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   idx->ndocs = h.ndocs; idx->ntok = h.ntok; idx->nnz = h.nnz;
   std::memcpy(idx->h_weights, h.weights.data(), h.weights.size() * 2);
   std::memcpy(idx->h_cut, h.cut_k.data(), h.cut_k.size() * 4);
+  std::vector<int8_t> dense_slot;
+  std::vector<uint64_t> doc_dense;
+  if (int rc = dense_lists(h, dense_slot, doc_dense, idx->ndense)) {
+    delete idx;
+    return rc;
+  }
   struct Sec { void **dst; const void *src; size_t bytes; } secs[] = {
       {(void **)&idx->d_cent, h.cent.data(), h.cent.size() * 2},
       {(void **)&idx->d_doc_off, h.doc_off.data(), h.doc_off.size() * 8},
@@ -67,6 +73,8 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
       {(void **)&idx->d_codes, h.codes.data(), h.codes.size()},
       {(void **)&idx->d_ivf_off, h.ivf_off.data(), h.ivf_off.size() * 8},
       {(void **)&idx->d_ivf_doc, h.ivf_doc.data(), h.ivf_doc.size() * 4},
+      {(void **)&idx->d_dense_slot, dense_slot.data(), dense_slot.size()},
+      {(void **)&idx->d_doc_dense, doc_dense.data(), doc_dense.size() * 8},
   };
   size_t need = 0;
   for (auto &s : secs) need += s.bytes;
@@ -78,7 +86,7 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   // Token arrays (cid, codes) are followed by kTokenPad zeroed tokens: the
   // residual scorer reads whole 16-token tiles and may run up to 15 tokens
   // past the last document.  Every section gets at least 256 spare bytes.
-  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256};
+  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256, 256, 256};
   int si = 0;
   for (auto &s : secs) {
     const size_t pad = pad_bytes[si++];
@@ -114,6 +122,8 @@ static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype
   if (Tq > CHIMERA_MAX_TQ) return fail(CHIMERA_E_UNSUPPORTED, "Tq %d > %d", Tq, CHIMERA_MAX_TQ);
   if (nprobe < 1 || nprobe > idx->ncent) return fail(CHIMERA_E_INVAL, "nprobe must be in [1, ncent=%d]", idx->ncent);
   if (nprobe > CHIMERA_MAX_NPROBE) return fail(CHIMERA_E_UNSUPPORTED, "nprobe %d > %d", nprobe, CHIMERA_MAX_NPROBE);
+  if (walk_lds_bytes(Tq <= 32 ? 32 : 64, nprobe, Tq) > kWalkMaxLds)
+    return fail(CHIMERA_E_UNSUPPORTED, "Tq %d x nprobe %d exceeds the candidate walk's local memory", Tq, nprobe);
   return CHIMERA_OK;
 }
 
@@ -247,7 +257,8 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
     launch_fill_zero(hist, (size_t)nb * 4096 * 4, s);
-    launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, fp, hist, s);
+    launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, idx->ndense,
+                     idx->d_dense_slot, idx->d_doc_dense, fp, hist, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_CANDIDATES) {
       int64_t *cnt = cv.take<int64_t>((size_t)nb + 1);
@@ -329,7 +340,8 @@ void chimera_index_free(chimera_index *idx) {
   if (!idx) return;
   DeviceGuard dg(idx->device);
   (void)hipDeviceSynchronize();
-  void *ptrs[] = {idx->d_cent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->d_ivf_off, idx->d_ivf_doc, idx->scratch};
+  void *ptrs[] = {idx->d_cent,    idx->d_doc_off,    idx->d_cid,       idx->d_codes,  idx->d_ivf_off,
+                  idx->d_ivf_doc, idx->d_dense_slot, idx->d_doc_dense, idx->scratch};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   if (idx->scratch_done) (void)hipEventDestroy(idx->scratch_done);

@@ -216,6 +216,42 @@ int load_index(const char *path, HostIndex &h) {
   return CHIMERA_OK;
 }
 
+int dense_lists(const HostIndex &h, std::vector<int8_t> &slot, std::vector<uint64_t> &doc_mask, int &ndense) {
+  slot.assign(h.ncent, -1);
+  doc_mask.clear();
+  ndense = 0;
+  std::vector<int32_t> cand;
+  for (int32_t c = 0; c < h.ncent; ++c)
+    if ((h.ivf_off[c + 1] - h.ivf_off[c]) * 16 > h.ndocs) cand.push_back(c);
+  std::sort(cand.begin(), cand.end(), [&](int32_t a, int32_t b) {
+    const int64_t la = h.ivf_off[a + 1] - h.ivf_off[a], lb = h.ivf_off[b + 1] - h.ivf_off[b];
+    return la != lb ? la > lb : a < b;
+  });
+  if ((int)cand.size() > kMaxDense) cand.resize(kMaxDense);
+  ndense = (int)cand.size();
+  if (!ndense) return CHIMERA_OK;
+  for (int i = 0; i < ndense; ++i) slot[cand[i]] = (int8_t)i;
+  doc_mask.assign(h.ndocs, 0);
+  parallel_for(h.ndocs, [&](int64_t a, int64_t e) {
+    for (int64_t v = a; v < e; ++v) {
+      uint64_t m = 0;
+      for (int64_t t = h.doc_off[v]; t < h.doc_off[v + 1]; ++t) {
+        const int sl = slot[h.cid[t]];
+        if (sl >= 0) m |= 1ull << sl;
+      }
+      doc_mask[v] = m;
+    }
+  });
+  // every dense list must hold exactly the documents whose mask has its bit
+  std::vector<int64_t> count(ndense, 0);
+  for (int64_t v = 0; v < h.ndocs; ++v)
+    for (uint64_t m = doc_mask[v]; m; m &= m - 1) ++count[__builtin_ctzll(m)];
+  for (int i = 0; i < ndense; ++i)
+    if (count[i] != h.ivf_off[cand[i] + 1] - h.ivf_off[cand[i]])
+      return fail(CHIMERA_E_FORMAT, "posting list %d does not match the token assignment", cand[i]);
+  return CHIMERA_OK;
+}
+
 }  // namespace chimera
 
 using namespace chimera;

@@ -44,6 +44,13 @@ struct HostIndex {
 };
 
 int save_index(const HostIndex &h, const char *path);
+// Dense posting lists: up to kMaxDense centroids whose doc-level list holds
+// more than ndocs / 16 documents (the longest first, ties to the lower id).
+// slot[c] is the centroid's bit (or -1) and doc_mask[v] has bit slot[c] set
+// iff document v has a token assigned to c.  Returns E_FORMAT if a mask
+// disagrees with the list lengths.
+constexpr int kMaxDense = 64;
+int dense_lists(const HostIndex &h, std::vector<int8_t> &slot, std::vector<uint64_t> &doc_mask, int &ndense);
 const HostIndex *builder_host(const chimera_builder *b);  // builds the lists on first use
 int load_index(const char *path, HostIndex &h);
 
@@ -74,9 +81,14 @@ void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const
 // [nq][4096] u32, zero on entry, receives the histogram of the top 12 bits of
 // F' ^ 0x80000000 over S_Q.
 void launch_fill_zero(void *p, size_t bytes, hipStream_t s);
+// LDS the candidate walk needs for Tq query tokens and nprobe ranks; a
+// workgroup can use at most kWalkMaxLds.
+size_t walk_lds_bytes(int TQP, int nprobe, int Tq);
+constexpr size_t kWalkMaxLds = 160 * 1024;
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
-                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
-                      uint32_t *hist, hipStream_t s);
+                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
+                      const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
+                      hipStream_t s);
 
 // Refinement select: per query, the ncand best of S_Q by (F' desc, V asc),
 // written in ascending V order; n_valid [nq].  scratch holds
@@ -115,6 +127,9 @@ struct chimera_index {
   uint8_t *d_codes = nullptr;
   int64_t *d_ivf_off = nullptr;
   int32_t *d_ivf_doc = nullptr;
+  int ndense = 0;                  // dense posting lists (see dense_lists)
+  int8_t *d_dense_slot = nullptr;  // [ncent]
+  uint64_t *d_doc_dense = nullptr;  // [ndocs] dense-list masks (see dense_lists)
   uint16_t h_weights[16] = {0};
   int32_t h_cut[15] = {0};
   // scratch arena, grown on demand, ordered across streams by scratch_done

@@ -70,11 +70,13 @@ __device__ __forceinline__ uint32_t fp_key(int32_t f) { return (uint32_t)f ^ 0x8
 // The query tokens whose rank-r centroid is the same form a group: the list
 // of the group's first token is walked once for all of them, with the
 // group's token mask and the sum of their scores S[j][c].
+// A group whose centroid has a dense list (see dense_lists) is not walked:
+// dslot is the centroid's bit in the documents' dense masks (-1 otherwise).
 template <typename MaskT>
 struct WalkList {
   int64_t beg;
   MaskT mask;
-  int32_t pos, len, next, gsum;
+  int32_t pos, len, next, gsum, dslot;
 };
 
 // One wave walks a list from pos up to the range's end d1, U blocks of 64
@@ -122,7 +124,9 @@ template <typename MaskT, int R>
 __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, int64_t nq, int Tq, int TQP,
     int nprobe, const int64_t *__restrict__ ivf_off, const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
-    int nranges, int G, int M, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
+    int ndense, const int8_t *__restrict__ dense_slot, const uint64_t *__restrict__ doc_dense, int nranges, int G,
+    int M, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
+  constexpr int DPT = R / WALK_THREADS;  // documents of a range each thread owns in the dense phase
   static_assert(R * sizeof(MaskT) >= SEL_BINS * 4, "the histogram reuses the mask array");
   extern __shared__ __align__(16) unsigned char walk_lds[];
   MaskT *smask = (MaskT *)walk_lds;                        // [R]
@@ -130,6 +134,10 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   WalkList<MaskT> *L = (WalkList<MaskT> *)(sfp + R);         // [nprobe][Tq]
   int32_t *skey = (int32_t *)(L + nprobe * Tq);              // [nprobe][Tq] S[j][c] keys
   int32_t *scid = skey + nprobe * Tq;                        // [nprobe][Tq] centroid ids
+  uint64_t *dset = (uint64_t *)(scid + nprobe * Tq);         // [nprobe] dense slots probed at each rank
+  int32_t *dcount = (int32_t *)(dset + nprobe);              // [nprobe] dense groups per rank
+  int8_t *dtab = (int8_t *)(dcount + nprobe);                // [kMaxDense] slot -> first token, current rank
+  int8_t *dlist = dtab + kMaxDense;                          // [nprobe][Tq] first tokens of the dense groups
   const int b = blockIdx.x;
   const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / G);
   const int g = (b >> 3) % G;
@@ -144,6 +152,10 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     scid[t] = cent_ids[e];
     skey[t] = cent_keys[e];
   }
+  for (int r = threadIdx.x; r < nprobe; r += WALK_THREADS) {
+    dcount[r] = 0;
+    dset[r] = 0;
+  }
   __syncthreads();
   for (int t = threadIdx.x; t < nl; t += WALK_THREADS) {
     const int r = t / Tq, j = t - r * Tq;
@@ -154,6 +166,7 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     w.len = 0;
     w.mask = 0;
     w.gsum = 0;
+    w.dslot = -1;
     // one pass over the rank's centroids: is j the group's first token, and
     // the group's mask and score sum
     bool head = (uint32_t)c < (uint32_t)ncent;
@@ -164,6 +177,15 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
       head = head && !(same && i < j);
       gm |= same ? (MaskT)1 << i : (MaskT)0;
       gs += same ? skey[r * Tq + i] : 0;
+    }
+    if (head && ndense > 0 && dense_slot[c] >= 0) {
+      // a dense list: applied from the documents' masks, never walked
+      dlist[r * Tq + atomicAdd(&dcount[r], 1)] = (int8_t)j;
+      atomicOr((unsigned long long *)&dset[r], 1ull << dense_slot[c]);
+      w.mask = gm;
+      w.gsum = gs;
+      w.dslot = dense_slot[c];
+      head = false;
     }
     if (head) {
       w.mask = gm;
@@ -186,8 +208,21 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
       smask[v] = 0;
       sfp[v] = 0;
     }
+    // dense-list masks of the documents this thread owns: tid + WALK_THREADS * i
+    uint64_t dm[DPT];
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int v = threadIdx.x + WALK_THREADS * i;
+      dm[i] = ndense > 0 && v < nd ? doc_dense[d0 + v] : 0;
+    }
     __syncthreads();  // the lists are set up; the previous range's reads are done
+
     for (int r = 0; r < nprobe; ++r) {
+      const int ndg = dcount[r];
+      if (threadIdx.x < ndg) {  // slot table of rank r; read after the barrier below
+        const int j = dlist[r * Tq + threadIdx.x];
+        dtab[L[r * Tq + j].dslot] = (int8_t)j;
+      }
       // list j of rank r is always walked by wave j % nwaves
       for (int j = wave; j < Tq; j += nwaves) {
         WalkList<MaskT> *w = &L[r * Tq + j];
@@ -207,7 +242,35 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
           w->next = next;
         }
       }
-      __syncthreads();  // rank r's LDS atomics complete before rank r+1's
+      if (ndg > 0) {  // uniform
+        // dense lists of rank r: each thread applies them to the documents it
+        // owns from their masks, without atomics (the sparse lists are done)
+        __syncthreads();
+        const uint64_t S = dset[r];
+#pragma unroll
+        for (int i = 0; i < DPT; ++i) {
+          uint64_t hits = dm[i] & S;
+          if (!hits) continue;
+          const int v = threadIdx.x + WALK_THREADS * i;
+          MaskT cur = smask[v];
+          int32_t add = 0;
+          do {
+            const WalkList<MaskT> &g = L[r * Tq + dtab[__builtin_ctzll(hits)]];
+            hits &= hits - 1;
+            const MaskT gmask = g.mask;
+            const MaskT fresh = gmask & ~cur;
+            cur |= fresh;
+            if (fresh == gmask) {
+              add += g.gsum;
+            } else {
+              for (MaskT m = fresh; m; m &= m - 1) add += skey[r * Tq + __builtin_ctzll((unsigned long long)m)];
+            }
+          } while (hits);
+          smask[v] = cur;
+          sfp[v] += add;
+        }
+      }
+      __syncthreads();  // rank r's LDS updates complete before rank r+1's
     }
     for (int v = threadIdx.x; v < nd; v += WALK_THREADS)
       if (smask[v] == 0) sfp[v] = NO_HIT;
@@ -229,10 +292,17 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   }
 }
 
+size_t walk_lds_bytes(int TQP, int nprobe, int Tq) {
+  const size_t mask = TQP == 32 ? 4 : 8, R = TQP == 32 ? 8192 : 4096;
+  const size_t list = TQP == 32 ? sizeof(WalkList<uint32_t>) : sizeof(WalkList<unsigned long long>);
+  return R * (mask + 4) + (size_t)nprobe * Tq * (list + 9) + (size_t)nprobe * 12 + kMaxDense;
+}
+
 template <typename MaskT, int R>
 static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
-                          const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
-                          uint32_t *hist, hipStream_t s) {
+                          const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
+                          const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
+                          hipStream_t s) {
   const int nranges = (int)((ndocs + R - 1) / R);
   // ranges per workgroup: enough groups per query for about 4096 workgroups
   int G = (int)std::min<int64_t>(nranges, std::max<int64_t>(1, (4096 + nq - 1) / nq));
@@ -240,25 +310,27 @@ static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int
   G = (nranges + M - 1) / M;
   const int64_t blocks = (nq + 7) / 8 * 8 * G;
   if (blocks == 0 || nranges == 0) return;
-  const size_t lds = (size_t)R * (sizeof(MaskT) + 4) + (size_t)nprobe * Tq * (sizeof(WalkList<MaskT>) + 8);
+  const size_t lds = walk_lds_bytes(TQP, nprobe, Tq);
   static bool attr = [] {
     return hipFuncSetAttribute((const void *)k_cand_walk<MaskT, R>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                160 * 1024) == hipSuccess;
   }();
   (void)attr;
   hipLaunchKernelGGL((k_cand_walk<MaskT, R>), dim3((unsigned)blocks), dim3(WALK_THREADS), lds, s, cent_ids, cent_keys,
-                     nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, nranges, G, M, fp, hist);
+                     nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense, dense_slot, doc_dense, nranges,
+                     G, M, fp, hist);
 }
 
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
-                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int32_t *fp,
-                      uint32_t *hist, hipStream_t s) {
+                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
+                      const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
+                      hipStream_t s) {
   if (TQP == 32)
-    launch_walk_t<uint32_t, 8192>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, fp, hist,
-                                  s);
+    launch_walk_t<uint32_t, 8192>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
+                                  dense_slot, doc_dense, fp, hist, s);
   else
     launch_walk_t<unsigned long long, 4096>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
-                                            fp, hist, s);
+                                            ndense, dense_slot, doc_dense, fp, hist, s);
 }
 
 // ------------------------------------------------------- block helpers

@@ -164,6 +164,7 @@ def test_validation_leaves_outputs_untouched():
         (dict(nprobe=0), chimera.E_INVAL), (dict(nprobe=1025), chimera.E_INVAL),
         (dict(nprobe=65), chimera.E_UNSUPPORTED), (dict(k=0), chimera.E_INVAL), (dict(k=20, ncand=10), chimera.E_INVAL),
         (dict(q_dtype=5), chimera.E_INVAL), (dict(nq=-1), chimera.E_INVAL), (dict(k=9000, ncand=9000), chimera.E_UNSUPPORTED),
+        (dict(Tq=64, nprobe=64), chimera.E_UNSUPPORTED),  # beyond the candidate walk's local memory
     ]
     for over, code in cases:
         a = dict(q_dtype=chimera.F32, nq=2, Tq=32, d=128, nprobe=2, ncand=256, k=10)
