@@ -336,6 +336,8 @@ void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t
 // ------------------------------------------------------- block helpers
 constexpr int SEL_THREADS = 1024;
 constexpr int SEL_ITEMS = 4;
+constexpr int SEL_UNROLL = 8;       // independent F' loads per thread in a histogram pass
+constexpr int SEL_COMPACT_ITEMS = 16;  // consecutive documents per thread in k_select's compaction
 
 // Exclusive prefix sum over the block; thread 0 leaves the block total in
 // *total (shared), readable by every thread once the call returns.
@@ -431,11 +433,18 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
       // pass 2: key bits 19..8 among keys with top bits b1
       for (int i = threadIdx.x; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0;
       __syncthreads();
-      for (int64_t v = threadIdx.x; v < ndocs; v += SEL_THREADS) {
-        const int32_t x = f[v];
-        if (x == NO_HIT) continue;
-        const uint32_t u = fp_key(x);
-        if ((u >> 20) == b1) atomicAdd(&hist[(u >> 8) & 4095u], 1u);
+      for (int64_t v0 = threadIdx.x; v0 < ndocs; v0 += SEL_THREADS * SEL_UNROLL) {
+        int32_t x[SEL_UNROLL];
+#pragma unroll
+        for (int i = 0; i < SEL_UNROLL; ++i) {
+          const int64_t v = v0 + (int64_t)i * SEL_THREADS;
+          x[i] = v < ndocs ? f[v] : NO_HIT;
+        }
+#pragma unroll
+        for (int i = 0; i < SEL_UNROLL; ++i) {
+          const uint32_t u = fp_key(x[i]);
+          if (x[i] != NO_HIT && (u >> 20) == b1) atomicAdd(&hist[(u >> 8) & 4095u], 1u);
+        }
       }
       __syncthreads();
       select_bin(hist, SEL_BINS, rem, wsum, &s_tot, &s_bin, &s_above);
@@ -444,11 +453,18 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
       // pass 3: key bits 7..0 among keys with top bits p2
       for (int i = threadIdx.x; i < 256; i += SEL_THREADS) hist[i] = 0;
       __syncthreads();
-      for (int64_t v = threadIdx.x; v < ndocs; v += SEL_THREADS) {
-        const int32_t x = f[v];
-        if (x == NO_HIT) continue;
-        const uint32_t u = fp_key(x);
-        if ((u >> 8) == p2) atomicAdd(&hist[u & 255u], 1u);
+      for (int64_t v0 = threadIdx.x; v0 < ndocs; v0 += SEL_THREADS * SEL_UNROLL) {
+        int32_t x[SEL_UNROLL];
+#pragma unroll
+        for (int i = 0; i < SEL_UNROLL; ++i) {
+          const int64_t v = v0 + (int64_t)i * SEL_THREADS;
+          x[i] = v < ndocs ? f[v] : NO_HIT;
+        }
+#pragma unroll
+        for (int i = 0; i < SEL_UNROLL; ++i) {
+          const uint32_t u = fp_key(x[i]);
+          if (x[i] != NO_HIT && (u >> 8) == p2) atomicAdd(&hist[u & 255u], 1u);
+        }
       }
       __syncthreads();
       select_bin(hist, 256, rem, wsum, &s_tot, &s_bin, &s_above);
@@ -460,13 +476,13 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
   // --- ordered compaction
   const int64_t base_out = MODE == 1 ? offsets[q] : q * (int64_t)ncand;
   long long written = 0, ties_seen = 0;
-  const int64_t chunk = (int64_t)SEL_THREADS * SEL_ITEMS;
+  const int64_t chunk = (int64_t)SEL_THREADS * SEL_COMPACT_ITEMS;
   for (int64_t c0 = 0; c0 < ndocs; c0 += chunk) {
-    const int64_t v0 = c0 + (int64_t)threadIdx.x * SEL_ITEMS;
+    const int64_t v0 = c0 + (int64_t)threadIdx.x * SEL_COMPACT_ITEMS;
     int take_flags = 0, tie_flags = 0, ntie = 0;
-    int32_t xs[SEL_ITEMS];
+    int32_t xs[SEL_COMPACT_ITEMS];
 #pragma unroll
-    for (int i = 0; i < SEL_ITEMS; ++i) {
+    for (int i = 0; i < SEL_COMPACT_ITEMS; ++i) {
       const int64_t v = v0 + i;
       xs[i] = v < ndocs ? f[v] : NO_HIT;
       if (xs[i] != NO_HIT) {
@@ -485,7 +501,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
       tie_total = s_tot;
     }
 #pragma unroll
-    for (int i = 0; i < SEL_ITEMS; ++i)
+    for (int i = 0; i < SEL_COMPACT_ITEMS; ++i)
       if (tie_flags & (1 << i)) {
         if (ties_seen + tie_rank < need) take_flags |= 1 << i;
         ++tie_rank;
@@ -493,7 +509,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
     long long pos = block_exclusive_scan(__popc(take_flags), wsum, &s_tot);
     const long long take_total = s_tot;
 #pragma unroll
-    for (int i = 0; i < SEL_ITEMS; ++i)
+    for (int i = 0; i < SEL_COMPACT_ITEMS; ++i)
       if (take_flags & (1 << i)) {
         if (MODE == 1 || written + pos < ncand) {
           out_ids[base_out + written + pos] = (int32_t)(v0 + i);

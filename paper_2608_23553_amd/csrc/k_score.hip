@@ -83,10 +83,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rs_rsrc(const void *p, uint32_
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-// value of lane 16*(l/16) + K for every lane l (DPP row_newbcast)
+// y of lane 16*(l/16) + K, plus a, for every lane l: one DPP add
+// (row_newbcast writes every lane, so the move needs no old value)
 template <int K>
-__device__ __forceinline__ int rs_row_bcast(int x) {
-  return __builtin_amdgcn_update_dpp(0, x, 0x150 + K, 0xF, 0xF, false);
+__device__ __forceinline__ uint32_t rs_row_bcast_add(uint32_t y, uint32_t a) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)y, 0x150 + K, 0xF, 0xF, true) + a;
 }
 // sum over the 32 lanes of each half wave, in lanes 31 and 63
 __device__ __forceinline__ int rs_half_sum(int v) {
@@ -107,6 +108,7 @@ struct RsWave {
   __amdgpu_buffer_rsrc_t st_rsrc;
   int64_t my_beg;
   int my_len, ndw, c, h, idrow, sentinel;
+  uint32_t hcol, l4;  // 64 * ((l >> 4) & 1) and 4 * (l & 15): 4 * c = hcol + l4
 
   // Cursor on document u of the wave (u >= ndw: past the end; those lanes
   // hold an empty document at token 0, so the cursor keeps reading valid,
@@ -125,14 +127,17 @@ struct RsWave {
     if (nb >= cu.len) set_doc(cu, cu.u + 1);
     else cu.base = nb;
   }
+  // tokens of the tile inside its document: the buffer ranges below end
+  // there, so rows past the document read 0 without touching memory
+  __device__ __forceinline__ uint32_t rows(const RsCur &cu) const { return (uint32_t)min(32, cu.len - cu.base); }
   // id of tile row idrow (the row D register l%16 holds in this lane's half)
   __device__ __forceinline__ int32_t load_id(const RsCur &cu) const {
-    const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + cu.beg + cu.base, 128);
+    const __amdgpu_buffer_rsrc_t r = rs_rsrc(cid + cu.beg + cu.base, 4 * rows(cu));
     return (int32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (uint32_t)(4 * idrow), 0, 0);
   }
   // this lane's half of token c's code: bytes CB/2 * h .. +CB/2
   __device__ __forceinline__ void load_codes(RsCodes<NBITS> &K, const RsCur &cu) const {
-    const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (cu.beg + cu.base) * CB, 32 * CB);
+    const __amdgpu_buffer_rsrc_t r = rs_rsrc(codes + (cu.beg + cu.base) * CB, CB * rows(cu));
     const uint32_t off = (uint32_t)(c * CB + (CB / 2) * h);
 #pragma unroll
     for (int p = 0; p < NBITS / 2; ++p) {
@@ -145,9 +150,12 @@ struct RsWave {
   // sentinel row
   __device__ __forceinline__ void gather(float (&st)[NCB][16], int32_t x, const RsCur &cu) const {
     x = cu.base + idrow < cu.len ? x : sentinel;
+    // byte offset of row x plus this lane's 16-lane group's first column;
+    // lane l reads that of lane 16*(l/16) + V and adds its own 4 * (l%16)
+    const uint32_t y = (uint32_t)x * (TQP * 4) + hcol;
 #define CHIMERA_G(V)                                                                                  \
   {                                                                                                   \
-    const uint32_t off = ((uint32_t)rs_row_bcast<V>(x) * TQP + c) * 4;                                \
+    const uint32_t off = rs_row_bcast_add<V>(y, l4);                                                  \
     _Pragma("unroll") for (int cb = 0; cb < NCB; ++cb) st[cb][V] =                                    \
         __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(st_rsrc, off + 128 * cb, 0, 0));         \
   }
@@ -199,6 +207,8 @@ __global__ __launch_bounds__(256) void k_residual_score(
   W.codes = codes;
   W.cid = cid;
   W.c = lane & 31;
+  W.hcol = 64 * ((lane >> 4) & 1);
+  W.l4 = 4 * (lane & 15);
   W.h = lane >> 5;
   // the row that D register k = l%16 holds in this lane's half
   W.idrow = 8 * ((lane & 15) >> 2) + 4 * W.h + (lane & 3);
@@ -252,6 +262,9 @@ __global__ __launch_bounds__(256) void k_residual_score(
     idm = W.load_id(c2);
     W.load_codes(kn, c1);
     W.gather(stn, x, c1);
+    // every load of tile t+1 is issued before tile t's products, so that
+    // the only wait below is for tile t itself
+    __builtin_amdgcn_sched_barrier(0);
     const int len = c0.len, cbase = c0.base;
     f32x16 acc[NCB];
 #pragma unroll
