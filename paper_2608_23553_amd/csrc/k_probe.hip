@@ -55,6 +55,63 @@ __device__ __forceinline__ void insert_desc(uint64_t (&L)[P], uint64_t K) {
   }
 }
 
+// Compare-exchange: a keeps the larger key.
+__device__ __forceinline__ void cx(uint64_t &a, uint64_t &b) {
+  const bool gt = b > a;
+  const uint64_t t = a;
+  a = gt ? b : a;
+  b = gt ? t : b;
+}
+
+// Bitonic sorting network, descending, on K[0 .. N).
+template <int N>
+__device__ __forceinline__ void bitonic_sort_desc(uint64_t *K) {
+#pragma unroll
+  for (int k = 2; k <= N; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          if ((i & k) == 0) cx(K[i], K[l]);
+          else cx(K[l], K[i]);
+        }
+      }
+}
+
+// A (sorted descending) becomes the top N of A and B (both sorted
+// descending): the elementwise maximum of A and reversed B is bitonic and
+// holds those N keys; a bitonic merge sorts it.
+template <int N>
+__device__ __forceinline__ void merge_top_desc(uint64_t *A, const uint64_t *B) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) A[i] = B[N - 1 - i] > A[i] ? B[N - 1 - i] : A[i];
+#pragma unroll
+  for (int j = N >> 1; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int l = i ^ j;
+      if (l > i) cx(A[i], A[l]);
+    }
+}
+
+// L (sorted descending, P keys) becomes the top P of L and the 16 keys K,
+// without branches: K is sorted in groups of P, the groups are merged
+// pairwise keeping the top P, and the winner is merged into L.
+template <int P>
+__device__ __forceinline__ void fold_tile(uint64_t (&L)[P], uint64_t (&K)[16]) {
+  static_assert(P == 4 || P == 8 || P == 16, "lists of 4, 8 or 16 keys");
+  constexpr int G = 16 / P;
+#pragma unroll
+  for (int g = 0; g < G; ++g) bitonic_sort_desc<P>(K + g * P);
+#pragma unroll
+  for (int step = 1; step < G; step <<= 1)
+#pragma unroll
+    for (int g = 0; g + step < G; g += 2 * step) merge_top_desc<P>(K + g * P, K + (g + step) * P);
+  merge_top_desc<P>(L, K);
+}
+
 // One workgroup: 32 query rows (one column block) x a range of centroid tiles.
 // Four waves stride over 32-centroid tiles; each wave computes a 32x32 tile
 // of S^T (rows = centroids, cols = query rows) with 8 MFMA 32x32x16 steps.
@@ -62,12 +119,18 @@ __device__ __forceinline__ void insert_desc(uint64_t (&L)[P], uint64_t K) {
 // dimension 64h + 8s + i for both operands (any common permutation of the
 // 128 dimensions gives the same exact sum), so every lane loads 128
 // contiguous bytes of its centroid row and of its query row.
-template <int PMAX, bool WRITE_ST>
-__global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, int TQP,
-                                               const uint16_t *__restrict__ cent, int ncent, int tiles_per_split,
-                                               int64_t rows, uint64_t *__restrict__ part, float *__restrict__ ST) {
+// Each lane keeps the sorted top PMAX keys of the centroids it sees.  Early in
+// its stream nearly every key enters some lane's list, and a tile's 16 keys go
+// in at once through sorting networks (lists of 4 to 16); lists of 4 or 8
+// switch, once a lane has seen 128 * PMAX keys and entries have become rare,
+// to inserting keys one by one where they beat the list's last, as lists of
+// 32 and 64 do throughout.
+template <int PMAX, int TQP, bool WRITE_ST>
+__global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, const uint16_t *__restrict__ cent,
+                                               int ncent, int tiles_per_split, int64_t rows,
+                                               uint64_t *__restrict__ part, float *__restrict__ ST) {
   __shared__ uint64_t lds[3][32][PMAX];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 31, h = lane >> 5;
   const int64_t qrow = (int64_t)blockIdx.x * 32 + col;
   const int split = blockIdx.y;
@@ -91,29 +154,57 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
   if (WRITE_ST && split == 0 && wave == 0 && h == 0) ST[st_base + (int64_t)ncent * TQP] = -INFINITY;
 
   for (int t = t0 + wave; t < t1; t += 4) {
-    const int crow = t * 32 + col;
+    // rows past the last centroid repeat it; their scores are dropped below
+    const int crow = min(t * 32 + col, ncent - 1);
     bf16x8 a[8];
-    if (crow < ncent) {
+    {
       const uint4 *cp = (const uint4 *)(cent + (int64_t)crow * 128 + 64 * h);
 #pragma unroll
       for (int s = 0; s < 8; ++s) a[s] = as_bf16x8(cp[s]);
-    } else {
-#pragma unroll
-      for (int s = 0; s < 8; ++s) a[s] = as_bf16x8(make_uint4(0, 0, 0, 0));
     }
+    __builtin_amdgcn_sched_barrier(0);  // the tile's 8 loads in flight together
     f32x16 acc;
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.f;
 #pragma unroll
     for (int s = 0; s < 8; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], bq[s], acc, 0, 0, 0);
-    // D layout: lane (col, h), register v holds centroid 8(v/4) + 4h + v%4 of the tile
+    // D layout: lane (col, h), register v holds centroid t*32 + 8(v/4) + 4h + v%4
+    const int cbase = t * 32 + 4 * h;
+    const bool full = t * 32 + 32 <= ncent;  // wave-uniform: only the last tile is partial
+    if (WRITE_ST) {
+      float *stp = ST + st_base + (int64_t)cbase * TQP;
+      if (full) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int c = t * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-      if (c < ncent) {
-        if (WRITE_ST) ST[st_base + (int64_t)c * TQP] = acc[v];
-        const uint64_t K = pack_key(to_key(acc[v]), (uint32_t)c);
-        if (K > L[PMAX - 1]) insert_desc<PMAX>(L, K);
+        for (int v = 0; v < 16; ++v) stp[(8 * (v >> 2) + (v & 3)) * TQP] = acc[v];
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (cbase + 8 * (v >> 2) + (v & 3) < ncent) stp[(8 * (v >> 2) + (v & 3)) * TQP] = acc[v];
+      }
+    }
+    // wave-uniform; lists of 16 stay on the networks throughout (measured faster)
+    const bool network = PMAX == 16 || (PMAX <= 8 && 16 * ((t - t0 - wave) / 4 + 1) <= 128 * PMAX);
+    if constexpr (PMAX <= 16) {
+      if (network) {
+        uint64_t K[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) K[v] = pack_key(to_key(acc[v]), (uint32_t)(cbase + 8 * (v >> 2) + (v & 3)));
+        if (!full) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (cbase + 8 * (v >> 2) + (v & 3) >= ncent) K[v] = 0;
+        }
+        fold_tile<PMAX>(L, K);
+      }
+    }
+    if (!network) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int c = cbase + 8 * (v >> 2) + (v & 3);
+        if (c < ncent) {
+          const uint64_t K = pack_key(to_key(acc[v]), (uint32_t)c);
+          if (K > L[PMAX - 1]) insert_desc<PMAX>(L, K);
+        }
       }
     }
   }
@@ -143,7 +234,7 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
 
 ProbePlan plan_probe(int64_t rows, int ncent, int nprobe) {
   ProbePlan p;
-  p.pmax = nprobe <= 8 ? 8 : nprobe <= 16 ? 16 : nprobe <= 32 ? 32 : 64;
+  p.pmax = nprobe <= 4 ? 4 : nprobe <= 8 ? 8 : nprobe <= 16 ? 16 : nprobe <= 32 ? 32 : 64;
   const int ntiles = (ncent + 31) / 32;
   const int64_t ncb = rows / 32;
   // aim at ~2048 workgroups, at least 4 tiles (one per wave) per split
@@ -159,24 +250,33 @@ ProbePlan plan_probe(int64_t rows, int ncent, int nprobe) {
 
 size_t probe_part_bytes(const ProbePlan &p, int64_t rows) { return (size_t)p.nsplit * rows * p.pmax * 8; }
 
-template <int P>
-static void launch_probe_t(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent,
-                           const ProbePlan &p, uint64_t *part, float *ST, hipStream_t s) {
+template <int P, int TQP>
+static void launch_probe_t(const uint16_t *Qs, int64_t rows, const uint16_t *cent, int ncent, const ProbePlan &p,
+                           uint64_t *part, float *ST, hipStream_t s) {
   dim3 grid((unsigned)(rows / 32), (unsigned)p.nsplit);
   if (ST)
-    hipLaunchKernelGGL((k_probe<P, true>), grid, dim3(256), 0, s, Qs, TQP, cent, ncent, p.tiles_per_split, rows, part, ST);
-  else
-    hipLaunchKernelGGL((k_probe<P, false>), grid, dim3(256), 0, s, Qs, TQP, cent, ncent, p.tiles_per_split, rows, part,
+    hipLaunchKernelGGL((k_probe<P, TQP, true>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows, part,
                        ST);
+  else
+    hipLaunchKernelGGL((k_probe<P, TQP, false>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows, part,
+                       ST);
+}
+
+template <int P>
+static void launch_probe_p(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent,
+                           const ProbePlan &p, uint64_t *part, float *ST, hipStream_t s) {
+  if (TQP == 32) launch_probe_t<P, 32>(Qs, rows, cent, ncent, p, part, ST, s);
+  else launch_probe_t<P, 64>(Qs, rows, cent, ncent, p, part, ST, s);
 }
 
 void launch_probe(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent, const ProbePlan &p,
                   uint64_t *part, float *ST, hipStream_t s) {
   switch (p.pmax) {
-    case 8: launch_probe_t<8>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    case 16: launch_probe_t<16>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    case 32: launch_probe_t<32>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    default: launch_probe_t<64>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 4: launch_probe_p<4>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 8: launch_probe_p<8>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 16: launch_probe_p<16>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 32: launch_probe_p<32>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    default: launch_probe_p<64>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
   }
 }
 
@@ -233,6 +333,7 @@ void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const
   const int64_t nrows = nq * Tq;
   dim3 grid((unsigned)((nrows + 3) / 4));
   switch (p.pmax) {
+    case 4: hipLaunchKernelGGL(k_probe_merge<4>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
     case 8: hipLaunchKernelGGL(k_probe_merge<8>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
     case 16: hipLaunchKernelGGL(k_probe_merge<16>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;
     case 32: hipLaunchKernelGGL(k_probe_merge<32>, grid, dim3(256), 0, s, part, nq, Tq, TQP, p.nsplit, nprobe, cent_ids, cent_keys); break;

@@ -100,7 +100,7 @@ def test_tiny_ragged_query_lengths(Tq):
 
 
 @pytest.mark.parametrize("nprobe,ncand,k", [(1, 1, 1), (64, 1000, 1000), (2, 5000, 200), (8, 300, 300),
-                                            (17, 999, 33)])
+                                            (16, 700, 50), (17, 999, 33)])
 def test_tiny_knob_extremes(nprobe, ncand, k):
     w, c, k_, cl, oi, idx = setup("tiny")
     q, _ = c.queries(6, 32, query_seed=7)
@@ -209,6 +209,23 @@ def test_100k_full_search():
     q, src = c.queries(w.nq, w.Tq)
     gi, _, _ = check_search(idx, oi, q, w.nprobe, w.ncand, w.k, "bf16", "100k")
     assert np.mean(gi[:, 0] == src) >= 0.9
+
+
+@pytest.mark.parametrize("nprobe", [3, 8, 16])
+def test_100k_probe_long_lane_streams(nprobe):
+    """2048 queries in one probe launch: every lane of the probe sees 2048
+    centroid keys, so lists of 4 and 8 pass from the sorting networks to key
+    by key insertion part way; sampled rows against the oracle."""
+    w, c, k, cl, oi, idx = setup("100k")
+    q, _ = c.queries(2048, w.Tq, query_seed=11)
+    say("probe 2048 queries", nprobe)
+    ci, ck = idx.probe(q_tensor(q, "bf16"), nprobe)
+    torch.cuda.synchronize()
+    ci, ck = ci.cpu().numpy(), ck.cpu().numpy()
+    for qi in (0, 1, 777, 1024, 1500, 2047):
+        ids, keys = oracle.probe(oracle.centroid_scores(q[qi], c.centroids_k), nprobe)
+        assert np.array_equal(ci[qi], ids), f"q{qi}: centroid ids differ"
+        assert np.array_equal(ck[qi].astype(np.int64), keys), f"q{qi}: centroid keys differ"
 
 
 def test_100k_prune_tap():
