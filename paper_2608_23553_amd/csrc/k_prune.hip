@@ -292,8 +292,15 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   }
 }
 
+// Documents per range: 8192 with 32-bit token masks, except when a query
+// walks 512 lists or more; then, as with 64-bit masks, 4096, which lets two
+// workgroups share a compute unit and hide each other's waits (measured: the
+// list setup and the per-rank barriers weigh more with many lists, the
+// per-range work with few).
+static int walk_range_docs(int TQP, int nprobe, int Tq) { return TQP == 32 && nprobe * Tq < 512 ? 8192 : 4096; }
+
 size_t walk_lds_bytes(int TQP, int nprobe, int Tq) {
-  const size_t mask = TQP == 32 ? 4 : 8, R = TQP == 32 ? 8192 : 4096;
+  const size_t mask = TQP == 32 ? 4 : 8, R = (size_t)walk_range_docs(TQP, nprobe, Tq);
   const size_t list = TQP == 32 ? sizeof(WalkList<uint32_t>) : sizeof(WalkList<unsigned long long>);
   return R * (mask + 4) + (size_t)nprobe * Tq * (list + 9) + (size_t)nprobe * 12 + kMaxDense;
 }
@@ -325,8 +332,11 @@ void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
                       const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
                       hipStream_t s) {
-  if (TQP == 32)
+  if (TQP == 32 && walk_range_docs(TQP, nprobe, Tq) == 8192)
     launch_walk_t<uint32_t, 8192>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
+                                  dense_slot, doc_dense, fp, hist, s);
+  else if (TQP == 32)
+    launch_walk_t<uint32_t, 4096>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
                                   dense_slot, doc_dense, fp, hist, s);
   else
     launch_walk_t<unsigned long long, 4096>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
