@@ -35,6 +35,7 @@ def _load():
         "orc_grid_bf16": ([P, I64, P], None),
         "orc_assign": ([P, I64, P, I32, I32, P, ctypes.c_int], None),
         "orc_ivf_docs": ([P, P, I64, I32, P, P], I64),
+        "orc_ivf_tokens": ([P, I64, I32, P, P], None),
         "orc_residual_hist": ([P, P, I64, P, I32, P], None),
         "orc_quantizer": ([P, ctypes.c_int, P, P], ctypes.c_int),
         "orc_encode": ([P, P, I64, P, I32, P, ctypes.c_int, P], None),
@@ -44,14 +45,15 @@ def _load():
         "orc_probe": ([P, I32, I32, I32, P, P], None),
         "orc_candidates": ([P, I32, I32, P, P, I64, P], I64),
         "orc_partial_scores": ([P, P, I32, I32, I32, P, P, I64, P, P], I64),
+        "orc_partial_scores_res": ([P, P, I32, I32, I32, P, I32, P, P, P, P, P, I64, P, P], I64),
         "orc_topk": ([P, P, I64, I64, P, P], I64),
         "orc_doc_scores": ([P, I32, I32, P, I32, P, I64, P, P, P, P, P], None),
         "orc_key_to_score": ([I64], ctypes.c_float),
         "orc_exact_chamfer": ([P, I32, I32, P, P, I64, P], None),
         "orc_search": ([P, I32, I32, P, I64, P, P, P, P, P, P, I64, I32, I32, I32, I32,
-                        P, P, P, P, P, P, P, P, ctypes.c_int], ctypes.c_int),
+                        P, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, ctypes.c_int], ctypes.c_int),
         "orc_prune_batch": ([P, I32, I32, I64, P, P, P, I64, I32, I32, I32, P, P, P, P, P, P,
-                             ctypes.c_int], ctypes.c_int),
+                             ctypes.c_int, P, P, P, P, P, ctypes.c_int], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -107,6 +109,21 @@ def ivf_docs(cid, doc_off, ncent: int):
     docs = np.empty(max(nnz, 1), dtype=np.int32)
     _load().orc_ivf_docs(_p(cid), _p(doc_off), ndocs, ncent, _p(off), _p(docs))
     return off, docs[:nnz]
+
+
+def ivf_tokens(cid, ncent: int):
+    """Token-level lists: (tok_off [ncent+1], ivf_tok [ntok]), tokens ascending."""
+    cid = _c(cid, np.int32)
+    off = np.empty(ncent + 1, dtype=np.int64)
+    tok = np.empty(max(cid.shape[0], 1), dtype=np.int32)
+    _load().orc_ivf_tokens(_p(cid), cid.shape[0], ncent, _p(off), _p(tok))
+    return off, tok[:cid.shape[0]]
+
+
+def token_docs(doc_off) -> np.ndarray:
+    """Document of every token (doc_off [ndocs+1])."""
+    doc_off = _c(doc_off, np.int64)
+    return np.repeat(np.arange(doc_off.shape[0] - 1, dtype=np.int32), np.diff(doc_off))
 
 
 def residual_hist(tok_k, cid, cent_k, hist=None) -> np.ndarray:
@@ -188,6 +205,20 @@ def partial_scores(S, cent_ids, ivf_off, ivf_doc, ndocs: int):
     return docs[:n].copy(), fp[:n].copy()
 
 
+def partial_scores_res(S, cent_ids, q_k, w_k, tok_off, ivf_tok, tok_doc, codes, ndocs: int):
+    """F' from the retrieved tokens' decoded scores (see orc_partial_scores_res)."""
+    S, cent_ids, q_k, w_k = _c(S, np.int64), _c(cent_ids, np.int32), _c(q_k, np.int16), _c(w_k, np.int32)
+    tok_off, ivf_tok, tok_doc = _c(tok_off, np.int64), _c(ivf_tok, np.int32), _c(tok_doc, np.int32)
+    codes = _c(codes, np.uint8)
+    Tq, ncent = S.shape
+    nprobe = cent_ids.shape[1]
+    docs = np.empty(max(ndocs, 1), dtype=np.int32)
+    fp = np.empty(max(ndocs, 1), dtype=np.int64)
+    n = _load().orc_partial_scores_res(_p(S), _p(cent_ids), Tq, ncent, nprobe, _p(q_k), q_k.shape[1], _p(w_k),
+                                       _p(tok_off), _p(ivf_tok), _p(tok_doc), _p(codes), ndocs, _p(docs), _p(fp))
+    return docs[:n].copy(), fp[:n].copy()
+
+
 def topk(ids, keys, k: int):
     ids, keys = _c(ids, np.int32), _c(keys, np.int64)
     n = ids.shape[0]
@@ -248,9 +279,27 @@ class OracleIndex:
         self.cut_k, self.w_k = quantizer(hist, nbits)
         self.codes = encode(tok_k, self.cid, self.cent_k, self.cut_k, nbits) if with_codes else None
         self.ivf_off, self.ivf_doc = ivf_docs(self.cid, self.doc_off, self.ncent)
+        self._tok = None
 
-    def search(self, q_k, nprobe: int, ncand: int, k: int, nthreads: int = 0):
-        """Full path for queries q_k [nq, Tq, dim]; returns a dict of arrays."""
+    def token_lists(self):
+        """(tok_off, ivf_tok, tok_doc), built on first use (refine 1 only)."""
+        if self._tok is None:
+            off, tok = ivf_tokens(self.cid, self.ncent)
+            self._tok = (off, tok, token_docs(self.doc_off))
+        return self._tok
+
+    def _refine_args(self, refine: bool):
+        if not refine:
+            return 0, None, None, None
+        if self.codes is None:
+            raise ValueError("refine mode scores retrieved tokens from their codes; build with codes")
+        off, tok, tdoc = self.token_lists()
+        return 1, off, tok, tdoc
+
+    def search(self, q_k, nprobe: int, ncand: int, k: int, nthreads: int = 0, refine: bool = False):
+        """Full path for queries q_k [nq, Tq, dim]; returns a dict of arrays.
+        refine: F' from the retrieved tokens' decoded scores instead of the
+        probed centroids' (orc_partial_scores_res)."""
         q_k = _c(q_k, np.int16)
         nq, Tq, dim = q_k.shape
         out = dict(
@@ -258,23 +307,26 @@ class OracleIndex:
             n_sq=np.empty(nq, np.int64), cand=np.full((nq, ncand), -1, np.int32),
             cand_keys=np.zeros((nq, ncand), np.int64), n_cand=np.empty(nq, np.int64),
             ids=np.empty((nq, k), np.int32), keys=np.empty((nq, k), np.int64))
+        rf, off, tok, tdoc = self._refine_args(refine)
         _load().orc_search(_p(self.cent_k), self.ncent, dim, _p(self.doc_off), self.ndocs, _p(self.cid),
                            _p(self.codes), _p(self.w_k), _p(self.ivf_off), _p(self.ivf_doc), _p(q_k), nq, Tq,
                            nprobe, ncand, k, _p(out["cent_ids"]), _p(out["cent_keys"]), _p(out["n_sq"]),
                            _p(out["cand"]), _p(out["cand_keys"]), _p(out["n_cand"]), _p(out["ids"]),
-                           _p(out["keys"]), nthreads)
+                           _p(out["keys"]), rf, _p(off), _p(tok), _p(tdoc), nthreads)
         out["scores"] = keys_to_scores(out["keys"])
         return out
 
-    def prune(self, q_k, nprobe: int, ncand: int, nthreads: int = 0):
+    def prune(self, q_k, nprobe: int, ncand: int, nthreads: int = 0, refine: bool = False):
         q_k = _c(q_k, np.int16)
         nq, Tq, dim = q_k.shape
         out = dict(
             cent_ids=np.empty((nq, Tq, nprobe), np.int32), cent_keys=np.empty((nq, Tq, nprobe), np.int64),
             n_sq=np.empty(nq, np.int64), cand=np.full((nq, ncand), -1, np.int32),
             cand_keys=np.zeros((nq, ncand), np.int64), n_cand=np.empty(nq, np.int64))
+        rf, off, tok, tdoc = self._refine_args(refine)
         _load().orc_prune_batch(_p(self.cent_k), self.ncent, dim, self.ndocs, _p(self.ivf_off), _p(self.ivf_doc),
                                 _p(q_k), nq, Tq, nprobe, ncand, _p(out["cent_ids"]), _p(out["cent_keys"]),
                                 _p(out["n_sq"]), _p(out["cand"]), _p(out["cand_keys"]), _p(out["n_cand"]),
-                                nthreads)
+                                rf, _p(self.w_k) if rf else None, _p(self.codes) if rf else None, _p(off), _p(tok),
+                                _p(tdoc), nthreads)
         return out

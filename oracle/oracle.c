@@ -96,6 +96,15 @@ int64_t orc_ivf_docs(const int32_t *cid, const int64_t *doc_off, int64_t ndocs, 
   return nnz;
 }
 
+void orc_ivf_tokens(const int32_t *cid, int64_t ntok, int32_t ncent, int64_t *tok_off, int32_t *ivf_tok) {
+  int64_t *fill = (int64_t *)calloc((size_t)ncent + 1, sizeof(int64_t));
+  for (int64_t t = 0; t < ntok; ++t) fill[cid[t] + 1]++;
+  for (int32_t c = 0; c < ncent; ++c) fill[c + 1] += fill[c];
+  memcpy(tok_off, fill, ((size_t)ncent + 1) * sizeof(int64_t));
+  for (int64_t t = 0; t < ntok; ++t) ivf_tok[fill[cid[t]]++] = (int32_t)t; /* ascending t */
+  free(fill);
+}
+
 /* ------------------------------------------------------------- quantiser */
 
 void orc_residual_hist(const int16_t *tok_k, const int32_t *cid, int64_t ntok, const int16_t *cent_k,
@@ -247,6 +256,40 @@ int64_t orc_partial_scores(const int64_t *S, const int32_t *cent_ids, int32_t Tq
   return n;
 }
 
+int64_t orc_partial_scores_res(const int64_t *S, const int32_t *cent_ids, int32_t Tq, int32_t ncent,
+                               int32_t nprobe, const int16_t *q_k, int32_t dim, const int32_t *w_k,
+                               const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
+                               const uint8_t *codes, int64_t ndocs, int32_t *docs, int64_t *fprime) {
+  int64_t *best = (int64_t *)malloc((size_t)ndocs * sizeof(int64_t));
+  int64_t *acc = (int64_t *)calloc((size_t)ndocs, sizeof(int64_t));
+  uint8_t *has = (uint8_t *)calloc((size_t)ndocs, 1);
+  uint8_t *in = (uint8_t *)calloc((size_t)ndocs, 1);
+  int32_t *touched = (int32_t *)malloc((size_t)ndocs * sizeof(int32_t));
+  for (int32_t j = 0; j < Tq; ++j) {
+    const int16_t *q = q_k + (int64_t)j * dim;
+    int64_t nt = 0;
+    for (int32_t r = 0; r < nprobe; ++r) {
+      int32_t c = cent_ids[(int64_t)j * nprobe + r];
+      for (int64_t p = tok_off[c]; p < tok_off[c + 1]; ++p) {
+        int64_t t = ivf_tok[p];
+        int64_t s = S[(int64_t)j * ncent + c];
+        for (int d = 0; d < dim; ++d) s += (int64_t)q[d] * (int64_t)w_k[codes[t * dim + d]];
+        int32_t v = tok_doc[t];
+        in[v] = 1;
+        if (!has[v]) { has[v] = 1; best[v] = s; touched[nt++] = v; }
+        else if (s > best[v]) best[v] = s;
+      }
+    }
+    /* V with no retrieved token for this j contributes 0 (not touched). */
+    for (int64_t i = 0; i < nt; ++i) { acc[touched[i]] += best[touched[i]]; has[touched[i]] = 0; }
+  }
+  int64_t n = 0;
+  for (int64_t v = 0; v < ndocs; ++v)
+    if (in[v]) { docs[n] = (int32_t)v; fprime[n] = acc[v]; ++n; }
+  free(best); free(acc); free(has); free(in); free(touched);
+  return n;
+}
+
 typedef struct { int64_t key; int32_t id; } kid;
 
 static int cmp_kid(const void *a, const void *b) {
@@ -307,13 +350,25 @@ void orc_exact_chamfer(const int16_t *q_k, int32_t Tq, int32_t dim, const int16_
 /* ---------------------------------------------------------- batch drivers */
 
 /* Probe, candidates, F' and top-ncand of one query; S is [Tq][ncent]. */
+/* What refine 1 needs besides the doc-level lists. */
+typedef struct {
+  int refine;
+  const int32_t *w_k;
+  const uint8_t *codes;
+  const int64_t *tok_off;
+  const int32_t *ivf_tok;
+  const int32_t *tok_doc;
+} refine_in;
+
 static int64_t prune_one(const int16_t *cent_k, int32_t ncent, int32_t dim, int64_t ndocs, const int64_t *ivf_off,
                          const int32_t *ivf_doc, const int16_t *q, int32_t Tq, int32_t nprobe, int32_t ncand,
-                         int64_t *S, int32_t *ci, int64_t *ck, int64_t *n_sq, int32_t *cand, int64_t *cand_keys,
-                         int32_t *docs, int64_t *fp) {
+                         const refine_in *rf, int64_t *S, int32_t *ci, int64_t *ck, int64_t *n_sq, int32_t *cand,
+                         int64_t *cand_keys, int32_t *docs, int64_t *fp) {
   orc_centroid_scores(q, Tq, cent_k, ncent, dim, S);
   orc_probe(S, Tq, ncent, nprobe, ci, ck);
-  int64_t nsq = orc_partial_scores(S, ci, Tq, ncent, nprobe, ivf_off, ivf_doc, ndocs, docs, fp);
+  int64_t nsq = rf->refine ? orc_partial_scores_res(S, ci, Tq, ncent, nprobe, q, dim, rf->w_k, rf->tok_off,
+                                                    rf->ivf_tok, rf->tok_doc, rf->codes, ndocs, docs, fp)
+                           : orc_partial_scores(S, ci, Tq, ncent, nprobe, ivf_off, ivf_doc, ndocs, docs, fp);
   if (n_sq) *n_sq = nsq;
   return orc_topk(docs, fp, nsq, ncand, cand, cand_keys);
 }
@@ -321,7 +376,9 @@ static int64_t prune_one(const int16_t *cent_k, int32_t ncent, int32_t dim, int6
 int orc_prune_batch(const int16_t *cent_k, int32_t ncent, int32_t dim, int64_t ndocs, const int64_t *ivf_off,
                     const int32_t *ivf_doc, const int16_t *q_k, int64_t nq, int32_t Tq, int32_t nprobe,
                     int32_t ncand, int32_t *cent_ids, int64_t *cent_keys, int64_t *n_sq, int32_t *cand,
-                    int64_t *cand_keys, int64_t *n_cand, int nthreads) {
+                    int64_t *cand_keys, int64_t *n_cand, int refine, const int32_t *w_k, const uint8_t *codes,
+                    const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc, int nthreads) {
+  const refine_in rf = {refine, w_k, codes, tok_off, ivf_tok, tok_doc};
 #ifdef _OPENMP
   if (nthreads <= 0) nthreads = omp_get_max_threads();
 #endif
@@ -336,7 +393,7 @@ int orc_prune_batch(const int16_t *cent_k, int32_t ncent, int32_t dim, int64_t n
     for (int64_t qi = 0; qi < nq; ++qi) {
       int64_t nsq = 0;
       int64_t nc = prune_one(cent_k, ncent, dim, ndocs, ivf_off, ivf_doc, q_k + qi * Tq * dim, Tq, nprobe, ncand,
-                             S, ci, ck, &nsq, cand + qi * ncand, cand_keys + qi * ncand, docs, fp);
+                             &rf, S, ci, ck, &nsq, cand + qi * ncand, cand_keys + qi * ncand, docs, fp);
       if (cent_ids) memcpy(cent_ids + qi * Tq * nprobe, ci, (size_t)Tq * nprobe * sizeof(int32_t));
       if (cent_keys) memcpy(cent_keys + qi * Tq * nprobe, ck, (size_t)Tq * nprobe * sizeof(int64_t));
       if (n_sq) n_sq[qi] = nsq;
@@ -352,7 +409,9 @@ int orc_search(const int16_t *cent_k, int32_t ncent, int32_t dim, const int64_t 
                const int32_t *ivf_doc, const int16_t *q_k, int64_t nq, int32_t Tq, int32_t nprobe,
                int32_t ncand, int32_t k, int32_t *cent_ids, int64_t *cent_keys, int64_t *n_sq,
                int32_t *cand, int64_t *cand_keys, int64_t *n_cand, int32_t *ids, int64_t *keys,
+               int refine, const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
                int nthreads) {
+  const refine_in rf = {refine, w_k, codes, tok_off, ivf_tok, tok_doc};
 #ifdef _OPENMP
   if (nthreads <= 0) nthreads = omp_get_max_threads();
 #endif
@@ -372,8 +431,8 @@ int orc_search(const int16_t *cent_k, int32_t ncent, int32_t dim, const int64_t 
     for (int64_t qi = 0; qi < nq; ++qi) {
       const int16_t *q = q_k + qi * Tq * dim;
       int64_t nsq = 0;
-      int64_t nc = prune_one(cent_k, ncent, dim, ndocs, ivf_off, ivf_doc, q, Tq, nprobe, ncand, S, ci, ck, &nsq,
-                             r, rk, docs, fp);
+      int64_t nc = prune_one(cent_k, ncent, dim, ndocs, ivf_off, ivf_doc, q, Tq, nprobe, ncand, &rf, S, ci, ck,
+                             &nsq, r, rk, docs, fp);
       if (cent_ids) memcpy(cent_ids + qi * Tq * nprobe, ci, (size_t)Tq * nprobe * sizeof(int32_t));
       if (cent_keys) memcpy(cent_keys + qi * Tq * nprobe, ck, (size_t)Tq * nprobe * sizeof(int64_t));
       if (n_sq) n_sq[qi] = nsq;

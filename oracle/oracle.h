@@ -44,6 +44,10 @@ void orc_assign(const int16_t *tok_k, int64_t ntok, const int16_t *cent_k, int32
  * [ncent+1]. Returns nnz. */
 int64_t orc_ivf_docs(const int32_t *cid, const int64_t *doc_off, int64_t ndocs, int32_t ncent,
                      int64_t *ivf_off, int32_t *ivf_doc);
+/* Token-level list of centroid c (Sec. 2.3, the IVF over token vectors): the
+ * tokens assigned to c in ascending token order.  tok_off is [ncent+1],
+ * ivf_tok [ntok]. */
+void orc_ivf_tokens(const int32_t *cid, int64_t ntok, int32_t ncent, int64_t *tok_off, int32_t *ivf_tok);
 
 /* ---- Residual quantiser (bucketed residual codes; the paper only names
  * residual compression among related systems, so this is the build's
@@ -86,6 +90,18 @@ int64_t orc_candidates(const int32_t *cent_ids, int32_t Tq, int32_t nprobe, cons
 int64_t orc_partial_scores(const int64_t *S, const int32_t *cent_ids, int32_t Tq, int32_t ncent,
                            int32_t nprobe, const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs,
                            int32_t *docs, int64_t *fprime);
+/* F'(V) of Sec. 3.2 (candidate refinement, Alg. 2) with each retrieved
+ * token's own score instead of its centroid's: the tokens L_j retrieved for
+ * query token j are those assigned to one of its probed centroids, and a
+ * retrieved token t scores as in document scoring, S[j][cid t] +
+ * sum_d q_jd w[code_td].  Per query token the max over V's retrieved tokens,
+ * 0 if V has none, summed over query tokens.  tok_doc[t] is t's document;
+ * codes are unpacked ([ntok][dim]).  docs/fprime need ndocs entries; returns
+ * |S_Q| with docs ascending (the same S_Q as orc_partial_scores). */
+int64_t orc_partial_scores_res(const int64_t *S, const int32_t *cent_ids, int32_t Tq, int32_t ncent,
+                               int32_t nprobe, const int16_t *q_k, int32_t dim, const int32_t *w_k,
+                               const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
+                               const uint8_t *codes, int64_t ndocs, int32_t *docs, int64_t *fprime);
 /* First min(k, n) of (key desc, id asc) (Alg. 1 topK; Alg. 2 last step).
  * Returns the count written. */
 int64_t orc_topk(const int32_t *ids, const int64_t *keys, int64_t n, int64_t k, int32_t *out_ids,
@@ -107,7 +123,10 @@ void orc_exact_chamfer(const int16_t *q_k, int32_t Tq, int32_t dim, const int16_
                        const int64_t *doc_off, int64_t ndocs, int64_t *F);
 
 /* Whole path for a batch of queries, in memory (Alg. 1 without the CPU
- * full-bit re-rank), OpenMP over queries only.  Per query q:
+ * full-bit re-rank), OpenMP over queries only.  refine 0 takes F' from the
+ * probed centroids' scores (orc_partial_scores), refine 1 from the retrieved
+ * tokens' decoded scores (orc_partial_scores_res, which needs tok_off,
+ * ivf_tok and tok_doc; they may be NULL otherwise).  Per query q:
  *   cent_ids/cent_keys [Tq][nprobe]   (may be NULL)
  *   n_sq[q] = |S_Q|                    (may be NULL)
  *   cand/cand_keys [ncand], n_cand[q]  (order: F' desc, doc asc; may be NULL)
@@ -118,14 +137,17 @@ int orc_search(const int16_t *cent_k, int32_t ncent, int32_t dim, const int64_t 
                const int32_t *ivf_doc, const int16_t *q_k, int64_t nq, int32_t Tq, int32_t nprobe,
                int32_t ncand, int32_t k, int32_t *cent_ids, int64_t *cent_keys, int64_t *n_sq,
                int32_t *cand, int64_t *cand_keys, int64_t *n_cand, int32_t *ids, int64_t *keys,
+               int refine, const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
                int nthreads);
 
 /* Only the prune half of orc_search (probe, candidates, F', top-ncand), for
- * corpora whose codes are produced on demand. */
+ * corpora whose codes are produced on demand (refine 0; w_k, codes and the
+ * token lists may then be NULL). */
 int orc_prune_batch(const int16_t *cent_k, int32_t ncent, int32_t dim, int64_t ndocs, const int64_t *ivf_off,
                     const int32_t *ivf_doc, const int16_t *q_k, int64_t nq, int32_t Tq, int32_t nprobe,
                     int32_t ncand, int32_t *cent_ids, int64_t *cent_keys, int64_t *n_sq, int32_t *cand,
-                    int64_t *cand_keys, int64_t *n_cand, int nthreads);
+                    int64_t *cand_keys, int64_t *n_cand, int refine, const int32_t *w_k, const uint8_t *codes,
+                    const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc, int nthreads);
 
 #ifdef __cplusplus
 }
