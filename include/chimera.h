@@ -56,6 +56,14 @@ enum {
 /* Element type of a query tensor. */
 enum { CHIMERA_F32 = 0, CHIMERA_BF16 = 1 };
 
+/* Score used by the candidate refinement (Sec. 3.2, the partial score F').
+ *   CHIMERA_REFINE_CENTROID: a retrieved token scores as its centroid,
+ *     S[j][c]; what chimera_search and chimera_prune do.
+ *   CHIMERA_REFINE_TOKEN: a retrieved token scores as document scoring
+ *     scores it, S[j][c] + <Q_j, w(code_t)> (centroid score plus its decoded
+ *     residual), the paper's use of the retrieved tokens' codes. */
+enum { CHIMERA_REFINE_CENTROID = 0, CHIMERA_REFINE_TOKEN = 1 };
+
 /* Limits of this build.  Besides these, the candidate walk keeps per-list
  * state for all Tq x nprobe probed lists of a query on chip: with more than
  * 32 query tokens, Tq * nprobe up to 2304 always fits (e.g. 64 x 32), and
@@ -179,6 +187,19 @@ int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out);
 int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
                    int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream);
 
+/* chimera_search with a choice of refinement score (Sec. 3.2 candidate
+ * refinement; Alg. 2).  refine CHIMERA_REFINE_CENTROID is chimera_search.
+ * refine CHIMERA_REFINE_TOKEN replaces step 3's F' by
+ *   F'(V) = sum_j max{ S[j][cid t] + <Q_j, w(code_t)> : t in V, cid t in C_j },
+ * a term being 0 when V has no such token: every token of a probed list is
+ * scored from its code (the index's token-level posting lists), so the work
+ * grows with the probed lists' token counts.  Other refine values return
+ * CHIMERA_E_INVAL; a Tq x nprobe whose per-list state exceeds the
+ * refinement's local memory (64 x 64) returns CHIMERA_E_UNSUPPORTED. */
+int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
+                          void *hip_stream);
+
 /* Stage taps: the same inputs as chimera_search, stopping after a stage.
  * They exist so that each stage can be compared with an independent
  * reference; they cost as much as the stages they run. */
@@ -201,6 +222,11 @@ int chimera_candidates(chimera_index *idx, const void *Q, int q_dtype, int64_t n
 int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
                   int32_t nprobe, int32_t ncand, int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid,
                   void *hip_stream);
+
+/* chimera_prune with the refinement score chosen as in chimera_search_refine. */
+int chimera_prune_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                         int32_t nprobe, int32_t ncand, int32_t refine, int32_t *cand_ids, int32_t *cand_keys,
+                         int32_t *n_valid, void *hip_stream);
 
 /* Per-stage device time of the searches run on this index since the last
  * call, in ms, measured with HIP events recorded on the search stream when

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "lib", "libchimera.so")
 
 OK, E_INVAL, E_NOMEM, E_IO, E_FORMAT, E_DEVICE, E_UNSUPPORTED, E_BUSY = range(8)
 F32, BF16 = 0, 1
+REFINE_CENTROID, REFINE_TOKEN = 0, 1
 _ERR_NAMES = {1: "INVAL", 2: "NOMEM", 3: "IO", 4: "FORMAT", 5: "DEVICE", 6: "UNSUPPORTED", 7: "BUSY"}
 
 _lib = None
@@ -60,9 +61,11 @@ def lib():
         "chimera_index_free": ([P], None),
         "chimera_index_info_get": ([P, P], INT),
         "chimera_search": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
+        "chimera_search_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_probe": ([P, P, INT, I64, I32, I32, I32, P, P, P], INT),
         "chimera_candidates": ([P, P, INT, I64, I32, I32, I32, P, P, I64, P], INT),
         "chimera_prune": ([P, P, INT, I64, I32, I32, I32, I32, P, P, P, P], INT),
+        "chimera_prune_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P, P], INT),
         "chimera_stage_times": ([P, P], INT),
     }
     for name, (args, res) in sig.items():
@@ -227,8 +230,10 @@ class Index:
         import torch
         return torch.device("cuda", self._info["device"])
 
-    def search(self, Q, nprobe: int, ncand: int, k: int, out=None, stream=None):
-        """Top-k (ids int32 [nq,k], scores float32 [nq,k]) for queries Q [nq,Tq,d]."""
+    def search(self, Q, nprobe: int, ncand: int, k: int, out=None, stream=None, refine: int = REFINE_CENTROID):
+        """Top-k (ids int32 [nq,k], scores float32 [nq,k]) for queries Q [nq,Tq,d].
+        refine: REFINE_CENTROID (chimera_search) or REFINE_TOKEN
+        (chimera_search_refine)."""
         import torch
         Q, dt = _q_args(Q)
         nq, Tq, d = Q.shape
@@ -237,9 +242,14 @@ class Index:
             scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
         else:
             ids, scores = out
-        _check(lib().chimera_search(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, k,
-                                    ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(scores.data_ptr()),
-                                    _stream_ptr(stream)))
+        if refine == REFINE_CENTROID:
+            _check(lib().chimera_search(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, k,
+                                        ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(scores.data_ptr()),
+                                        _stream_ptr(stream)))
+        else:
+            _check(lib().chimera_search_refine(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand,
+                                               k, refine, ctypes.c_void_p(ids.data_ptr()),
+                                               ctypes.c_void_p(scores.data_ptr()), _stream_ptr(stream)))
         return ids, scores
 
     def search_raw(self, q_ptr: int, q_dtype: int, nq: int, Tq: int, d: int, nprobe: int, ncand: int, k: int,
@@ -272,7 +282,7 @@ class Index:
                                         capacity, _stream_ptr(stream)))
         return offsets, doc_ids
 
-    def prune(self, Q, nprobe: int, ncand: int, stream=None):
+    def prune(self, Q, nprobe: int, ncand: int, stream=None, refine: int = REFINE_CENTROID):
         import torch
         Q, dt = _q_args(Q)
         nq, Tq, d = Q.shape
@@ -280,9 +290,15 @@ class Index:
         cand = torch.empty((nq, nc), dtype=torch.int32, device=Q.device)
         keys = torch.empty((nq, nc), dtype=torch.int32, device=Q.device)
         nval = torch.empty(nq, dtype=torch.int32, device=Q.device)
-        _check(lib().chimera_prune(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand,
-                                   ctypes.c_void_p(cand.data_ptr()), ctypes.c_void_p(keys.data_ptr()),
-                                   ctypes.c_void_p(nval.data_ptr()), _stream_ptr(stream)))
+        if refine == REFINE_CENTROID:
+            _check(lib().chimera_prune(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand,
+                                       ctypes.c_void_p(cand.data_ptr()), ctypes.c_void_p(keys.data_ptr()),
+                                       ctypes.c_void_p(nval.data_ptr()), _stream_ptr(stream)))
+        else:
+            _check(lib().chimera_prune_refine(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand,
+                                              refine, ctypes.c_void_p(cand.data_ptr()),
+                                              ctypes.c_void_p(keys.data_ptr()), ctypes.c_void_p(nval.data_ptr()),
+                                              _stream_ptr(stream)))
         return cand, keys, nval
 
     def stage_times(self) -> np.ndarray:

@@ -66,6 +66,9 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
     delete idx;
     return rc;
   }
+  std::vector<int64_t> tok_off;
+  std::vector<int32_t> ivf_tok, tok_doc;
+  token_lists(h, tok_off, ivf_tok, tok_doc);
   struct Sec { void **dst; const void *src; size_t bytes; } secs[] = {
       {(void **)&idx->d_cent, h.cent.data(), h.cent.size() * 2},
       {(void **)&idx->d_doc_off, h.doc_off.data(), h.doc_off.size() * 8},
@@ -75,6 +78,9 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
       {(void **)&idx->d_ivf_doc, h.ivf_doc.data(), h.ivf_doc.size() * 4},
       {(void **)&idx->d_dense_slot, dense_slot.data(), dense_slot.size()},
       {(void **)&idx->d_doc_dense, doc_dense.data(), doc_dense.size() * 8},
+      {(void **)&idx->d_tok_off, tok_off.data(), tok_off.size() * 8},
+      {(void **)&idx->d_ivf_tok, ivf_tok.data(), ivf_tok.size() * 4},
+      {(void **)&idx->d_tok_doc, tok_doc.data(), tok_doc.size() * 4},
   };
   size_t need = 0;
   for (auto &s : secs) need += s.bytes;
@@ -86,7 +92,9 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   // Token arrays (cid, codes) are followed by kTokenPad zeroed tokens: the
   // residual scorer reads whole 16-token tiles and may run up to 15 tokens
   // past the last document.  Every section gets at least 256 spare bytes.
-  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256, 256, 256};
+  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256, 256,
+                              256, 256, 256, 256};
+  static_assert(sizeof(pad_bytes) / sizeof(pad_bytes[0]) == sizeof(secs) / sizeof(secs[0]), "one pad per section");
   int si = 0;
   for (auto &s : secs) {
     const size_t pad = pad_bytes[si++];
@@ -112,7 +120,7 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
 
 // ----------------------------------------------------------- validation
 static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
-                            int32_t nprobe) {
+                            int32_t nprobe, int refine = CHIMERA_REFINE_CENTROID) {
   if (!idx) return fail(CHIMERA_E_INVAL, "null index");
   if (nq < 0) return fail(CHIMERA_E_INVAL, "nq must be >= 0");
   if (nq > 0 && !Q) return fail(CHIMERA_E_INVAL, "null query pointer");
@@ -124,6 +132,10 @@ static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype
   if (nprobe > CHIMERA_MAX_NPROBE) return fail(CHIMERA_E_UNSUPPORTED, "nprobe %d > %d", nprobe, CHIMERA_MAX_NPROBE);
   if (walk_lds_bytes(Tq <= 32 ? 32 : 64, nprobe, Tq) > kWalkMaxLds)
     return fail(CHIMERA_E_UNSUPPORTED, "Tq %d x nprobe %d exceeds the candidate walk's local memory", Tq, nprobe);
+  if (refine != CHIMERA_REFINE_CENTROID && refine != CHIMERA_REFINE_TOKEN)
+    return fail(CHIMERA_E_INVAL, "refine must be CHIMERA_REFINE_CENTROID or CHIMERA_REFINE_TOKEN");
+  if (refine == CHIMERA_REFINE_TOKEN && refine_lds_bytes(Tq <= 32 ? 32 : 64, nprobe, Tq) > kWalkMaxLds)
+    return fail(CHIMERA_E_UNSUPPORTED, "Tq %d x nprobe %d exceeds the token refinement's local memory", Tq, nprobe);
   return CHIMERA_OK;
 }
 
@@ -208,7 +220,7 @@ static void stage_mark(chimera_index *idx, hipStream_t s, bool on) {
 }
 
 static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int Tq, int nprobe, int ncand, int k,
-               Stop stop, Outs o, hipStream_t s) {
+               Stop stop, Outs o, hipStream_t s, int refine = CHIMERA_REFINE_CENTROID) {
   const int TQP = Tq <= 32 ? 32 : 64;
   // sub-batch size from the scratch budget
   const size_t perq = carve_bytes(idx, 1, TQP, nprobe, ncand, stop);
@@ -257,8 +269,12 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
     launch_fill_zero(hist, (size_t)nb * 4096 * 4, s);
-    launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent, idx->ndense,
-                     idx->d_dense_slot, idx->d_doc_dense, fp, hist, s);
+    if (refine == CHIMERA_REFINE_TOKEN)
+      launch_refine_walk(ci, ck, Qs, nb, Tq, TQP, nprobe, idx->d_tok_off, idx->d_ivf_tok, idx->d_tok_doc,
+                         idx->d_doc_off, idx->d_codes, idx->nbits, idx->h_weights, idx->ndocs, fp, hist, s);
+    else
+      launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent,
+                       idx->ndense, idx->d_dense_slot, idx->d_doc_dense, fp, hist, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_CANDIDATES) {
       int64_t *cnt = cv.take<int64_t>((size_t)nb + 1);
@@ -340,8 +356,9 @@ void chimera_index_free(chimera_index *idx) {
   if (!idx) return;
   DeviceGuard dg(idx->device);
   (void)hipDeviceSynchronize();
-  void *ptrs[] = {idx->d_cent,    idx->d_doc_off,    idx->d_cid,       idx->d_codes,  idx->d_ivf_off,
-                  idx->d_ivf_doc, idx->d_dense_slot, idx->d_doc_dense, idx->scratch};
+  void *ptrs[] = {idx->d_cent,    idx->d_doc_off,    idx->d_cid,       idx->d_codes,     idx->d_ivf_off,
+                  idx->d_ivf_doc, idx->d_dense_slot, idx->d_doc_dense, idx->d_tok_off,   idx->d_ivf_tok,
+                  idx->d_tok_doc, idx->scratch};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   if (idx->scratch_done) (void)hipEventDestroy(idx->scratch_done);
@@ -359,7 +376,14 @@ int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out) {
 
 int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
                    int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream) {
-  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  return chimera_search_refine(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, k, CHIMERA_REFINE_CENTROID, ids, scores,
+                               hip_stream);
+}
+
+int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
+                          void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe, refine);
   if (rc) return rc;
   if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
   if (ncand < k) return fail(CHIMERA_E_INVAL, "ncand (%d) must be >= k (%d)", ncand, k);
@@ -375,7 +399,7 @@ int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, i
   Outs o;
   o.ids = ids;
   o.scores = scores;
-  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream);
+  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine);
 }
 
 int chimera_probe(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
@@ -417,7 +441,14 @@ int chimera_candidates(chimera_index *idx, const void *Q, int q_dtype, int64_t n
 
 int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
                   int32_t ncand, int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, void *hip_stream) {
-  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  return chimera_prune_refine(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, CHIMERA_REFINE_CENTROID, cand_ids, cand_keys,
+                              n_valid, hip_stream);
+}
+
+int chimera_prune_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                         int32_t nprobe, int32_t ncand, int32_t refine, int32_t *cand_ids, int32_t *cand_keys,
+                         int32_t *n_valid, void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe, refine);
   if (rc) return rc;
   if (ncand < 1) return fail(CHIMERA_E_INVAL, "ncand must be >= 1");
   if (ncand > CHIMERA_MAX_NCAND) return fail(CHIMERA_E_UNSUPPORTED, "ncand %d > %d", ncand, CHIMERA_MAX_NCAND);
@@ -433,7 +464,7 @@ int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, in
   o.cand_ids = cand_ids;
   o.cand_keys = cand_keys;
   o.n_valid = n_valid;
-  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_PRUNE, o, (hipStream_t)hip_stream);
+  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_PRUNE, o, (hipStream_t)hip_stream, refine);
 }
 
 int chimera_stage_times(chimera_index *idx, float *ms6) {

@@ -216,6 +216,21 @@ int load_index(const char *path, HostIndex &h) {
   return CHIMERA_OK;
 }
 
+void token_lists(const HostIndex &h, std::vector<int64_t> &tok_off, std::vector<int32_t> &ivf_tok,
+                 std::vector<int32_t> &tok_doc) {
+  tok_off.assign((size_t)h.ncent + 1, 0);
+  for (int64_t t = 0; t < h.ntok; ++t) tok_off[(size_t)h.cid[t] + 1]++;
+  for (int32_t c = 0; c < h.ncent; ++c) tok_off[c + 1] += tok_off[c];
+  std::vector<int64_t> fill(tok_off.begin(), tok_off.end() - 1);
+  ivf_tok.resize((size_t)h.ntok);
+  for (int64_t t = 0; t < h.ntok; ++t) ivf_tok[fill[h.cid[t]]++] = (int32_t)t;  // ascending within a list
+  tok_doc.resize((size_t)h.ntok);
+  parallel_for(h.ndocs, [&](int64_t a, int64_t e) {
+    for (int64_t v = a; v < e; ++v)
+      for (int64_t t = h.doc_off[v]; t < h.doc_off[v + 1]; ++t) tok_doc[t] = (int32_t)v;
+  });
+}
+
 int dense_lists(const HostIndex &h, std::vector<int8_t> &slot, std::vector<uint64_t> &doc_mask, int &ndense) {
   slot.assign(h.ncent, -1);
   doc_mask.clear();

@@ -39,6 +39,23 @@ __device__ __forceinline__ int32_t to_key(float s) { return (int32_t)(s * KEY_SC
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
 
+// F' of a document outside the candidate set S_Q (a real F' is never this small).
+constexpr int NO_HIT = (int)0x80000000;
+// Bins of the first radix pass of the refinement select (top 12 key bits).
+constexpr int SEL_BINS = 4096;
+
+// Unsigned order key of a partial score: larger F' <-> larger key.
+__device__ __forceinline__ uint32_t fp_key(int32_t f) { return (uint32_t)f ^ 0x80000000u; }
+
+// First position p in [lo, hi) of the ascending array a with a[p] >= x.
+__device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a, int64_t lo, int64_t hi, int64_t x) {
+  while (lo < hi) {
+    const int64_t mid = lo + ((hi - lo) >> 1);
+    if ((int64_t)a[mid] < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
 template <class T>
 __device__ __forceinline__ T shfl_xor(T v, int m) {
   return __shfl_xor(v, m, 64);

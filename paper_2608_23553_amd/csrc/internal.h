@@ -51,6 +51,11 @@ int save_index(const HostIndex &h, const char *path);
 // disagrees with the list lengths.
 constexpr int kMaxDense = 64;
 int dense_lists(const HostIndex &h, std::vector<int8_t> &slot, std::vector<uint64_t> &doc_mask, int &ndense);
+// Token-level posting lists (refinement from decoded token scores): tok_off
+// [ncent+1], ivf_tok [ntok] the tokens of each centroid in ascending order,
+// tok_doc [ntok] each token's document.
+void token_lists(const HostIndex &h, std::vector<int64_t> &tok_off, std::vector<int32_t> &ivf_tok,
+                 std::vector<int32_t> &tok_doc);
 const HostIndex *builder_host(const chimera_builder *b);  // builds the lists on first use
 int load_index(const char *path, HostIndex &h);
 
@@ -102,6 +107,16 @@ void launch_count_hits(const int32_t *fp, int64_t nq, int64_t ndocs, int64_t *co
 void launch_list_hits(const int32_t *fp, int64_t nq, int64_t ndocs, const int64_t *offsets, int32_t *doc_ids,
                       hipStream_t s);
 
+// Refinement from the retrieved tokens' decoded scores: the same outputs as
+// launch_cand_walk (fp, hist added to), from token-level lists, the rounded
+// queries Qs [nq][TQP][128] and the probe's ids and keys.  The workgroup's
+// LDS is refine_lds_bytes (at most kWalkMaxLds).
+size_t refine_lds_bytes(int TQP, int nprobe, int Tq);
+void launch_refine_walk(const int32_t *cent_ids, const int32_t *cent_keys, const uint16_t *Qs, int64_t nq, int Tq,
+                        int TQP, int nprobe, const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
+                        const int64_t *doc_off, const uint8_t *codes, int nbits, const uint16_t *weights_host,
+                        int64_t ndocs, int32_t *fp, uint32_t *hist, hipStream_t s);
+
 // Residual scoring: fhat [nq][ncand] i32 keys of the kept documents; ST is
 // [nq][ncent + 1][TQP] (row ncent all -inf).
 void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,
@@ -130,6 +145,9 @@ struct chimera_index {
   int ndense = 0;                  // dense posting lists (see dense_lists)
   int8_t *d_dense_slot = nullptr;  // [ncent]
   uint64_t *d_doc_dense = nullptr;  // [ndocs] dense-list masks (see dense_lists)
+  int64_t *d_tok_off = nullptr;     // token-level lists (see token_lists)
+  int32_t *d_ivf_tok = nullptr;
+  int32_t *d_tok_doc = nullptr;
   uint16_t h_weights[16] = {0};
   int32_t h_cut[15] = {0};
   // scratch arena, grown on demand, ordered across streams by scratch_done

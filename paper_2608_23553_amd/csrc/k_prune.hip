@@ -50,19 +50,8 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
 // histogram, the first pass of the refinement select.  Workgroup b runs on
 // XCD b % 8; all groups of query q run on XCD q % 8.
 constexpr int WALK_THREADS = 512;
-constexpr int NO_HIT = (int)0x80000000;  // F' is never this small
-constexpr int SEL_BINS = 4096;
 
-__device__ __forceinline__ int64_t lower_bound_i32(const int32_t *__restrict__ a, int64_t lo, int64_t hi, int64_t x) {
-  while (lo < hi) {
-    const int64_t mid = lo + ((hi - lo) >> 1);
-    if ((int64_t)a[mid] < x) lo = mid + 1; else hi = mid;
-  }
-  return lo;
-}
 
-// Unsigned order key of a partial score: larger F' <-> larger key.
-__device__ __forceinline__ uint32_t fp_key(int32_t f) { return (uint32_t)f ^ 0x80000000u; }
 
 // Walk state of one probed list (rank r, query token j): entries
 // ivf_doc[beg .. beg + len), cursor pos and the document at the cursor

@@ -33,6 +33,10 @@ def test_null_arguments_are_rejected_without_gpu():
     assert L.chimera_probe(None, None, 0, 1, 32, 128, 2, None, None, None) == chimera.E_INVAL
     assert L.chimera_prune(None, None, 0, 1, 32, 128, 2, 10, None, None, None, None) == chimera.E_INVAL
     assert L.chimera_candidates(None, None, 0, 1, 32, 128, 2, None, None, 0, None) == chimera.E_INVAL
+    assert L.chimera_search_refine(None, None, 0, 1, 32, 128, 2, 256, 10, chimera.REFINE_TOKEN, None, None,
+                                   None) == chimera.E_INVAL
+    assert L.chimera_prune_refine(None, None, 0, 1, 32, 128, 2, 10, chimera.REFINE_TOKEN, None, None, None,
+                                  None) == chimera.E_INVAL
     assert L.chimera_index_info_get(None, None) == chimera.E_INVAL
     assert L.chimera_index_load(None, 0, None) == chimera.E_INVAL
     assert L.chimera_stage_times(None, None) == chimera.E_INVAL

@@ -42,11 +42,12 @@ def q_tensor(qk, dtype):
     return torch.from_numpy(synth.k_to_bf16_bits(qk).view(np.int16)).cuda().view(torch.bfloat16)
 
 
-def check_search(idx, oi, qk, nprobe, ncand, k, dtype="bf16", label=""):
-    say("search", label, qk.shape, nprobe, ncand, k, dtype)
-    ids, scores = idx.search(q_tensor(qk, dtype), nprobe, ncand, k)
+def check_search(idx, oi, qk, nprobe, ncand, k, dtype="bf16", label="", refine=False):
+    say("search", label, qk.shape, nprobe, ncand, k, dtype, "refine" if refine else "")
+    ids, scores = idx.search(q_tensor(qk, dtype), nprobe, ncand, k,
+                             refine=chimera.REFINE_TOKEN if refine else chimera.REFINE_CENTROID)
     torch.cuda.synchronize()
-    ref = oi.search(qk, nprobe, ncand, k)
+    ref = oi.search(qk, nprobe, ncand, k, refine=refine)
     gi, gs = ids.cpu().numpy(), scores.cpu().numpy()
     bad = np.nonzero((gi != ref["ids"]).any(axis=1))[0]
     assert bad.size == 0, f"{label}: ids differ for queries {bad[:8]}: gpu {gi[bad[0]][:8]} oracle {ref['ids'][bad[0]][:8]}"
@@ -237,6 +238,86 @@ def test_100k_prune_tap():
     ref = oi.prune(q, w.nprobe, w.ncand)
     cand, ckeys, nval = cand.cpu().numpy(), ckeys.cpu().numpy(), nval.cpu().numpy()
     for qi in range(32):
+        n = ref["n_cand"][qi]
+        assert nval[qi] == n
+        order = np.argsort(ref["cand"][qi, :n])
+        assert np.array_equal(cand[qi, :n], ref["cand"][qi, :n][order])
+        assert np.array_equal(ckeys[qi, :n].astype(np.int64), ref["cand_keys"][qi, :n][order])
+
+
+# ------------------------------------------- refinement from token scores
+# F' from each retrieved token's decoded score (chimera_search_refine /
+# chimera_prune_refine with CHIMERA_REFINE_TOKEN) against the oracle's
+# orc_partial_scores_res, then the same document scoring and top-k.
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_refine_token_search(dtype):
+    w, c, k, cl, oi, idx = setup("tiny")
+    q, src = c.queries(w.nq, w.Tq)
+    gi, _, _ = check_search(idx, oi, q, w.nprobe, w.ncand, w.k, dtype, "tiny refine", refine=True)
+    assert np.mean(gi[:, 0] == src) >= 0.9
+
+
+def test_tiny_refine_token_prune_tap():
+    w, c, k, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(w.nq, w.Tq, query_seed=5)
+    say("prune tap tiny refine")
+    cand, ckeys, nval = idx.prune(q_tensor(q, "bf16"), w.nprobe, w.ncand, refine=chimera.REFINE_TOKEN)
+    torch.cuda.synchronize()
+    cand, ckeys, nval = cand.cpu().numpy(), ckeys.cpu().numpy(), nval.cpu().numpy()
+    ref = oi.prune(q, w.nprobe, w.ncand, refine=True)
+    for qi in range(w.nq):
+        n = ref["n_cand"][qi]
+        assert nval[qi] == n
+        order = np.argsort(ref["cand"][qi, :n])
+        assert np.array_equal(cand[qi, :n], ref["cand"][qi, :n][order])
+        assert np.array_equal(ckeys[qi, :n].astype(np.int64), ref["cand_keys"][qi, :n][order])
+        assert np.all(cand[qi, n:] == -1)
+
+
+@pytest.mark.parametrize("Tq", [1, 7, 33, 64])
+def test_tiny_refine_token_ragged_query_lengths(Tq):
+    w, c, k, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(4, Tq, query_seed=40 + Tq)
+    check_search(idx, oi, q, 3, 100, 10, "bf16", f"tiny refine Tq={Tq}", refine=True)
+
+
+@pytest.mark.parametrize("nprobe,ncand,k", [(1, 1, 1), (64, 1000, 1000), (17, 999, 33)])
+def test_tiny_refine_token_knob_extremes(nprobe, ncand, k):
+    w, c, k_, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(4, 32, query_seed=8)
+    check_search(idx, oi, q, nprobe, ncand, k, "bf16", f"tiny refine np={nprobe} nc={ncand} k={k}", refine=True)
+
+
+def test_refine_token_long_doc_4bit_small():
+    w, c, k, cl, oi, idx = setup("2m-long", ndocs=800)
+    q, _ = c.queries(4, w.Tq)
+    check_search(idx, oi, q, w.nprobe, 2048, 200, "bf16", "2m-long recipe refine, 800 docs", refine=True)
+
+
+def test_refine_token_rejects_bad_mode_and_oversized_state():
+    w, c, k, cl, oi, idx = setup("tiny")
+    L = chimera.lib()
+    Q = q_tensor(c.queries(2, 64)[0], "bf16")
+    ids = torch.empty((2, 10), dtype=torch.int32, device="cuda")
+    sc = torch.empty((2, 10), dtype=torch.float32, device="cuda")
+    rc = L.chimera_search_refine(idx._h, Q.data_ptr(), chimera.BF16, 2, 64, 128, 2, 256, 10, 7, ids.data_ptr(),
+                                 sc.data_ptr(), None)
+    assert rc == chimera.E_INVAL
+    rc = L.chimera_search_refine(idx._h, Q.data_ptr(), chimera.BF16, 2, 64, 128, 64, 256, 10, chimera.REFINE_TOKEN,
+                                 ids.data_ptr(), sc.data_ptr(), None)
+    assert rc == chimera.E_UNSUPPORTED
+
+
+def test_100k_refine_token_search_and_prune_tap():
+    w, c, k, cl, oi, idx = setup("100k")
+    q, src = c.queries(64, w.Tq, query_seed=21)
+    gi, _, _ = check_search(idx, oi, q, w.nprobe, w.ncand, w.k, "bf16", "100k refine", refine=True)
+    assert np.mean(gi[:, 0] == src) >= 0.9
+    cand, ckeys, nval = idx.prune(q_tensor(q[:16], "bf16"), w.nprobe, w.ncand, refine=chimera.REFINE_TOKEN)
+    torch.cuda.synchronize()
+    cand, ckeys, nval = cand.cpu().numpy(), ckeys.cpu().numpy(), nval.cpu().numpy()
+    ref = oi.prune(q[:16], w.nprobe, w.ncand, refine=True)
+    for qi in range(16):
         n = ref["n_cand"][qi]
         assert nval[qi] == n
         order = np.argsort(ref["cand"][qi, :n])
