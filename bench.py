@@ -122,6 +122,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="100k")
     ap.add_argument("--nq", type=int, default=0, help="override the batch size")
+    ap.add_argument("--ncand", type=int, default=0, help="override the documents kept by the refinement")
+    ap.add_argument("--refine", choices=["centroid", "token"], default="centroid",
+                    help="refinement score: probed centroids' (chimera_search) or retrieved tokens' decoded "
+                         "scores (chimera_search_refine)")
     ap.add_argument("--latency-iters", type=int, default=300)
     ap.add_argument("--recall-queries", type=int, default=64)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample duration")
@@ -158,6 +162,10 @@ def main():
     w = synth.WORKLOADS[args.workload]
     if args.nq:
         w = w.scaled(nq=args.nq)
+    if args.ncand:
+        w = w.scaled(ncand=args.ncand)
+    from paper_2608_23553_amd import chimera as _ch
+    rmode = _ch.REFINE_TOKEN if args.refine == "token" else _ch.REFINE_CENTROID
     corpus, builder = build_corpus_index(w, threads)
     idx = builder.upload(0)
     info = idx.info()
@@ -168,13 +176,13 @@ def main():
 
     # ---- timed region: K whole-batch searches
     for _ in range(args.warmup):
-        idx.search(Q, w.nprobe, w.ncand, w.k, out=(ids, scores))
+        idx.search(Q, w.nprobe, w.ncand, w.k, out=(ids, scores), refine=rmode)
     torch.cuda.synchronize()
     idx.stage_times()  # clear warm-up events
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        idx.search(Q, w.nprobe, w.ncand, w.k, out=(ids, scores))
+        idx.search(Q, w.nprobe, w.ncand, w.k, out=(ids, scores), refine=rmode)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     st = idx.stage_times()
@@ -190,19 +198,33 @@ def main():
 
     # ---- algorithmic work of one step, from the stage taps and host copies
     ci, _ = idx.probe(Q, w.nprobe)
-    cand, _, nval = idx.prune(Q, w.nprobe, w.ncand)
+    cand, _, nval = idx.prune(Q, w.nprobe, w.ncand, refine=rmode)
     torch.cuda.synchronize()
     sec = builder.sections()
     lens = np.diff(sec["doc_off"])
     ci = ci.cpu().numpy()
     list_len = np.diff(sec["ivf_off"])
-    entries = int(list_len[ci].sum())
+    entries = int(list_len[ci].sum())  # every probed (token, centroid) list, as the paper counts them
+    # what the walk reads: each rank's distinct centroids once per query, except
+    # the dense lists (up to 64 lists holding more than ndocs/16 docs, longest
+    # first, ties to the lower id), which it applies from 8-byte per-doc masks
+    dense_c = np.nonzero(list_len * 16 > w.ndocs)[0]
+    dense_c = dense_c[np.lexsort((dense_c, -list_len[dense_c]))][:64]
+    walked_len = list_len.copy()
+    walked_len[dense_c] = 0
+    walked = sum(int(walked_len[np.unique(ci[q, :, r])].sum()) for q in range(w.nq) for r in range(w.nprobe))
+    walk_bytes = 4.0 * walked + (8.0 if len(dense_c) else 0.0) * w.nq * w.ndocs + 4.0 * w.nq * w.ndocs
+    if rmode == _ch.REFINE_TOKEN:
+        # every token of every probed list: its id, its document and its code
+        tok_len = np.bincount(sec["cid"], minlength=w.ncent)
+        walked = int(tok_len[ci].sum())
+        walk_bytes = (8.0 + 16 * w.nbits) * walked + 4.0 * w.nq * w.ndocs
     cand, nval = cand.cpu().numpy(), nval.cpu().numpy()
     scored_tokens = int(sum(lens[cand[q, :nval[q]]].sum() for q in range(w.nq)))
     code_bytes_tok = 16 * w.nbits + 4
     work = {
         "probe": ("mfma", 2.0 * w.nq * w.Tq * w.ncent * 128, BF16_PEAK_TFLOPS, "TFLOP/s"),
-        "walk": ("hbm", 4.0 * entries, HBM_PEAK_GBS, "GB/s"),
+        "walk": ("hbm", walk_bytes, HBM_PEAK_GBS, "GB/s"),
         "select": ("hbm", 8.0 * w.nq * w.ndocs, HBM_PEAK_GBS, "GB/s"),
         "score": ("hbm", float(code_bytes_tok * scored_tokens), HBM_PEAK_GBS, "GB/s"),
         "topk": ("hbm", 8.0 * int(nval.sum()), HBM_PEAK_GBS, "GB/s"),
@@ -213,7 +235,9 @@ def main():
     per_launch_s = stage_ms[dominant] * args.steps / launches / 1e3
     per_launch_amount = amount * args.steps / launches
     achieved = per_launch_amount / per_launch_s / (1e12 if unit == "TFLOP/s" else 1e9)
-    traffic = measured_traffic(dominant, w.name)
+    # the committed counter summary describes the default configuration only
+    default_cfg = not (args.nq or args.ncand or args.refine != "centroid")
+    traffic = measured_traffic(dominant, w.name) if default_cfg else None
     roofline = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
                 "traffic": traffic, "kernel": KERNEL_OF_STAGE[dominant],
                 "per_launch": {"algorithmic": per_launch_amount, "ms": per_launch_s * 1e3}}
@@ -230,14 +254,14 @@ def main():
     h_ids = torch.empty((1, w.k), dtype=torch.int32).pin_memory()
     h_sc = torch.empty((1, w.k), dtype=torch.float32).pin_memory()
     for i in range(5):
-        idx.search(dq.copy_(host_q[i:i + 1]), w.nprobe, w.ncand, w.k, out=(o_ids, o_sc))
+        idx.search(dq.copy_(host_q[i:i + 1]), w.nprobe, w.ncand, w.k, out=(o_ids, o_sc), refine=rmode)
     torch.cuda.synchronize()
     idx.stage_times()
     lat = []
     for i in range(nlat):
         s = time.perf_counter()
         dq.copy_(host_q[i:i + 1], non_blocking=True)
-        idx.search(dq, w.nprobe, w.ncand, w.k, out=(o_ids, o_sc))
+        idx.search(dq, w.nprobe, w.ncand, w.k, out=(o_ids, o_sc), refine=rmode)
         h_ids.copy_(o_ids, non_blocking=True)
         h_sc.copy_(o_sc, non_blocking=True)
         torch.cuda.synchronize()
@@ -262,11 +286,11 @@ def main():
         del tk
         probe_n = min(w.nq, max(1, threads))  # one query per thread
         s = time.perf_counter()
-        oi.search(q_k[:probe_n], w.nprobe, w.ncand, w.k, nthreads=threads)
+        oi.search(q_k[:probe_n], w.nprobe, w.ncand, w.k, nthreads=threads, refine=args.refine == "token")
         t_probe = time.perf_counter() - s
         n_cpu = int(min(w.nq, max(probe_n, probe_n * args.cpu_seconds / max(t_probe, 1e-3) // probe_n * probe_n)))
         s = time.perf_counter()
-        ref = oi.search(q_k[:n_cpu], w.nprobe, w.ncand, w.k, nthreads=threads)
+        ref = oi.search(q_k[:n_cpu], w.nprobe, w.ncand, w.k, nthreads=threads, refine=args.refine == "token")
         t_cpu = time.perf_counter() - s
         agree = bool(np.array_equal(ref["ids"], ids[:n_cpu].cpu().numpy()))
         cpu = {"value": n_cpu / t_cpu, "unit": "queries/s", "cores": threads, "kind": "oracle",
@@ -280,12 +304,13 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": describe(w), "ndocs": w.ndocs, "ntokens": info["ntokens"], "ncent": w.ncent,
                    "nbits": w.nbits, "nq": w.nq, "Tq": w.Tq, "nprobe": w.nprobe, "ncand": w.ncand, "k": w.k,
+                   "refine": args.refine,
                    "index_device_bytes": info["device_bytes"]},
         "recall_at_k": recall, "recall_queries": nr, "source_doc_top1": src_first,
         "p50_ms_nq1": float(np.percentile(lat, 50)), "p95_ms_nq1": float(np.percentile(lat, 95)),
         "p99_ms_nq1": float(np.percentile(lat, 99)), "nq1_stages_ms": lat_stage_ms,
         "code_scan_GBps": score_gbs, "probe_TFLOPs": probe_tflops, "stages_ms": stage_ms,
-        "work_per_step": {"posting_entries": entries, "scored_tokens": scored_tokens,
+        "work_per_step": {"posting_entries": entries, "posting_entries_walked": walked, "scored_tokens": scored_tokens,
                           "candidates": int(nval.sum())},
         "roofline": roofline, "cpu_baseline": cpu,
     }

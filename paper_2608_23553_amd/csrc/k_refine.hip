@@ -14,11 +14,15 @@
 // token), LDS `m[j][v]`, since a decoded score is not decided by the rank of
 // its list.  Every probed list (j, r) is token-level (ascending token ids,
 // hence ascending documents) with a cursor that only moves forward; all lists
-// are walked in any order (maxima commute), one entry per lane: the lane
-// decodes the token's code bytes through the byte-indexed weight table and
-// takes the dot product with q_j two dimensions at a time (v_dot2 on bf16
-// pairs; on the value grid every product and partial sum is an exact fp32
-// value, so the key is exact), then one LDS atomic max.  The range then sums
+// are walked in any order (maxima commute).  A list expected to hold at most
+// 32 entries per range is walked by one lane (one list per thread, so the
+// lists' memory latencies overlap, and q_j stays in that lane's registers
+// across ranges); longer lists are walked by a whole wave, one entry per
+// lane.  Per entry the lane decodes the token's code bytes through the
+// byte-indexed weight table and takes the dot product with q_j two
+// dimensions at a time (v_dot2 on bf16 pairs; on the value grid every product
+// and partial sum is an exact fp32 value, so the key is exact), then one LDS
+// atomic max.  The range then sums
 // its rows into F' (or NO_HIT), writes them, and adds its histogram of the top
 // 12 key bits, the same outputs as the centroid-only walk, so the select,
 // document scoring and top-k that follow are shared.
@@ -45,6 +49,39 @@ struct RefList {
   int32_t len, pos, next, skey;
 };
 
+// Key of token t for query token j: S[j][c] + <q_j, w[codes t]>, q_j as 64
+// bf16 pairs (dimensions 2i, 2i+1 in word i).
+template <int NBITS>
+__device__ __forceinline__ int32_t token_key(const uint8_t *__restrict__ codes, int32_t t, const uint32_t (&qv)[64],
+                                             const uint32_t *lut, int32_t skey) {
+  constexpr int CB = 16 * NBITS;
+  const uint4 *cp = (const uint4 *)(codes + (int64_t)t * CB);
+  float acc = 0.f;
+#pragma unroll
+  for (int u = 0; u < CB / 16; ++u) {
+    const uint4 c4 = cp[u];
+    const uint32_t cw[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const uint32_t byte = (cw[k >> 2] >> (8 * (k & 3))) & 255u;
+      const int bi = 16 * u + k;  // code byte index
+      if (NBITS == 2) {
+        // byte bi holds dimensions 4bi .. 4bi+3: q pairs 2bi, 2bi+1
+        const uint2 wv = *(const uint2 *)&lut[2 * byte];
+        acc = dot2(wv.x, qv[2 * bi], acc);
+        acc = dot2(wv.y, qv[2 * bi + 1], acc);
+      } else {
+        // byte bi holds dimensions 2bi, 2bi+1: q pair bi
+        acc = dot2(lut[byte], qv[bi], acc);
+      }
+    }
+  }
+  return skey + to_key(acc);
+}
+
+// A list walked by one lane: expected entries per range at most this.
+constexpr int REF_LANE_ENTRIES = 32;
+
 // Documents per range: the state m is TQP x RR int32, 64 KiB.
 template <int TQP>
 constexpr int ref_range_docs() { return 16384 / TQP; }
@@ -57,13 +94,15 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     uint4 w_lo, uint4 w_hi, int64_t ndocs, int nranges, int G, int M, int32_t *__restrict__ fp,
     uint32_t *__restrict__ hist) {
   constexpr int RR = ref_range_docs<TQP>();
-  constexpr int CB = 16 * NBITS;  // code bytes per token
   static_assert(RR * TQP >= SEL_BINS, "the histogram reuses the state array");
   extern __shared__ __align__(16) unsigned char ref_lds[];
   int32_t *m = (int32_t *)ref_lds;                         // [TQP][RR]: query token major
   int32_t *sfp = m + RR * TQP;                             // [RR]
   uint32_t *lut = (uint32_t *)(sfp + RR);                  // [256][NBITS == 2 ? 2 : 1]
   RefList *L = (RefList *)(lut + 256 * (NBITS == 2 ? 2 : 1));  // [nprobe * Tq], list i = r * Tq + j
+  int32_t *wide = (int32_t *)(L + nprobe * Tq);                 // [nprobe * Tq] lists walked by a wave
+  int32_t &s_nwide = wide[nprobe * Tq];                         // their number
+  // (all of it in the dynamic allocation: the launch asks for the whole LDS)
 
   const int b = blockIdx.x;
   const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / G);
@@ -92,6 +131,8 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
   }
   // list cursors, positioned at the group's first token
   const int nl = nprobe * Tq;
+  if (threadIdx.x == 0) s_nwide = 0;
+  __syncthreads();
   const int64_t tstart = doc_off[(int64_t)rg0 * RR];
   for (int i = threadIdx.x; i < nl; i += REF_THREADS) {
     const int r = i / Tq, j = i - r * Tq;
@@ -105,8 +146,14 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     w.pos = (int32_t)(p - beg);
     w.next = w.pos < w.len ? ivf_tok[p] : INT32_MAX;
     w.skey = cent_keys[e];
+    if ((int64_t)w.len * RR > (int64_t)REF_LANE_ENTRIES * ndocs) {
+      wide[atomicAdd(&s_nwide, 1)] = i;
+      w.len = -w.len;  // marks a list walked by a wave
+    }
     L[i] = w;
   }
+  int32_t qj = -1;  // the query token whose q this thread holds
+  uint32_t qv[64];
 
   for (int rg = rg0; rg < rg1; ++rg) {
     const int64_t d0 = (int64_t)rg * RR;
@@ -116,47 +163,58 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     for (int i = threadIdx.x; i < RR * TQP; i += REF_THREADS) m[i] = NO_HIT;
     __syncthreads();  // cursors, table and state ready; the previous range's reads done
 
-    for (int i = wave; i < nl; i += nwaves) {
+    // lists walked by one lane each
+    for (int i = threadIdx.x; i < nl; i += REF_THREADS) {
+      RefList *w = &L[i];
+      int32_t t = w->next;
+      if (t >= t1 || w->len < 0) continue;
+      const int j = i % Tq;
+      if (j != qj) {
+        const uint4 *qp = (const uint4 *)(Qs + (q * TQP + j) * 128);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const uint4 x = qp[k];
+          qv[4 * k] = x.x; qv[4 * k + 1] = x.y; qv[4 * k + 2] = x.z; qv[4 * k + 3] = x.w;
+        }
+        qj = j;
+      }
+      const int32_t len = w->len, skey = w->skey;
+      const int32_t *list = ivf_tok + w->beg;
+      int32_t pos = w->pos;
+      do {
+        const int32_t tn = pos + 1 < len ? list[pos + 1] : INT32_MAX;  // next entry, loaded early
+        const int32_t key = token_key<NBITS>(codes, t, qv, lut, skey);
+        atomicMax(&m[j * RR + (tok_doc[t] - (int)d0)], key);
+        ++pos;
+        t = tn;
+      } while (t < t1);
+      w->pos = pos;
+      w->next = t;
+    }
+    // lists walked by a whole wave, one entry per lane
+    const int nwide = s_nwide;
+    for (int wi = wave; wi < nwide; wi += nwaves) {
+      const int i = wide[wi];
       RefList *w = &L[i];
       if (w->next >= t1) continue;  // wave-uniform: nothing of this list in the range
       const int j = i % Tq;
-      const int32_t len = w->len, skey = w->skey;
+      const int32_t len = -w->len, skey = w->skey;
       const int32_t *list = ivf_tok + w->beg;
-      // q_j as bf16 pairs, the same for every lane
-      const uint32_t *qw = (const uint32_t *)(Qs + (q * TQP + j) * 128);
-      uint32_t qv[64];
+      {  // q_j into the lane's q registers (their cached token is dropped)
+        const uint4 *qp = (const uint4 *)(Qs + (q * TQP + j) * 128);
 #pragma unroll
-      for (int k = 0; k < 64; ++k) qv[k] = qw[k];
+        for (int k = 0; k < 16; ++k) {
+          const uint4 x = qp[k];
+          qv[4 * k] = x.x; qv[4 * k + 1] = x.y; qv[4 * k + 2] = x.z; qv[4 * k + 3] = x.w;
+        }
+        qj = -1;
+      }
       int32_t pos = w->pos, next = INT32_MAX;
       for (;;) {
         const int32_t p = pos + lane;
         const int32_t t = p < len ? list[p] : INT32_MAX;
         const bool in = t < t1;
-        if (in) {
-          const uint4 *cp = (const uint4 *)(codes + (int64_t)t * CB);
-          float acc = 0.f;
-#pragma unroll
-          for (int u = 0; u < CB / 16; ++u) {
-            const uint4 c4 = cp[u];
-            const uint32_t cw[4] = {c4.x, c4.y, c4.z, c4.w};
-#pragma unroll
-            for (int k = 0; k < 16; ++k) {
-              const uint32_t byte = (cw[k >> 2] >> (8 * (k & 3))) & 255u;
-              const int bi = 16 * u + k;  // code byte index
-              if (NBITS == 2) {
-                // byte bi holds dimensions 4bi .. 4bi+3: q pairs 2bi, 2bi+1
-                const uint2 wv = *(const uint2 *)&lut[2 * byte];
-                acc = dot2(wv.x, qv[2 * bi], acc);
-                acc = dot2(wv.y, qv[2 * bi + 1], acc);
-              } else {
-                // byte bi holds dimensions 2bi, 2bi+1: q pair bi
-                acc = dot2(lut[byte], qv[bi], acc);
-              }
-            }
-          }
-          const int v = tok_doc[t] - (int)d0;
-          atomicMax(&m[j * RR + v], skey + to_key(acc));
-        }
+        if (in) atomicMax(&m[j * RR + (tok_doc[t] - (int)d0)], token_key<NBITS>(codes, t, qv, lut, skey));
         const unsigned long long out = __ballot(!in);
         if (out) {
           const int first = __ffsll((long long)out) - 1;
@@ -204,7 +262,7 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
 
 size_t refine_lds_bytes(int TQP, int nprobe, int Tq) {
   const size_t RR = 16384 / TQP;
-  return RR * TQP * 4 + RR * 4 + 256 * 8 + (size_t)nprobe * Tq * sizeof(RefList);
+  return RR * TQP * 4 + RR * 4 + 256 * 8 + (size_t)nprobe * Tq * (sizeof(RefList) + 4) + 4;
 }
 
 template <int NBITS, int TQP>

@@ -323,3 +323,14 @@ def test_100k_refine_token_search_and_prune_tap():
         order = np.argsort(ref["cand"][qi, :n])
         assert np.array_equal(cand[qi, :n], ref["cand"][qi, :n][order])
         assert np.array_equal(ckeys[qi, :n].astype(np.int64), ref["cand_keys"][qi, :n][order])
+
+
+@pytest.mark.parametrize("refine", [False, True])
+def test_zipf_small_hot_lists(refine):
+    """The 1M recipe (Zipf(1.1) centroids) at 3,000 documents: the hot
+    centroids' lists hold a large share of every range, so the centroid-only
+    walk applies them from the per-document masks and the token refinement
+    walks them with whole waves."""
+    w, c, k, cl, oi, idx = setup("1m", ndocs=3000)
+    q, _ = c.queries(6, w.Tq, query_seed=13)
+    check_search(idx, oi, q, w.nprobe, 500, 50, "bf16", f"1m recipe, 3000 docs, refine={refine}", refine=refine)
