@@ -52,14 +52,13 @@ struct RefList {
 // Key of token t for query token j: S[j][c] + <q_j, w[codes t]>, q_j as 64
 // bf16 pairs (dimensions 2i, 2i+1 in word i).
 template <int NBITS>
-__device__ __forceinline__ int32_t token_key(const uint8_t *__restrict__ codes, int32_t t, const uint32_t (&qv)[64],
-                                             const uint32_t *lut, int32_t skey) {
+__device__ __forceinline__ int32_t key_of_code(const uint4 (&cc)[NBITS], const uint32_t (&qv)[64],
+                                               const uint32_t *lut, int32_t skey) {
   constexpr int CB = 16 * NBITS;
-  const uint4 *cp = (const uint4 *)(codes + (int64_t)t * CB);
   float acc = 0.f;
 #pragma unroll
   for (int u = 0; u < CB / 16; ++u) {
-    const uint4 c4 = cp[u];
+    const uint4 c4 = cc[u];
     const uint32_t cw[4] = {c4.x, c4.y, c4.z, c4.w};
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
@@ -79,12 +78,42 @@ __device__ __forceinline__ int32_t token_key(const uint8_t *__restrict__ codes, 
   return skey + to_key(acc);
 }
 
+template <int NBITS>
+__device__ __forceinline__ void load_code(const uint8_t *__restrict__ codes, int32_t t, uint4 (&cc)[NBITS]) {
+  const uint4 *cp = (const uint4 *)(codes + (int64_t)t * (16 * NBITS));
+#pragma unroll
+  for (int u = 0; u < NBITS; ++u) cc[u] = cp[u];
+}
+
+template <int NBITS>
+__device__ __forceinline__ int32_t token_key(const uint8_t *__restrict__ codes, int32_t t, const uint32_t (&qv)[64],
+                                             const uint32_t *lut, int32_t skey) {
+  uint4 cc[NBITS];
+  load_code<NBITS>(codes, t, cc);
+  return key_of_code<NBITS>(cc, qv, lut, skey);
+}
+
 // A list walked by one lane: expected entries per range at most this.
 constexpr int REF_LANE_ENTRIES = 32;
+// Entries of a lane's list handled together.
+constexpr int REF_BATCH = 2;
 
-// Documents per range: the state m is TQP x RR int32, 64 KiB.
+// Documents per range: the state m is TQP x RR int32, 32 KiB.
 template <int TQP>
-constexpr int ref_range_docs() { return 16384 / TQP; }
+constexpr int ref_range_docs() { return 8192 / TQP; }
+
+// (document, query token) entries a range records for its sweep; beyond this
+// the range sweeps its whole state instead.
+constexpr int REF_TOUCH_CAP = 2048;
+
+// m[idx] = max(m[idx], key); the first update of an entry (which holds NO_HIT
+// between ranges) records idx.
+__device__ __forceinline__ void ref_update(int32_t *m, int32_t *tl, int32_t *ntl, int idx, int32_t key) {
+  if (atomicMax(&m[idx], key) == NO_HIT) {
+    const int slot = atomicAdd(ntl, 1);
+    if (slot < REF_TOUCH_CAP) tl[slot] = idx;
+  }
+}
 
 template <int NBITS, int TQP>
 __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
@@ -94,14 +123,18 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     uint4 w_lo, uint4 w_hi, int64_t ndocs, int nranges, int G, int M, int32_t *__restrict__ fp,
     uint32_t *__restrict__ hist) {
   constexpr int RR = ref_range_docs<TQP>();
-  static_assert(RR * TQP >= SEL_BINS, "the histogram reuses the state array");
+  static_assert((RR & (RR - 1)) == 0 && RR % 32 == 0, "ranges of a power of two documents");
   extern __shared__ __align__(16) unsigned char ref_lds[];
-  int32_t *m = (int32_t *)ref_lds;                         // [TQP][RR]: query token major
-  int32_t *sfp = m + RR * TQP;                             // [RR]
-  uint32_t *lut = (uint32_t *)(sfp + RR);                  // [256][NBITS == 2 ? 2 : 1]
-  RefList *L = (RefList *)(lut + 256 * (NBITS == 2 ? 2 : 1));  // [nprobe * Tq], list i = r * Tq + j
-  int32_t *wide = (int32_t *)(L + nprobe * Tq);                 // [nprobe * Tq] lists walked by a wave
-  int32_t &s_nwide = wide[nprobe * Tq];                         // their number
+  int32_t *m = (int32_t *)ref_lds;                         // [TQP][RR] query token major, NO_HIT between ranges
+  uint32_t *hsh = (uint32_t *)(m + RR * TQP);              // [SEL_BINS] the group's histogram
+  int32_t *tl = (int32_t *)(hsh + SEL_BINS);               // [REF_TOUCH_CAP] entries updated in the range
+  int32_t *sfp = tl + REF_TOUCH_CAP;                       // [RR] F' being summed
+  uint32_t *hitw = (uint32_t *)(sfp + RR);                 // [RR / 32] documents hit in the range
+  uint32_t *lut = hitw + RR / 32;                          // [256][NBITS == 2 ? 2 : 1]
+  RefList *L = (RefList *)(lut + 512);                     // [nprobe * Tq], list i = r * Tq + j
+  int32_t *wide = (int32_t *)(L + nprobe * Tq);            // [nprobe * Tq] lists walked by a wave
+  int32_t &s_nwide = wide[nprobe * Tq];                    // their number
+  int32_t &s_ntl = wide[nprobe * Tq + 1];                  // entries recorded in tl
   // (all of it in the dynamic allocation: the launch asks for the whole LDS)
 
   const int b = blockIdx.x;
@@ -131,7 +164,14 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
   }
   // list cursors, positioned at the group's first token
   const int nl = nprobe * Tq;
-  if (threadIdx.x == 0) s_nwide = 0;
+  if (threadIdx.x == 0) {
+    s_nwide = 0;
+    s_ntl = 0;
+  }
+  for (int i = threadIdx.x; i < RR * TQP; i += REF_THREADS) m[i] = NO_HIT;
+  for (int i = threadIdx.x; i < SEL_BINS; i += REF_THREADS) hsh[i] = 0;
+  for (int i = threadIdx.x; i < RR; i += REF_THREADS) sfp[i] = 0;
+  for (int i = threadIdx.x; i < RR / 32; i += REF_THREADS) hitw[i] = 0;
   __syncthreads();
   const int64_t tstart = doc_off[(int64_t)rg0 * RR];
   for (int i = threadIdx.x; i < nl; i += REF_THREADS) {
@@ -160,8 +200,7 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     const int64_t d1 = min(ndocs, d0 + RR);
     const int nd = (int)(d1 - d0);
     const int64_t t1 = doc_off[d1];  // tokens of the range: [doc_off[d0], t1)
-    for (int i = threadIdx.x; i < RR * TQP; i += REF_THREADS) m[i] = NO_HIT;
-    __syncthreads();  // cursors, table and state ready; the previous range's reads done
+    __syncthreads();  // cursors, table and state ready; the previous range's resets done
 
     // lists walked by one lane each
     for (int i = threadIdx.x; i < nl; i += REF_THREADS) {
@@ -181,13 +220,39 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
       const int32_t len = w->len, skey = w->skey;
       const int32_t *list = ivf_tok + w->beg;
       int32_t pos = w->pos;
-      do {
-        const int32_t tn = pos + 1 < len ? list[pos + 1] : INT32_MAX;  // next entry, loaded early
-        const int32_t key = token_key<NBITS>(codes, t, qv, lut, skey);
-        atomicMax(&m[j * RR + (tok_doc[t] - (int)d0)], key);
-        ++pos;
-        t = tn;
-      } while (t < t1);
+      // REF_BATCH entries at a time: their ids, then their codes and
+      // documents, are loaded together (the entries ascend, so those inside
+      // the range are a prefix; the others load entry pos's data and are
+      // dropped)
+      for (;;) {
+        int32_t tt[REF_BATCH + 1];
+        tt[0] = t;
+#pragma unroll
+        for (int u = 1; u <= REF_BATCH; ++u) tt[u] = pos + u < len ? list[pos + u] : INT32_MAX;
+        uint4 cc[REF_BATCH][NBITS];
+        int32_t key[REF_BATCH], doc[REF_BATCH];
+#pragma unroll
+        for (int u = 0; u < REF_BATCH; ++u) {
+          const int32_t tu = tt[u] < t1 ? tt[u] : t;
+          load_code<NBITS>(codes, tu, cc[u]);
+          doc[u] = tok_doc[tu];
+        }
+#pragma unroll
+        for (int u = 0; u < REF_BATCH; ++u) {
+          __builtin_amdgcn_sched_barrier(0);  // one entry's products at a time
+          key[u] = key_of_code<NBITS>(cc[u], qv, lut, skey);
+        }
+        int n = 0;
+#pragma unroll
+        for (int u = 0; u < REF_BATCH; ++u)
+          if (tt[u] < t1) {
+            ref_update(m, tl, &s_ntl, j * RR + (doc[u] - (int)d0), key[u]);
+            n = u + 1;
+          }
+        pos += n;
+        t = tt[n];
+        if (n < REF_BATCH || t >= t1) break;
+      }
       w->pos = pos;
       w->next = t;
     }
@@ -214,7 +279,7 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
         const int32_t p = pos + lane;
         const int32_t t = p < len ? list[p] : INT32_MAX;
         const bool in = t < t1;
-        if (in) atomicMax(&m[j * RR + (tok_doc[t] - (int)d0)], token_key<NBITS>(codes, t, qv, lut, skey));
+        if (in) ref_update(m, tl, &s_ntl, j * RR + (tok_doc[t] - (int)d0), token_key<NBITS>(codes, t, qv, lut, skey));
         const unsigned long long out = __ballot(!in);
         if (out) {
           const int first = __ffsll((long long)out) - 1;
@@ -230,39 +295,44 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
       }
     }
     __syncthreads();
-    for (int v = threadIdx.x; v < nd; v += REF_THREADS) {
-      int32_t s = 0;
-      bool hit = false;
-      for (int j = 0; j < Tq; ++j) {
-        const int32_t x = m[j * RR + v];
-        if (x != NO_HIT) {
-          s += x;
-          hit = true;
-        }
-      }
-      sfp[v] = hit ? s : NO_HIT;
+    // sum the updated entries into F' and put them back to NO_HIT
+    const int ntl = s_ntl;  // uniform
+    auto take = [&](int idx) {
+      const int32_t x = m[idx];
+      m[idx] = NO_HIT;
+      const int v = idx & (RR - 1);
+      atomicAdd(&sfp[v], x);
+      atomicOr(&hitw[v >> 5], 1u << (v & 31));
+    };
+    if (ntl <= REF_TOUCH_CAP) {
+      for (int e = threadIdx.x; e < ntl; e += REF_THREADS) take(tl[e]);
+    } else {
+      for (int idx = threadIdx.x; idx < Tq * RR; idx += REF_THREADS)
+        if (m[idx] != NO_HIT) take(idx);
     }
-    __syncthreads();
-    uint32_t *sh = (uint32_t *)m;  // the state is no longer needed
-    for (int i = threadIdx.x; i < SEL_BINS; i += REF_THREADS) sh[i] = 0;
     __syncthreads();
     int32_t *f = fp + q * ndocs + d0;
     for (int v = threadIdx.x; v < nd; v += REF_THREADS) {
-      const int32_t x = sfp[v];
+      const bool hit = (hitw[v >> 5] >> (v & 31)) & 1u;
+      const int32_t x = hit ? sfp[v] : NO_HIT;
       f[v] = x;
-      if (x != NO_HIT) atomicAdd(&sh[fp_key(x) >> 20], 1u);
+      sfp[v] = 0;
+      if (hit) atomicAdd(&hsh[fp_key(x) >> 20], 1u);
     }
     __syncthreads();
-    uint32_t *hq = hist + q * SEL_BINS;
-    for (int i = threadIdx.x; i < SEL_BINS; i += REF_THREADS)
-      if (sh[i]) atomicAdd(&hq[i], sh[i]);
-    __syncthreads();  // sh (the state array) is reset by the next range
+    for (int i = threadIdx.x; i < RR / 32; i += REF_THREADS) hitw[i] = 0;
+    if (threadIdx.x == 0) s_ntl = 0;
   }
+  __syncthreads();
+  uint32_t *hq = hist + q * SEL_BINS;
+  for (int i = threadIdx.x; i < SEL_BINS; i += REF_THREADS)
+    if (hsh[i]) atomicAdd(&hq[i], hsh[i]);
 }
 
 size_t refine_lds_bytes(int TQP, int nprobe, int Tq) {
-  const size_t RR = 16384 / TQP;
-  return RR * TQP * 4 + RR * 4 + 256 * 8 + (size_t)nprobe * Tq * (sizeof(RefList) + 4) + 4;
+  const size_t RR = 8192 / TQP;
+  return RR * TQP * 4 + SEL_BINS * 4 + REF_TOUCH_CAP * 4 + RR * 4 + RR / 8 + 512 * 4 +
+         (size_t)nprobe * Tq * (sizeof(RefList) + 4) + 8;
 }
 
 template <int NBITS, int TQP>
