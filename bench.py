@@ -83,17 +83,24 @@ def exact_topk_gpu(q_k, corpus, k, device):
     nd = corpus.spec.ndocs
     Q = torch.from_numpy(q_k.astype(np.float64) / 2048.0).to(device)  # [nq, Tq, d]
     nq, Tq, _ = Q.shape
-    best = torch.full((nq, Tq, nd), -float("inf"), dtype=torch.float64, device=device)
-    step = max(100, int(2e8 // (nq * Tq * 70)))  # ~1.6 GB of fp64 scores per chunk
+    F = torch.empty((nq, nd), dtype=torch.float64, device=device)
+    # chunks of whole documents, ~8 GB of fp64 scores each; a chunk's
+    # documents are finished inside it
+    step = max(100, int(1e9 // (nq * Tq * 70)))
+    t_log = time.perf_counter()
     for d0 in range(0, nd, step):
         d1 = min(nd, d0 + step)
         tk, _ = corpus.tokens(d0, d1)
         T = torch.from_numpy(tk.astype(np.float64) / 2048.0).to(device)  # [rows, d]
         lens = torch.from_numpy(corpus.lengths[d0:d1].astype(np.int64)).to(device)
-        doc = torch.repeat_interleave(torch.arange(d0, d1, device=device), lens)
+        doc = torch.repeat_interleave(torch.arange(d1 - d0, device=device), lens)
         S = torch.matmul(Q.reshape(nq * Tq, -1), T.T).reshape(nq, Tq, -1)
+        best = torch.full((nq, Tq, d1 - d0), -float("inf"), dtype=torch.float64, device=device)
         best.scatter_reduce_(2, doc.view(1, 1, -1).expand(nq, Tq, -1), S, reduce="amax", include_self=True)
-    F = best.sum(dim=1)  # [nq, nd], exact
+        F[:, d0:d1] = best.sum(dim=1)  # exact
+        if time.perf_counter() - t_log > 20:
+            log(f"exact MaxSim reference: {d1}/{nd} docs")
+            t_log = time.perf_counter()
     order = torch.sort(F, dim=1, descending=True, stable=True).indices[:, :k]
     return order.cpu().numpy()
 
@@ -197,6 +204,7 @@ def main():
         return
 
     # ---- algorithmic work of one step, from the stage taps and host copies
+    log("counting the step's algorithmic work")
     ci, _ = idx.probe(Q, w.nprobe)
     cand, _, nval = idx.prune(Q, w.nprobe, w.ncand, refine=rmode)
     torch.cuda.synchronize()
@@ -245,6 +253,7 @@ def main():
     probe_tflops = work["probe"][1] / (stage_ms["probe"] / 1e3) / 1e12
 
     # ---- latency at nq=1 (H2D of the query, search, D2H of the results)
+    log("latency at nq=1")
     nlat = args.latency_iters
     lq, _ = corpus.queries(nlat, w.Tq, query_seed=99)
     host_q = torch.from_numpy(synth.k_to_bf16_bits(lq).view(np.int16)).view(torch.bfloat16).pin_memory()
@@ -270,7 +279,27 @@ def main():
     lat_stage = idx.stage_times()
     lat_stage_ms = {s: float(lat_stage[i]) / nlat for i, s in enumerate(STAGES)}
 
+    # ---- QPS at smaller batches (the same index and queries, resident in HBM)
+    log("QPS at smaller batches")
+    qps_by_batch = {}
+    for nb in sorted({1, 8, 32, 128, w.nq}):
+        if nb > w.nq:
+            continue
+        reps = max(3, min(50, int(2048 // nb)))
+        bi = torch.empty((nb, w.k), dtype=torch.int32, device=dev)
+        bs = torch.empty((nb, w.k), dtype=torch.float32, device=dev)
+        idx.search(Q[:nb], w.nprobe, w.ncand, w.k, out=(bi, bs), refine=rmode)
+        torch.cuda.synchronize()
+        s = time.perf_counter()
+        for _ in range(reps):
+            idx.search(Q[:nb], w.nprobe, w.ncand, w.k, out=(bi, bs), refine=rmode)
+        torch.cuda.synchronize()
+        qps_by_batch[str(nb)] = nb * reps / (time.perf_counter() - s)
+    idx.stage_times()  # drop these searches' events
+    log(f"QPS by batch: {qps_by_batch}")
+
     # ---- recall@k against exact MaxSim
+    log("recall against exact MaxSim")
     nr = min(args.recall_queries, w.nq)
     truth = exact_topk_gpu(q_k[:nr], corpus, w.k, dev)
     got = ids[:nr].cpu().numpy()
@@ -278,8 +307,15 @@ def main():
     src_first = float(np.mean(got[:, 0] == q_src[:nr]))
 
     # ---- CPU baseline: the oracle, untouched, on a bounded sample
+    log("CPU baseline")
     cpu = None
-    if not args.no_cpu_baseline:
+    # the oracle keeps every raw token (256 B) and its unpacked codes (128 B)
+    oracle_bytes = info["ntokens"] * (2 * 128 + 128)
+    if not args.no_cpu_baseline and oracle_bytes > 64 * 2**30:
+        log(f"CPU baseline skipped: the oracle's in-memory index would take {oracle_bytes / 2**30:.0f} GiB")
+        cpu = {"value": None, "kind": "oracle",
+               "skipped": f"the oracle's in-memory index needs {oracle_bytes / 2**30:.0f} GiB of host memory"}
+    elif not args.no_cpu_baseline:
         import oracle
         tk, cl = corpus.tokens()
         oi = oracle.OracleIndex(corpus.centroids_k, corpus.doc_off, cl, w.nbits, tok_k=tk)
@@ -306,7 +342,7 @@ def main():
                    "nbits": w.nbits, "nq": w.nq, "Tq": w.Tq, "nprobe": w.nprobe, "ncand": w.ncand, "k": w.k,
                    "refine": args.refine,
                    "index_device_bytes": info["device_bytes"]},
-        "recall_at_k": recall, "recall_queries": nr, "source_doc_top1": src_first,
+        "recall_at_k": recall, "recall_queries": nr, "source_doc_top1": src_first, "qps_by_batch": qps_by_batch,
         "p50_ms_nq1": float(np.percentile(lat, 50)), "p95_ms_nq1": float(np.percentile(lat, 95)),
         "p99_ms_nq1": float(np.percentile(lat, 99)), "nq1_stages_ms": lat_stage_ms,
         "code_scan_GBps": score_gbs, "probe_TFLOPs": probe_tflops, "stages_ms": stage_ms,

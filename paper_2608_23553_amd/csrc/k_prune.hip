@@ -530,14 +530,18 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
 
 // ---------------------------------------------------------------------
 // Refinement select split over P chunks of documents per query, so that a
-// launch with few queries still fills the chip (with 128 queries or more,
+// launch with few queries still fills the chip, and long F' rows are read by
+// many workgroups (with 128 queries or more over fewer than 2^19 documents,
 // k_select runs one workgroup per query instead).  A radix select on the order
 // key u = fp_key(F') finds the ncand-th largest key T and how many documents
 // with key T to keep (the lowest ids): bits 31..20 come from the walk's
 // histogram, bits 19..8 and 7..0 from two histogram passes over the chunks
-// (global atomics, only documents whose higher bits match count).  Then every
-// chunk counts what it keeps, the counts are scanned per query, and each
-// chunk writes its part of the candidate list in ascending doc order.
+// (global atomics, only documents whose higher bits match count).  The last
+// pass also records, per chunk, how many keys lie above the 24-bit prefix and
+// the chunk's own histogram of the low 8 bits, so that once T is known every
+// chunk's kept and tied counts follow without another pass; the counts are
+// scanned per query, and each chunk that keeps documents writes its part of
+// the candidate list in ascending doc order.
 // SelState per query: the bins found so far, the count still to place, T and
 // the ties to keep.
 struct SelState {
@@ -590,11 +594,18 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_hist(const int32_t *__res
   __syncthreads();
   const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
   const int32_t *f = fp + q * ndocs;
-  for (int64_t v = v0 + threadIdx.x; v < v1; v += SPLIT_THREADS) {
-    const int32_t x = f[v];
-    if (x == NO_HIT) continue;
-    const uint32_t u = fp_key(x);
-    if ((u >> (SHIFT + BITS)) == prefix) atomicAdd(&h[(u >> SHIFT) & ((1u << BITS) - 1)], 1u);
+  for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += SPLIT_THREADS * SEL_UNROLL) {
+    int32_t x[SEL_UNROLL];
+#pragma unroll
+    for (int i = 0; i < SEL_UNROLL; ++i) {
+      const int64_t v = vb + (int64_t)i * SPLIT_THREADS;
+      x[i] = v < v1 ? f[v] : NO_HIT;
+    }
+#pragma unroll
+    for (int i = 0; i < SEL_UNROLL; ++i) {
+      const uint32_t u = fp_key(x[i]);
+      if (x[i] != NO_HIT && (u >> (SHIFT + BITS)) == prefix) atomicAdd(&h[(u >> SHIFT) & ((1u << BITS) - 1)], 1u);
+    }
   }
   __syncthreads();
   uint32_t *o = hout + q * (1 << BITS);
@@ -625,51 +636,87 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_next(const uint32_t *__re
   }
 }
 
-// Per chunk: documents kept outright (key > T) and ties (key == T).
-__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_count(const int32_t *__restrict__ fp, int64_t ndocs, int P,
-                                                             const SelState *__restrict__ st,
-                                                             long long *__restrict__ counts) {
-  __shared__ long long wsum[SPLIT_THREADS / 64];
-  __shared__ long long s_tot;
+// Last histogram pass over one chunk (bits 7..0 under the 24-bit prefix), as
+// k_sel_hist, plus the chunk's own record: chunk_hist [256] of those keys and
+// chunk_above, the number of keys above the prefix (every hit when all are
+// kept).
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__restrict__ fp, int64_t ndocs, int P,
+                                                            const SelState *__restrict__ st,
+                                                            uint32_t *__restrict__ hout,
+                                                            uint32_t *__restrict__ chunk_hist,
+                                                            uint32_t *__restrict__ chunk_above) {
+  __shared__ uint32_t h[256];
+  __shared__ uint32_t s_above;
   const int64_t q = blockIdx.x / P;
   const int c = blockIdx.x % P;
-  const uint32_t T = st[q].T;
+  const bool all = st[q].T == 0;  // uniform: every hit is kept
+  const uint32_t prefix = st[q].prefix;
+  for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) h[i] = 0;
+  if (threadIdx.x == 0) s_above = 0;
+  __syncthreads();
   const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
   const int32_t *f = fp + q * ndocs;
-  long long above = 0, ties = 0;
-  for (int64_t v = v0 + threadIdx.x; v < v1; v += SPLIT_THREADS) {
-    const int32_t x = f[v];
-    if (x == NO_HIT) continue;
-    const uint32_t u = fp_key(x);
-    above += u > T;
-    ties += u == T;
+  uint32_t above = 0;
+  for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += SPLIT_THREADS * SEL_UNROLL) {
+    int32_t x[SEL_UNROLL];
+#pragma unroll
+    for (int i = 0; i < SEL_UNROLL; ++i) {
+      const int64_t v = vb + (int64_t)i * SPLIT_THREADS;
+      x[i] = v < v1 ? f[v] : NO_HIT;
+    }
+#pragma unroll
+    for (int i = 0; i < SEL_UNROLL; ++i) {
+      if (x[i] == NO_HIT) continue;
+      const uint32_t u = fp_key(x[i]);
+      if (all || (u >> 8) > prefix) ++above;
+      else if ((u >> 8) == prefix) atomicAdd(&h[u & 255u], 1u);
+    }
   }
-  block_exclusive_scan(above, wsum, &s_tot);
-  const long long a = s_tot;
-  block_exclusive_scan(ties, wsum, &s_tot);
-  if (threadIdx.x == 0) {
-    counts[2 * (q * P + c)] = a;
-    counts[2 * (q * P + c) + 1] = s_tot;
+  atomicAdd(&s_above, above);
+  __syncthreads();
+  uint32_t *o = hout + q * 256, *ch = chunk_hist + ((int64_t)q * P + c) * 256;
+  for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) {
+    ch[i] = h[i];
+    if (h[i]) atomicAdd(&o[i], h[i]);
   }
+  if (threadIdx.x == 0) chunk_above[(int64_t)q * P + c] = s_above;
 }
 
-// Per query: output offset and ties-before of every chunk (in place), the
-// number of candidates, and the padding of the unused slots.
+// Per query: every chunk's kept (key > T) and tied (key == T) counts from its
+// record, then (in order) its output offset, ties before it and the number it
+// keeps [3 per chunk], the number of candidates, and the padding of the
+// unused slots.
 __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_scan(int P, int ncand, SelState *__restrict__ st,
+                                                            const uint32_t *__restrict__ chunk_hist,
+                                                            const uint32_t *__restrict__ chunk_above,
                                                             long long *__restrict__ counts, int32_t *__restrict__ out_ids,
                                                             int32_t *__restrict__ out_keys,
                                                             int32_t *__restrict__ n_valid) {
   __shared__ long long total;
   const int64_t q = blockIdx.x;
+  const uint32_t T = st[q].T;
+  const int b3 = (int)(T & 255u);
+  for (int c = threadIdx.x; c < P; c += SPLIT_THREADS) {
+    const uint32_t *ch = chunk_hist + ((int64_t)q * P + c) * 256;
+    long long above = chunk_above[(int64_t)q * P + c], ties = 0;
+    if (T != 0) {
+      for (int b = b3 + 1; b < 256; ++b) above += ch[b];
+      ties = ch[b3];
+    }
+    counts[3 * (q * P + c)] = above;
+    counts[3 * (q * P + c) + 1] = ties;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
     const long long need = st[q].need;
     long long off = 0, tb = 0;
     for (int c = 0; c < P; ++c) {
-      long long *cc = counts + 2 * (q * P + c);
+      long long *cc = counts + 3 * (q * P + c);
       const long long a = cc[0], t = cc[1];
       const long long take = a + max(0ll, min(t, need - tb));
       cc[0] = off;
       cc[1] = tb;
+      cc[2] = take;
       off += take;
       tb += t;
     }
@@ -697,7 +744,9 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__re
   const int c = blockIdx.x % P;
   const uint32_t T = st[q].T;
   const long long need = st[q].need;
-  long long written = counts[2 * (q * P + c)], ties_seen = counts[2 * (q * P + c) + 1];
+  const long long *cc = counts + 3 * (q * P + c);
+  if (cc[2] == 0 || cc[0] >= ncand) return;  // uniform: the chunk keeps nothing that fits
+  long long written = cc[0], ties_seen = cc[1];
   const int64_t per = (ndocs + P - 1) / P, vb = c * per, ve = min(ndocs, vb + per);
   const int32_t *f = fp + q * ndocs;
   const int64_t step = (int64_t)SPLIT_THREADS * SEL_ITEMS;
@@ -747,15 +796,16 @@ int select_chunks(int64_t nq, int64_t ndocs) {
 
 size_t select_scratch_bytes(int64_t nq, int64_t ndocs) {
   const int P = select_chunks(nq, ndocs);
-  return (size_t)nq * (sizeof(SelState) + (SEL_BINS + 256) * 4 + (size_t)P * 16) + 256;
+  return (size_t)nq * (sizeof(SelState) + (SEL_BINS + 256) * 4 + (size_t)P * (24 + 256 * 4 + 4)) + 512;
 }
 
 void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, void *scratch,
                    int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s) {
   if (nq <= 0) return;
-  if (nq >= 128) {
-    // enough queries to fill the chip with one workgroup each (three passes
-    // over F' instead of four, and one launch)
+  if (nq >= 128 && ndocs < (1 << 19)) {
+    // enough queries to fill the chip with one workgroup each, over short
+    // enough F' rows (one launch; measured faster than the split passes at
+    // 100k documents, slower at 1M)
     hipLaunchKernelGGL((k_select<0>), dim3((unsigned)nq), dim3(SEL_THREADS), 0, s, fp, hist, ndocs, ncand,
                        (const int64_t *)nullptr, cand_ids, cand_keys, n_valid);
     return;
@@ -765,14 +815,16 @@ void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t 
   uint32_t *hist2 = (uint32_t *)(st + nq);
   uint32_t *hist3 = hist2 + nq * SEL_BINS;
   long long *counts = (long long *)(((uintptr_t)(hist3 + nq * 256) + 15) & ~(uintptr_t)15);
+  uint32_t *chunk_hist = (uint32_t *)(counts + 3 * nq * P);
+  uint32_t *chunk_above = chunk_hist + (size_t)nq * P * 256;
   const dim3 gq((unsigned)nq), gc((unsigned)(nq * P)), tb(SPLIT_THREADS);
   hipLaunchKernelGGL(k_sel_first, gq, tb, 0, s, hist, ncand, hist2, hist3, st);
   hipLaunchKernelGGL((k_sel_hist<8, 12>), gc, tb, 0, s, fp, ndocs, P, st, hist2);
   hipLaunchKernelGGL((k_sel_next<12, false>), gq, tb, 0, s, hist2, st);
-  hipLaunchKernelGGL((k_sel_hist<0, 8>), gc, tb, 0, s, fp, ndocs, P, st, hist3);
+  hipLaunchKernelGGL(k_sel_last, gc, tb, 0, s, fp, ndocs, P, st, hist3, chunk_hist, chunk_above);
   hipLaunchKernelGGL((k_sel_next<8, true>), gq, tb, 0, s, hist3, st);
-  hipLaunchKernelGGL(k_sel_count, gc, tb, 0, s, fp, ndocs, P, st, counts);
-  hipLaunchKernelGGL(k_sel_scan, gq, tb, 0, s, P, ncand, st, counts, cand_ids, cand_keys, n_valid);
+  hipLaunchKernelGGL(k_sel_scan, gq, tb, 0, s, P, ncand, st, chunk_hist, chunk_above, counts, cand_ids, cand_keys,
+                     n_valid);
   hipLaunchKernelGGL(k_sel_write, gc, tb, 0, s, fp, ndocs, P, ncand, st, counts, cand_ids, cand_keys);
 }
 
