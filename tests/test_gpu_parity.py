@@ -334,3 +334,37 @@ def test_zipf_small_hot_lists(refine):
     w, c, k, cl, oi, idx = setup("1m", ndocs=3000)
     q, _ = c.queries(6, w.Tq, query_seed=13)
     check_search(idx, oi, q, w.nprobe, 500, 50, "bf16", f"1m recipe, 3000 docs, refine={refine}", refine=refine)
+
+
+# ------------------------------------------------------ degenerate queries
+@pytest.mark.parametrize("refine", [False, True])
+def test_tiny_zero_queries_break_every_tie_by_lowest_id(refine):
+    """All-zero queries: every centroid and document score is 0, so the
+    probe, the refinement select and the top-k are decided by the lowest-id
+    rules alone."""
+    w, c, k, cl, oi, idx = setup("tiny")
+    q = np.zeros((3, 32, 128), np.int16)
+    gi, gs, ref = check_search(idx, oi, q, 4, 300, 20, "bf16", f"tiny zero queries refine={refine}", refine=refine)
+    assert np.all(gs == 0.0)
+    assert np.all(np.diff(gi, axis=1) > 0)  # ascending ids among equal scores
+
+
+@pytest.mark.parametrize("refine", [False, True])
+def test_tiny_repeated_query_token(refine):
+    """All 32 tokens of a query equal: at every rank they probe one centroid,
+    so the walk shares one list among the whole query."""
+    w, c, k, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(4, 32, query_seed=17)
+    q = np.repeat(q[:, :1, :], 32, axis=1)
+    check_search(idx, oi, q, 3, 200, 10, "bf16", f"tiny repeated token refine={refine}", refine=refine)
+
+
+@pytest.mark.parametrize("refine", [False, True])
+def test_tiny_negated_queries(refine):
+    """Negated queries (q -> -q): the probe turns to the centroids facing away
+    from every source document, so the candidates and answers share nothing
+    with the queries' own documents."""
+    w, c, k, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(4, 32, query_seed=18)
+    check_search(idx, oi, (-q.astype(np.int32)).astype(np.int16), 2, 256, 10, "bf16",
+                 f"tiny negated refine={refine}", refine=refine)
