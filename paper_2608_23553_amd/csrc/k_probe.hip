@@ -9,6 +9,8 @@
 // the MFMA result is exact whatever its internal summation order, and the
 // selected ids are bit-exact.  S is never materialised for selection: each
 // lane keeps a running sorted list of its best (score, id) keys.
+#include <algorithm>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -237,8 +239,9 @@ ProbePlan plan_probe(int64_t rows, int ncent, int nprobe) {
   p.pmax = nprobe <= 4 ? 4 : nprobe <= 8 ? 8 : nprobe <= 16 ? 16 : nprobe <= 32 ? 32 : 64;
   const int ntiles = (ncent + 31) / 32;
   const int64_t ncb = rows / 32;
-  // aim at ~2048 workgroups, at least 4 tiles (one per wave) per split
-  int64_t want = (2048 + ncb - 1) / ncb;
+  // aim at ~2048 workgroups, at least 4 tiles (one per wave) per split, and
+  // at most 512 splits (the merge folds every split's list)
+  int64_t want = std::min<int64_t>(512, (2048 + ncb - 1) / ncb);
   int64_t maxsplit = (ntiles + 3) / 4;
   int64_t ns = want < 1 ? 1 : want;
   if (ns > maxsplit) ns = maxsplit;

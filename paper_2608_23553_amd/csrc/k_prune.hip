@@ -48,7 +48,8 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
 // workgroup then writes F' (or NO_HIT for documents outside S_Q) and adds the
 // range's histogram of the top 12 bits of the order key to the query's
 // histogram, the first pass of the refinement select.  Workgroup b runs on
-// XCD b % 8; all groups of query q run on XCD q % 8.
+// XCD b % 8; with 8 or more queries all groups of query q run on XCD q % 8,
+// with fewer they spread over every XCD.
 constexpr int WALK_THREADS = 512;
 
 
@@ -127,9 +128,11 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   int32_t *dcount = (int32_t *)(dset + nprobe);              // [nprobe] dense groups per rank
   int8_t *dtab = (int8_t *)(dcount + nprobe);                // [kMaxDense] slot -> first token, current rank
   int8_t *dlist = dtab + kMaxDense;                          // [nprobe][Tq] first tokens of the dense groups
+  // workgroup b runs on XCD b % 8: with 8 or more queries, the groups of
+  // query q run on XCD q % 8; fewer queries spread over every XCD
   const int b = blockIdx.x;
-  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / G);
-  const int g = (b >> 3) % G;
+  const int64_t q = nq >= 8 ? (b & 7) + 8 * (int64_t)((b >> 3) / G) : b / G;
+  const int g = nq >= 8 ? (b >> 3) % G : b % G;
   if (q >= nq) return;
   const int rg0 = g * M, rg1 = min(nranges, rg0 + M);
   if (rg0 >= rg1) return;  // uniform, before any barrier
@@ -304,7 +307,7 @@ static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int
   int G = (int)std::min<int64_t>(nranges, std::max<int64_t>(1, (4096 + nq - 1) / nq));
   const int M = (nranges + G - 1) / G;
   G = (nranges + M - 1) / M;
-  const int64_t blocks = (nq + 7) / 8 * 8 * G;
+  const int64_t blocks = (nq >= 8 ? (nq + 7) / 8 * 8 : nq) * G;
   if (blocks == 0 || nranges == 0) return;
   const size_t lds = walk_lds_bytes(TQP, nprobe, Tq);
   static bool attr = [] {
@@ -692,11 +695,18 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_scan(int P, int ncand, Se
                                                             long long *__restrict__ counts, int32_t *__restrict__ out_ids,
                                                             int32_t *__restrict__ out_keys,
                                                             int32_t *__restrict__ n_valid) {
-  __shared__ long long total;
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot;
   const int64_t q = blockIdx.x;
   const uint32_t T = st[q].T;
+  const long long need = st[q].need;
   const int b3 = (int)(T & 255u);
-  for (int c = threadIdx.x; c < P; c += SPLIT_THREADS) {
+  // thread t owns chunks [c0, c1): two block scans (ties before each chunk,
+  // then output offsets) instead of one thread walking every chunk
+  const int per = (P + SPLIT_THREADS - 1) / SPLIT_THREADS;
+  const int c0 = min(P, (int)threadIdx.x * per), c1 = min(P, c0 + per);
+  long long my_ties = 0;
+  for (int c = c0; c < c1; ++c) {
     const uint32_t *ch = chunk_hist + ((int64_t)q * P + c) * 256;
     long long above = chunk_above[(int64_t)q * P + c], ties = 0;
     if (T != 0) {
@@ -705,28 +715,31 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_scan(int P, int ncand, Se
     }
     counts[3 * (q * P + c)] = above;
     counts[3 * (q * P + c) + 1] = ties;
+    my_ties += ties;
   }
-  __syncthreads();
+  long long tb = block_exclusive_scan(my_ties, wsum, &s_tot);
+  long long my_take = 0;
+  for (int c = c0; c < c1; ++c) {
+    long long *cc = counts + 3 * (q * P + c);
+    const long long a = cc[0], t = cc[1];
+    const long long take = a + max(0ll, min(t, need - tb));
+    cc[1] = tb;
+    cc[2] = take;
+    tb += t;
+    my_take += take;
+  }
+  long long off = block_exclusive_scan(my_take, wsum, &s_tot);
+  const long long n = min(s_tot, (long long)ncand);
+  for (int c = c0; c < c1; ++c) {
+    long long *cc = counts + 3 * (q * P + c);
+    cc[0] = off;
+    off += cc[2];
+  }
   if (threadIdx.x == 0) {
-    const long long need = st[q].need;
-    long long off = 0, tb = 0;
-    for (int c = 0; c < P; ++c) {
-      long long *cc = counts + 3 * (q * P + c);
-      const long long a = cc[0], t = cc[1];
-      const long long take = a + max(0ll, min(t, need - tb));
-      cc[0] = off;
-      cc[1] = tb;
-      cc[2] = take;
-      off += take;
-      tb += t;
-    }
-    const long long n = min(off, (long long)ncand);
     st[q].total = n;
     n_valid[q] = (int32_t)n;
-    total = n;
   }
-  __syncthreads();
-  for (long long i = total + threadIdx.x; i < ncand; i += SPLIT_THREADS) {
+  for (long long i = n + threadIdx.x; i < ncand; i += SPLIT_THREADS) {
     out_ids[q * ncand + i] = -1;
     out_keys[q * ncand + i] = 0;
   }

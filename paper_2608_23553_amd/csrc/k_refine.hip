@@ -137,9 +137,11 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
   int32_t &s_ntl = wide[nprobe * Tq + 1];                  // entries recorded in tl
   // (all of it in the dynamic allocation: the launch asks for the whole LDS)
 
+  // workgroup b runs on XCD b % 8: with 8 or more queries, the groups of
+  // query q run on XCD q % 8; fewer queries spread over every XCD
   const int b = blockIdx.x;
-  const int64_t q = (b & 7) + 8 * (int64_t)((b >> 3) / G);
-  const int g = (b >> 3) % G;
+  const int64_t q = nq >= 8 ? (b & 7) + 8 * (int64_t)((b >> 3) / G) : b / G;
+  const int g = nq >= 8 ? (b >> 3) % G : b % G;
   if (q >= nq) return;
   const int rg0 = g * M, rg1 = min(nranges, rg0 + M);
   if (rg0 >= rg1) return;  // uniform, before any barrier
@@ -346,7 +348,7 @@ static void launch_refine_t(const int32_t *cent_ids, const int32_t *cent_keys, c
   int G = (int)std::min<int64_t>(nranges, std::max<int64_t>(1, (4096 + nq - 1) / nq));
   const int M = (nranges + G - 1) / G;
   G = (nranges + M - 1) / M;
-  const int64_t blocks = (nq + 7) / 8 * 8 * G;
+  const int64_t blocks = (nq >= 8 ? (nq + 7) / 8 * 8 : nq) * G;
   if (blocks == 0 || nranges == 0) return;
   const size_t lds = refine_lds_bytes(TQP, nprobe, Tq);
   static bool attr = [] {
