@@ -227,6 +227,9 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
   int64_t B = std::max<int64_t>(1, (int64_t)(scratch_budget() / perq));
   B = std::min<int64_t>(B, nq);
   B = std::min<int64_t>(B, 65535);
+  // equal sub-batches: the same number of passes, without a short last one
+  const int64_t npass = (nq + B - 1) / B;
+  B = (nq + npass - 1) / npass;
   size_t need = carve_bytes(idx, B, TQP, nprobe, ncand, stop);
   if (nq % B) need = std::max(need, carve_bytes(idx, nq % B, TQP, nprobe, ncand, stop));
   int rc = ensure_scratch(idx, need);
