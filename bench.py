@@ -12,6 +12,9 @@ queries already resident in HBM.  Prints ONE JSON line:
   cpu_baseline     the CPU oracle on a bounded sample of the same queries
   recall_at_k      against exact MaxSim (Chamfer, Def. 1) on raw tokens,
                    brute force in fp64 on the GPU for a sample of queries
+  collab           the CPU-GPU collaborative scoring (Alg. 3) on the same
+                   batch: QPS with chunks and with one chunk, the number of
+                   full-precision scores per query, recall@k
 
 The default workload is the 100k-document corpus (256 queries x 32 tokens,
 nprobe 4, ncand 4096, k 10); ``--workload`` selects another.
@@ -137,6 +140,10 @@ def main():
     ap.add_argument("--recall-queries", type=int, default=64)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample duration")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kfb", type=int, default=0, help="full-precision budget of the collaborative scoring "
+                                                         "(default 4 k)")
+    ap.add_argument("--chunks", type=int, default=4, help="chunks of the collaborative scoring")
+    ap.add_argument("--no-collab", action="store_true", help="skip the collaborative-scoring measurement")
     ap.add_argument("--profile", action="store_true", help="warmup + timed steps only (for rocprofv3)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates rocprofv3 byte counters)")
@@ -306,6 +313,36 @@ def main():
     recall = float(np.mean([len(set(got[i]) & set(truth[i])) / w.k for i in range(nr)]))
     src_first = float(np.mean(got[:, 0] == q_src[:nr]))
 
+    # ---- CPU-GPU collaborative scoring (Alg. 3): the GPU path's candidates
+    # re-ranked on the host from the full-precision tokens, chunk by chunk
+    collab = None
+    fb_bytes = info["ntokens"] * 2 * 128
+    if not args.no_collab and fb_bytes <= 32 * 2**30:
+        kfb = args.kfb or 4 * w.k
+        log(f"collaborative scoring: kfb {kfb}, {args.chunks} chunks, {threads} host threads")
+        tk, _ = corpus.tokens()
+        fb = synth.k_to_bf16_bits(tk)
+        del tk
+        idx.attach_fullbit(fb)
+        runs = {}
+        for c in (args.chunks, 1):
+            idx.search_collab(Q, w.nprobe, w.ncand, kfb, c, w.k, nthreads=threads)  # warm-up
+            reps, s = 3, time.perf_counter()
+            for _ in range(reps):
+                cids, _, nfull = idx.search_collab(Q, w.nprobe, w.ncand, kfb, c, w.k, nthreads=threads)
+            runs[c] = (w.nq * reps / (time.perf_counter() - s), cids, nfull)
+            log(f"  chunks {c}: {runs[c][0]:.0f} QPS, full-precision scores per query "
+                f"mean {nfull.mean():.2f} max {nfull.max()}")
+        idx.attach_fullbit(None)
+        del fb
+        qc, cids, nfull = runs[args.chunks]
+        collab = {"qps": qc, "qps_one_chunk": runs[1][0], "kfb": kfb, "chunks": args.chunks, "host_threads": threads,
+                  "k_hat_full_bit_mean": float(nfull.mean()), "k_hat_full_bit_max": int(nfull.max()),
+                  "recall_at_k": float(np.mean([len(set(cids[i]) & set(truth[i])) / w.k for i in range(nr)])),
+                  "recall_queries": nr}
+    elif not args.no_collab:
+        collab = {"skipped": f"the full-precision host store would take {fb_bytes / 2**30:.0f} GiB"}
+
     # ---- CPU baseline: the oracle, untouched, on a bounded sample
     log("CPU baseline")
     cpu = None
@@ -348,7 +385,7 @@ def main():
         "code_scan_GBps": score_gbs, "probe_TFLOPs": probe_tflops, "stages_ms": stage_ms,
         "work_per_step": {"posting_entries": entries, "posting_entries_walked": walked, "scored_tokens": scored_tokens,
                           "candidates": int(nval.sum())},
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "cpu_baseline": cpu, "collab": collab,
     }
     print(json.dumps(out), flush=True)
 

@@ -200,6 +200,52 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
                           int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
                           void *hip_stream);
 
+/* ===================================================================== *
+ * CPU-GPU collaborative scoring (Sec. 4, document scoring; Alg. 3).
+ *
+ * The index keeps compressed codes in HBM; the full-precision token
+ * vectors stay in host memory and only the host scores them, so no
+ * document data crosses PCIe at query time.
+ *
+ * chimera_fullbit_attach: tokens is a HOST array [ntok][dim] of bf16 bit
+ * patterns, in the index's token order (document-major, the order the
+ * builder was given).  The library keeps the pointer, not a copy: the
+ * caller keeps the memory alive and unchanged until chimera_index_free or
+ * another attach (tokens == NULL detaches).  Each value is read as the
+ * builder reads it (snapped onto the value grid), so with the builder's own
+ * input the full-precision scores are the exact Chamfer scores of the
+ * indexed tokens.  E_INVAL if ntok differs from the index's token count.
+ *
+ * chimera_search_collab: steps 1-3 of chimera_search, then Alg. 3 over each
+ * query's kept candidates S_refine, taken in ascending document id:
+ *  - chunk i (0 <= i < chunks) is candidates floor(i*ncand/chunks) ..
+ *    floor((i+1)*ncand/chunks) - 1 (those below n_valid); the GPU computes
+ *    F^ (step 4) chunk by chunk and copies each chunk's scores to pinned
+ *    host memory as it finishes;
+ *  - after chunk i arrives, host threads rank every candidate seen so far
+ *    by (F^ desc, id asc) and compute the full-precision score
+ *       F(V) = sum_j max_{t in V} <Q_j, v_t>
+ *    of each of the first ceil((i+1) * kfb / chunks) that has none yet,
+ *    while the GPU scores the later chunks;
+ *  - ids/scores = the k best of the documents with a full-precision score,
+ *    by (F desc, id asc), padded with (-1, -INFINITY).
+ *   kfb      k <= kfb: the full-precision budget (k_full-bit)
+ *   chunks   1 .. 64 (c of Alg. 3; 1 is the non-concurrent strategy)
+ *   ids, scores, n_full   HOST arrays [nq][k], [nq][k], [nq]; n_full[q] is
+ *            the number of full-precision scores computed for query q
+ *            (k-hat_full-bit): at least min(kfb, n_valid), at most the sum
+ *            of the chunk quotas, kfb (chunks + 1) / 2 when chunks divides
+ *            kfb (Sec. 4)
+ *   nthreads host threads for the full-precision scores (0: all cores)
+ * Returns when the results are written (the stream is synchronised).
+ * E_INVAL without an attached store, or for k > kfb, chunks out of range;
+ * other arguments as chimera_search.
+ * ===================================================================== */
+int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens, int64_t ntok);
+int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
+                          float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream);
+
 /* Stage taps: the same inputs as chimera_search, stopping after a stage.
  * They exist so that each stage can be compared with an independent
  * reference; they cost as much as the stages they run. */

@@ -261,6 +261,40 @@ def exact_chamfer(q_k, tok_k, doc_off) -> np.ndarray:
     return F[:ndocs].copy()
 
 
+def collaborative_scoring(refine_ids, approx_keys, exact_key, ncand: int, kfb: int, chunks: int, k: int):
+    """CPU-GPU collaborative document scoring (Sec. 4, document scoring;
+    Alg. 3) for one query, written from the algorithm's steps.
+
+    refine_ids  S_refine, in the order it is cut into chunks (ascending
+                document id: the paper leaves the order open)
+    approx_keys the GPU-side complete scores F^ of those documents (keys)
+    exact_key   doc -> full-precision score key
+    Chunk i (0-based) holds positions floor(i ncand / chunks) ..
+    floor((i+1) ncand / chunks) - 1 of S_refine.  After chunk i every document
+    seen so far that ranks among the first ceil((i+1) kfb / chunks) by
+    (F^ desc, id asc) gets a full-precision score if it has none.  Returns the
+    k best scored documents by (F desc, id asc) as (ids, keys) padded with
+    (-1, INT64_MIN), and the number of full-precision scores computed."""
+    n = len(refine_ids)
+    seen = []
+    full = {}
+    for i in range(chunks):
+        lo, hi = i * ncand // chunks, (i + 1) * ncand // chunks
+        seen.extend(range(lo, min(hi, n)))
+        quota = min(-(-(i + 1) * kfb // chunks), len(seen))
+        ranked = sorted(seen, key=lambda u: (-int(approx_keys[u]), int(refine_ids[u])))
+        for u in ranked[:quota]:
+            d = int(refine_ids[u])
+            if d not in full:
+                full[d] = int(exact_key(d))
+    best = sorted(full.items(), key=lambda kv: (-kv[1], kv[0]))[:k]
+    ids = np.full(k, -1, np.int32)
+    keys = np.full(k, np.iinfo(np.int64).min, np.int64)
+    for r, (d, key) in enumerate(best):
+        ids[r], keys[r] = d, key
+    return ids, keys, len(full)
+
+
 # ------------------------------------------------------- oracle index
 class OracleIndex:
     """The oracle's own view of a corpus: assignment given by the corpus,
@@ -313,6 +347,32 @@ class OracleIndex:
                            nprobe, ncand, k, _p(out["cent_ids"]), _p(out["cent_keys"]), _p(out["n_sq"]),
                            _p(out["cand"]), _p(out["cand_keys"]), _p(out["n_cand"]), _p(out["ids"]),
                            _p(out["keys"]), rf, _p(off), _p(tok), _p(tdoc), nthreads)
+        out["scores"] = keys_to_scores(out["keys"])
+        return out
+
+    def search_collab(self, q_k, tok_k, nprobe: int, ncand: int, kfb: int, chunks: int, k: int):
+        """Steps 1-3 of the search, then Alg. 3 (collaborative_scoring) with
+        F^ from the residual codes (doc_scores) and the full-precision score
+        the exact Chamfer score of the grid tokens tok_k [ntok, dim]."""
+        q_k = _c(q_k, np.int16)
+        tok_k = _c(tok_k, np.int16)
+        nq = q_k.shape[0]
+        nc = min(ncand, self.ndocs)
+        pr = self.prune(q_k, nprobe, nc)
+        out = dict(ids=np.empty((nq, k), np.int32), keys=np.empty((nq, k), np.int64),
+                   n_full=np.empty(nq, np.int64))
+        lens = np.diff(self.doc_off)
+        for qi in range(nq):
+            r = np.sort(pr["cand"][qi, :pr["n_cand"][qi]]).astype(np.int32)
+            S = centroid_scores(q_k[qi], self.cent_k)
+            fh = doc_scores(S, q_k[qi], self.w_k, self.doc_off[r], lens[r].astype(np.int32), self.cid, self.codes)
+
+            def exact(d, q=q_k[qi]):
+                b, e = int(self.doc_off[d]), int(self.doc_off[d + 1])
+                return exact_chamfer(q, tok_k[b:e], np.array([0, e - b], np.int64))[0]
+
+            ids, keys, nf = collaborative_scoring(r, fh, exact, nc, kfb, chunks, k)
+            out["ids"][qi], out["keys"][qi], out["n_full"][qi] = ids, keys, nf
         out["scores"] = keys_to_scores(out["keys"])
         return out
 

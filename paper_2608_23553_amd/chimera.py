@@ -67,6 +67,8 @@ def lib():
         "chimera_prune": ([P, P, INT, I64, I32, I32, I32, I32, P, P, P, P], INT),
         "chimera_prune_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P, P], INT),
         "chimera_stage_times": ([P, P], INT),
+        "chimera_fullbit_attach": ([P, P, I64], INT),
+        "chimera_search_collab": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, I32, P, P, P, I32, P], INT),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -251,6 +253,34 @@ class Index:
                                                k, refine, ctypes.c_void_p(ids.data_ptr()),
                                                ctypes.c_void_p(scores.data_ptr()), _stream_ptr(stream)))
         return ids, scores
+
+    def attach_fullbit(self, tokens_bf16):
+        """Attaches the full-precision store: host uint16 [ntok, d] bf16 bits
+        in the index's token order (chimera_fullbit_attach).  The index keeps
+        a reference to the array; None detaches."""
+        if tokens_bf16 is None:
+            _check(lib().chimera_fullbit_attach(self._h, None, 0))
+            self._fullbit = None
+            return
+        a = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
+        if a.ndim != 2:
+            raise ValueError("tokens must be [ntok, d]")
+        _check(lib().chimera_fullbit_attach(self._h, _np(a), a.shape[0]))
+        self._fullbit = a
+
+    def search_collab(self, Q, nprobe: int, ncand: int, kfb: int, chunks: int, k: int, nthreads: int = 0,
+                      stream=None):
+        """CPU-GPU collaborative scoring (chimera_search_collab): host numpy
+        (ids int32 [nq,k], scores float32 [nq,k], n_full int32 [nq])."""
+        Q, dt = _q_args(Q)
+        nq, Tq, d = Q.shape
+        ids = np.empty((nq, k), dtype=np.int32)
+        scores = np.empty((nq, k), dtype=np.float32)
+        n_full = np.empty(nq, dtype=np.int32)
+        _check(lib().chimera_search_collab(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, kfb,
+                                           chunks, k, _np(ids), _np(scores), _np(n_full), nthreads,
+                                           _stream_ptr(stream)))
+        return ids, scores, n_full
 
     def search_raw(self, q_ptr: int, q_dtype: int, nq: int, Tq: int, d: int, nprobe: int, ncand: int, k: int,
                    ids_ptr: int, scores_ptr: int, stream_ptr: int) -> int:

@@ -58,6 +58,7 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   idx->device = device;
   idx->ncent = h.ncent; idx->dim = h.dim; idx->nbits = h.nbits; idx->max_doc_len = h.max_doc_len;
   idx->ndocs = h.ndocs; idx->ntok = h.ntok; idx->nnz = h.nnz;
+  idx->h_doc_off = h.doc_off;
   std::memcpy(idx->h_weights, h.weights.data(), h.weights.size() * 2);
   std::memcpy(idx->h_cut, h.cut_k.data(), h.cut_k.size() * 4);
   std::vector<int8_t> dense_slot;
@@ -142,13 +143,14 @@ static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype
 static const int kMaxK = 8192;
 
 // ------------------------------------------------------------- pipeline
-enum Stop { STOP_PROBE = 1, STOP_CANDIDATES = 2, STOP_PRUNE = 3, STOP_FULL = 4 };
+enum Stop { STOP_PROBE = 1, STOP_CANDIDATES = 2, STOP_PRUNE = 3, STOP_FULL = 4, STOP_COLLAB = 5 };
 
 struct Outs {
   int32_t *cent_ids = nullptr, *cent_keys = nullptr;            // probe tap [nq][Tq][nprobe]
   int64_t *offsets = nullptr; int32_t *doc_ids = nullptr; int64_t capacity = 0;  // candidates tap
   int32_t *cand_ids = nullptr, *cand_keys = nullptr, *n_valid = nullptr;         // prune tap
   int32_t *ids = nullptr; float *scores = nullptr;                               // search
+  const CollabOut *collab = nullptr;                                             // collaborative scoring
 };
 
 static size_t align_up(size_t x) { return (x + 255) / 256 * 256; }
@@ -310,9 +312,14 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     launch_select(fp, hist, nb, idx->ndocs, ncand, selw, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
+    if (stop == STOP_COLLAB) {
+      rc = collab_subbatch(idx, s, Qs, nb, q0, Tq, TQP, ST, cand, nval, ncand, fhat, *o.collab);
+      if (rc) return rc;
+      continue;
+    }
     stage_mark(idx, s, mark);
     launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
-                          idx->h_weights, cand, nval, ncand, fhat, s);
+                          idx->h_weights, cand, nval, ncand, 0, ncand, fhat, s);
     stage_mark(idx, s, mark);
     launch_topk(fhat, cand, nval, nb, ncand, k, o.ids + q0 * k, o.scores + q0 * k, s);
     stage_mark(idx, s, mark);
@@ -364,6 +371,7 @@ void chimera_index_free(chimera_index *idx) {
                   idx->d_tok_doc, idx->scratch};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
+  collab_free(idx);
   if (idx->scratch_done) (void)hipEventDestroy(idx->scratch_done);
   for (hipEvent_t e : idx->ev) (void)hipEventDestroy(e);
   delete idx;
@@ -403,6 +411,43 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
   o.ids = ids;
   o.scores = scores;
   return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine);
+}
+
+int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
+                          float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream) {
+  int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
+  if (rc) return rc;
+  if (!idx->fullbit) return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
+  if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
+  if (kfb < k) return fail(CHIMERA_E_INVAL, "kfb (%d) must be >= k (%d)", kfb, k);
+  if (ncand < 1) return fail(CHIMERA_E_INVAL, "ncand must be >= 1");
+  if (chunks < 1 || chunks > 64) return fail(CHIMERA_E_INVAL, "chunks must be in [1, 64]");
+  if (nthreads < 0) return fail(CHIMERA_E_INVAL, "nthreads must be >= 0");
+  if (ncand > CHIMERA_MAX_NCAND) return fail(CHIMERA_E_UNSUPPORTED, "ncand %d > %d", ncand, CHIMERA_MAX_NCAND);
+  if (nq > 0 && (!ids || !scores || !n_full)) return fail(CHIMERA_E_INVAL, "null output pointer");
+  if (nq == 0) return CHIMERA_OK;
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  int nc = (int)std::min<int64_t>(ncand, idx->ndocs);
+  if (nc == 0) return fail(CHIMERA_E_INVAL, "index has no documents");
+  CollabOut co;
+  co.kfb = kfb;
+  co.chunks = chunks;
+  co.k = k;
+  co.nthreads = nthreads;
+  co.ids = ids;
+  co.scores = scores;
+  co.n_full = n_full;
+  Outs o;
+  o.collab = &co;
+  hipStream_t s = (hipStream_t)hip_stream;
+  rc = run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_COLLAB, o, s);
+  if (rc) return rc;
+  CHIMERA_HIP(hipStreamSynchronize(s));
+  return CHIMERA_OK;
 }
 
 int chimera_probe(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,

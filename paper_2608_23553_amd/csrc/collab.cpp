@@ -1,0 +1,300 @@
+// collab.cpp - the host half of the CPU-GPU collaborative document scoring
+// (Sec. 4, document scoring; Alg. 3).
+//
+// The GPU scores each query's kept candidates chunk by chunk from their
+// compressed codes (k_residual_score over a candidate range) and copies each
+// chunk's keys into pinned host memory behind an event.  Host threads wait
+// for chunk i, rank every candidate seen so far by its GPU key, and compute
+// full-precision scores for the ones that entered the current top
+// ceil((i+1) kfb / c) and have none yet, while the GPU works on chunk i+1.
+// The final answer is the top-k of the full-precision scores.
+//
+// Full-precision scores are exact: query and document values are grid
+// integers (multiples of 2^-11, as the builder and the query rounding make
+// them), so a product is an integer in units of 2^-22, a 128-term dot
+// product fits int32, and the sum over query tokens is int64.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <atomic>
+#include <condition_variable>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+#include "internal.h"
+
+namespace chimera {
+
+// ------------------------------------------------------------ thread pool
+// Fixed workers; run(n, fn) calls fn(i) for every i in [0, n) on the
+// workers and the calling thread, and returns when all calls are done.
+class Pool {
+ public:
+  explicit Pool(int nthreads) : nworkers_(std::max(0, nthreads - 1)) {
+    for (int w = 0; w < nworkers_; ++w) th_.emplace_back([this] { work(); });
+  }
+  ~Pool() {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto &t : th_) t.join();
+  }
+  int threads() const { return nworkers_ + 1; }
+  void run(int64_t n, const std::function<void(int64_t)> &fn) {
+    if (n <= 0) return;
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      fn_ = &fn;
+      n_ = n;
+      next_.store(0);
+      pending_ = nworkers_;
+      ++gen_;
+    }
+    cv_.notify_all();
+    drain(fn, n);
+    std::unique_lock<std::mutex> lk(mu_);
+    done_.wait(lk, [this] { return pending_ == 0; });
+    fn_ = nullptr;
+  }
+
+ private:
+  void drain(const std::function<void(int64_t)> &fn, int64_t n) {
+    for (int64_t i = next_.fetch_add(1); i < n; i = next_.fetch_add(1)) fn(i);
+  }
+  void work() {
+    uint64_t seen = 0;
+    for (;;) {
+      const std::function<void(int64_t)> *fn;
+      int64_t n;
+      {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
+        if (stop_) return;
+        seen = gen_;
+        fn = fn_;
+        n = n_;
+      }
+      drain(*fn, n);
+      {
+        std::lock_guard<std::mutex> lk(mu_);
+        if (--pending_ == 0) done_.notify_one();
+      }
+    }
+  }
+  const int nworkers_;
+  std::vector<std::thread> th_;
+  std::mutex mu_;
+  std::condition_variable cv_, done_;
+  const std::function<void(int64_t)> *fn_ = nullptr;
+  int64_t n_ = 0;
+  std::atomic<int64_t> next_{0};
+  int pending_ = 0;
+  uint64_t gen_ = 0;
+  bool stop_ = false;
+};
+
+// ------------------------------------------------- per-index host state
+struct Collab {
+  Pool *pool = nullptr;
+  // pinned staging, sized for the largest sub-batch seen
+  int32_t *h_cand = nullptr, *h_fhat = nullptr, *h_nval = nullptr;
+  uint16_t *h_qs = nullptr;
+  size_t cap_cand = 0, cap_fhat = 0, cap_q = 0, cap_qs = 0;
+  hipEvent_t ev_sel = nullptr;
+  std::vector<hipEvent_t> ev;  // one per chunk
+  // per-query working state of one sub-batch
+  std::vector<std::vector<uint64_t>> ranked;              // GPU order keys of the candidates seen so far
+  std::vector<std::vector<uint8_t>> done;                 // candidate has a full-precision score
+  std::vector<std::vector<std::pair<int64_t, int32_t>>> full;  // (F, doc id)
+  std::vector<int16_t> qk;                                // [nb][Tq][dim] query grid integers
+};
+
+static void free_pinned(void *&p) {
+  if (p) (void)hipHostFree(p);
+  p = nullptr;
+}
+
+void collab_free(chimera_index *idx) {
+  Collab *c = idx->collab;
+  if (!c) return;
+  delete c->pool;
+  free_pinned((void *&)c->h_cand);
+  free_pinned((void *&)c->h_fhat);
+  free_pinned((void *&)c->h_nval);
+  free_pinned((void *&)c->h_qs);
+  if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
+  for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
+  delete c;
+  idx->collab = nullptr;
+}
+
+template <class T>
+static int grow_pinned(T *&p, size_t &cap, size_t n) {
+  if (n <= cap) return CHIMERA_OK;
+  free_pinned((void *&)p);
+  cap = 0;
+  void *q = nullptr;
+  if (hipHostMalloc(&q, n * sizeof(T), hipHostMallocDefault) != hipSuccess)
+    return fail(CHIMERA_E_NOMEM, "pinned host buffer of %zu bytes", n * sizeof(T));
+  p = (T *)q;
+  cap = n;
+  return CHIMERA_OK;
+}
+
+// F(V) = sum_j max_t <Q_j, v_t> in units of 2^-22 (Def. 1 on the
+// full-precision tokens); an empty document scores INT64_MIN.  A bf16 value
+// v reads as the grid integer nearbyint(2048 v), which is what the builder
+// makes of it (an integer already when |v| >= 2^-4).  Grid integers are at
+// most 2^11 in magnitude (|value| <= 1), so a product is below 2^22 and a
+// 128-term dot product below 2^29.  One function, so that the conversion
+// and the dot products vectorise together (AVX2 where the host has it).
+__attribute__((target_clones("avx2", "default"))) static int64_t full_score(const int16_t *qk, int Tq, int dim,
+                                                                             const uint16_t *tok, int64_t t0,
+                                                                             int64_t t1, int16_t *buf) {
+  if (t1 <= t0) return INT64_MIN;
+  const int64_t n = (t1 - t0) * dim;
+  const uint16_t *src = tok + t0 * dim;
+  for (int64_t i = 0; i < n; ++i) {
+    const uint32_t u = (uint32_t)src[i] << 16;
+    float v;
+    std::memcpy(&v, &u, 4);
+    const float k = std::nearbyint(v * 2048.0f);
+    buf[i] = (int16_t)(int32_t)std::fmin(std::fmax(k, -32768.0f), 32767.0f);
+  }
+  int32_t best[CHIMERA_MAX_TQ];
+  for (int j = 0; j < Tq; ++j) best[j] = INT32_MIN;
+  for (const int16_t *v = buf; v < buf + n; v += dim) {
+    for (int j = 0; j < Tq; ++j) {
+      const int16_t *q = qk + (size_t)j * dim;
+      int32_t s = 0;
+      for (int d = 0; d < dim; ++d) s += (int32_t)q[d] * (int32_t)v[d];
+      best[j] = s > best[j] ? s : best[j];
+    }
+  }
+  int64_t F = 0;
+  for (int j = 0; j < Tq; ++j) F += best[j];
+  return F;
+}
+
+int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64_t nb, int64_t q0, int Tq, int TQP,
+                    const float *ST, const int32_t *cand, const int32_t *nval, int ncand, int32_t *fhat,
+                    const CollabOut &o) {
+  if (!idx->collab) idx->collab = new Collab();
+  Collab &C = *idx->collab;
+  const int nthreads = o.nthreads > 0 ? o.nthreads : (int)std::max(1u, std::thread::hardware_concurrency());
+  if (!C.pool || C.pool->threads() != nthreads) {
+    delete C.pool;
+    C.pool = new Pool(nthreads);
+  }
+  const int dim = idx->dim, c = o.chunks;
+  if (int rc = grow_pinned(C.h_cand, C.cap_cand, (size_t)nb * ncand)) return rc;
+  if (int rc = grow_pinned(C.h_fhat, C.cap_fhat, (size_t)nb * ncand)) return rc;
+  if (int rc = grow_pinned(C.h_nval, C.cap_q, (size_t)nb)) return rc;
+  if (int rc = grow_pinned(C.h_qs, C.cap_qs, (size_t)nb * TQP * dim)) return rc;
+  if (!C.ev_sel) CHIMERA_HIP(hipEventCreateWithFlags(&C.ev_sel, hipEventDisableTiming));
+  while ((int)C.ev.size() < c) {
+    hipEvent_t e;
+    CHIMERA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    C.ev.push_back(e);
+  }
+
+  // device side: the kept candidates and the rounded queries, then the
+  // scores chunk by chunk, each chunk's copy behind its own event
+  CHIMERA_HIP(hipMemcpyAsync(C.h_cand, cand, (size_t)nb * ncand * 4, hipMemcpyDeviceToHost, s));
+  CHIMERA_HIP(hipMemcpyAsync(C.h_nval, nval, (size_t)nb * 4, hipMemcpyDeviceToHost, s));
+  CHIMERA_HIP(hipMemcpyAsync(C.h_qs, Qs, (size_t)nb * TQP * dim * 2, hipMemcpyDeviceToHost, s));
+  CHIMERA_HIP(hipEventRecord(C.ev_sel, s));
+  for (int i = 0; i < c; ++i) {
+    const int lo = (int)((int64_t)i * ncand / c), hi = (int)((int64_t)(i + 1) * ncand / c);
+    if (hi > lo) {
+      launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
+                            idx->h_weights, cand, nval, ncand, lo, hi, fhat, s);
+      CHIMERA_HIP(hipGetLastError());
+      CHIMERA_HIP(hipMemcpy2DAsync(C.h_fhat + lo, (size_t)ncand * 4, fhat + lo, (size_t)ncand * 4,
+                                   (size_t)(hi - lo) * 4, nb, hipMemcpyDeviceToHost, s));
+    }
+    CHIMERA_HIP(hipEventRecord(C.ev[i], s));
+  }
+
+  // host side
+  CHIMERA_HIP(hipEventSynchronize(C.ev_sel));
+  C.ranked.resize(nb);
+  C.done.resize(nb);
+  C.full.resize(nb);
+  C.qk.resize((size_t)nb * Tq * dim);
+  C.pool->run(nb, [&](int64_t q) {
+    C.ranked[q].clear();
+    C.done[q].assign(ncand, 0);
+    C.full[q].clear();
+    for (int j = 0; j < Tq; ++j)
+      for (int d = 0; d < dim; ++d)
+        C.qk[((size_t)q * Tq + j) * dim + d] =
+            (int16_t)grid_k_of_float(float_of_bf16(C.h_qs[((size_t)q * TQP + j) * dim + d]));
+  });
+  const uint16_t *tok = idx->fullbit;
+  const int64_t *doc_off = idx->h_doc_off.data();
+  for (int i = 0; i < c; ++i) {
+    CHIMERA_HIP(hipEventSynchronize(C.ev[i]));
+    const int lo = (int)((int64_t)i * ncand / c), hi = (int)((int64_t)(i + 1) * ncand / c);
+    const int64_t budget = ((int64_t)(i + 1) * o.kfb + c - 1) / c;  // ceil((i+1) kfb / c)
+    C.pool->run(nb, [&](int64_t q) {
+      thread_local std::vector<int16_t> buf;
+      const int nv = std::min(C.h_nval[q], hi);
+      std::vector<uint64_t> &R = C.ranked[q];
+      const int32_t *cq = C.h_cand + q * ncand;
+      const int32_t *fq = C.h_fhat + q * ncand;
+      // order key: F^ desc, then candidate position asc (= document id asc)
+      for (int u = lo; u < nv; ++u)
+        R.push_back(((uint64_t)((uint32_t)fq[u] ^ 0x80000000u) << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)u));
+      const int64_t m = std::min<int64_t>(budget, (int64_t)R.size());
+      if (m <= 0) return;
+      std::nth_element(R.begin(), R.begin() + (m - 1), R.end(), std::greater<uint64_t>());
+      for (int64_t r = 0; r < m; ++r) {
+        const uint32_t u = 0xFFFFFFFFu - (uint32_t)R[r];
+        if (C.done[q][u]) continue;
+        C.done[q][u] = 1;
+        const int32_t V = cq[u];
+        const int64_t L = doc_off[V + 1] - doc_off[V];
+        if ((int64_t)buf.size() < L * dim) buf.resize((size_t)L * dim);
+        const int64_t F = full_score(C.qk.data() + (size_t)q * Tq * dim, Tq, dim, tok, doc_off[V], doc_off[V + 1],
+                                     buf.data());
+        C.full[q].emplace_back(F, V);
+      }
+    });
+  }
+  C.pool->run(nb, [&](int64_t q) {
+    auto &Fq = C.full[q];
+    const int kk = std::min<int>(o.k, (int)Fq.size());
+    auto better = [](const std::pair<int64_t, int32_t> &a, const std::pair<int64_t, int32_t> &b) {
+      return a.first != b.first ? a.first > b.first : a.second < b.second;
+    };
+    std::partial_sort(Fq.begin(), Fq.begin() + kk, Fq.end(), better);
+    int32_t *ids = o.ids + (q0 + q) * o.k;
+    float *sc = o.scores + (q0 + q) * o.k;
+    for (int r = 0; r < o.k; ++r) {
+      ids[r] = r < kk ? Fq[r].second : -1;
+      sc[r] = r < kk ? (float)Fq[r].first * (1.0f / 4194304.0f) : -INFINITY;
+    }
+    o.n_full[q0 + q] = (int32_t)Fq.size();
+  });
+  return CHIMERA_OK;
+}
+
+}  // namespace chimera
+
+using namespace chimera;
+
+extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens, int64_t ntok) {
+  if (!idx) return fail(CHIMERA_E_INVAL, "null index");
+  if (tokens && ntok != idx->ntok)
+    return fail(CHIMERA_E_INVAL, "full-precision store has %lld tokens, the index %lld", (long long)ntok,
+                (long long)idx->ntok);
+  idx->fullbit = tokens;
+  return CHIMERA_OK;
+}

@@ -117,12 +117,26 @@ void launch_refine_walk(const int32_t *cent_ids, const int32_t *cent_keys, const
                         const int64_t *doc_off, const uint8_t *codes, int nbits, const uint16_t *weights_host,
                         int64_t ndocs, int32_t *fp, uint32_t *hist, hipStream_t s);
 
-// Residual scoring: fhat [nq][ncand] i32 keys of the kept documents; ST is
-// [nq][ncent + 1][TQP] (row ncent all -inf).
+// Residual scoring of candidates lo .. hi-1 of each query (those below
+// n_valid): fhat [nq][ncand] i32 keys; ST is [nq][ncent + 1][TQP] (row ncent
+// all -inf).
 void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,
                            const int64_t *doc_off, const int32_t *cid, const uint8_t *codes, int nbits,
                            const uint16_t *weights_host, const int32_t *cand_ids, const int32_t *n_valid,
-                           int ncand, int32_t *fhat, hipStream_t s);
+                           int ncand, int lo, int hi, int32_t *fhat, hipStream_t s);
+
+// Collaborative scoring of one sub-batch (collab.cpp): ids, scores, n_full
+// are host arrays for the whole batch, written at query q0 onwards.
+struct CollabOut {
+  int kfb = 0, chunks = 1, k = 1, nthreads = 0;
+  int32_t *ids = nullptr;
+  float *scores = nullptr;
+  int32_t *n_full = nullptr;
+};
+int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64_t nb, int64_t q0, int Tq, int TQP,
+                    const float *ST, const int32_t *cand, const int32_t *nval, int ncand, int32_t *fhat,
+                    const CollabOut &o);
+void collab_free(chimera_index *idx);
 
 // Final top-k: ids/scores [nq][k].
 void launch_topk(const int32_t *fhat, const int32_t *cand_ids, const int32_t *n_valid, int64_t nq, int ncand,
@@ -131,6 +145,10 @@ void launch_topk(const int32_t *fhat, const int32_t *cand_ids, const int32_t *n_
 }  // namespace chimera
 
 // ---- the opaque handle -----------------------------------------------------
+namespace chimera {
+struct Collab;
+}
+
 struct chimera_index {
   int device = 0;
   int32_t ncent = 0, dim = 0, nbits = 0, max_doc_len = 0;
@@ -156,6 +174,10 @@ struct chimera_index {
   hipEvent_t scratch_done = nullptr;
   bool scratch_pending = false;
   std::atomic<int> busy{0};
+  // CPU-GPU collaborative scoring (collab.cpp)
+  std::vector<int64_t> h_doc_off;      // host copy of doc_off [ndocs + 1]
+  const uint16_t *fullbit = nullptr;   // caller-owned host tokens [ntok][dim] bf16
+  chimera::Collab *collab = nullptr;   // pinned staging, events, host threads
   // per-stage timing
   bool timing = false;
   std::vector<hipEvent_t> ev;  // 7 events per sub-batch

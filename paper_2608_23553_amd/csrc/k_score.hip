@@ -170,7 +170,7 @@ __global__ __launch_bounds__(256) void k_residual_score(
     const uint16_t *__restrict__ Qs, int64_t nq, int Tq, const float *__restrict__ ST, int ncent,
     const int64_t *__restrict__ doc_off, const int32_t *__restrict__ cid, const uint8_t *__restrict__ codes,
     uint4 w_lo, uint4 w_hi, const int32_t *__restrict__ cand_ids, const int32_t *__restrict__ n_valid, int ncand,
-    int dpw, int nchunks, int32_t *__restrict__ fhat) {
+    int lo, int hi, int dpw, int nchunks, int32_t *__restrict__ fhat) {
   constexpr int TQP = NCB * 32;
   // 2-bit: byte -> 4 weights (two bf16x2 words); 4-bit: byte -> 2 weights
   __shared__ uint2 lut2[NBITS == 2 ? 256 : 1];
@@ -197,8 +197,9 @@ __global__ __launch_bounds__(256) void k_residual_score(
   const int64_t q = nq >= 8 ? (b & 7) + 8 * (int64_t)((b >> 3) / nchunks) : b / nchunks;
   const int chunk = nq >= 8 ? (b >> 3) % nchunks : b % nchunks;
   if (q >= nq) return;
-  const int nv = n_valid[q];
-  // this wave's documents: candidates d0 .. d0 + nd - 1
+  // candidates lo .. min(hi, n_valid) - 1 of query q
+  const int nv = min(n_valid[q], hi) - lo;
+  // this wave's documents: those candidates' d0 .. d0 + nd - 1
   const int d0 = (chunk * 4 + wave) * dpw;
   const int nd = min(dpw, nv - d0);
   if (nd <= 0) return;
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(256) void k_residual_score(
   W.my_beg = 0;
   W.my_len = 0;
   if (lane < nd) {
-    const int32_t V = cand_ids[q * ncand + d0 + lane];
+    const int32_t V = cand_ids[q * ncand + lo + d0 + lane];
     W.my_beg = doc_off[V];
     W.my_len = (int)(doc_off[V + 1] - W.my_beg);
   }
@@ -231,7 +232,7 @@ __global__ __launch_bounds__(256) void k_residual_score(
 #pragma unroll
     for (int s = 0; s < 8; ++s) bq[cb][s] = as_bf16x8(qp[s]);
   }
-  int32_t *fout = fhat + q * ncand + d0;
+  int32_t *fout = fhat + q * ncand + lo + d0;
 
   // cursors of tiles t (c0), t+1 (c1), t+2 (c2)
   RsCur c0, c1, c2;
@@ -324,8 +325,8 @@ __global__ __launch_bounds__(256) void k_residual_score(
 void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, const float *ST, int ncent,
                            const int64_t *doc_off, const int32_t *cid, const uint8_t *codes, int nbits,
                            const uint16_t *weights_host, const int32_t *cand_ids, const int32_t *n_valid, int ncand,
-                           int32_t *fhat, hipStream_t s) {
-  if (nq <= 0 || ncand <= 0) return;
+                           int lo, int hi, int32_t *fhat, hipStream_t s) {
+  if (nq <= 0 || hi <= lo) return;
   uint32_t w[8] = {0};
   const int B = 1 << nbits;
   for (int u = 0; u < B; ++u) w[u >> 1] |= (uint32_t)weights_host[u] << (16 * (u & 1));
@@ -334,12 +335,13 @@ void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, cons
   // documents per wave put more queries' S^T tables in flight per XCD, fewer
   // add per-wave setup), fewer for small batches so that the chip still gets
   // about 2048 workgroups
-  const int dpw = (int)std::max<int64_t>(1, std::min<int64_t>(8, (int64_t)ncand * nq / (4 * 2048)));
-  const int nchunks = (ncand + 4 * dpw - 1) / (4 * dpw);
+  const int span = hi - lo;
+  const int dpw = (int)std::max<int64_t>(1, std::min<int64_t>(8, (int64_t)span * nq / (4 * 2048)));
+  const int nchunks = (span + 4 * dpw - 1) / (4 * dpw);
   const int64_t blocks = (nq >= 8 ? (nq + 7) / 8 * 8 : nq) * nchunks;
 #define CHIMERA_RS(NB, NC)                                                                                        \
   hipLaunchKernelGGL((k_residual_score<NB, NC>), dim3((unsigned)blocks), dim3(256), 0, s, Qs, nq, Tq, ST, ncent, \
-                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, dpw, nchunks, fhat)
+                     doc_off, cid, codes, w_lo, w_hi, cand_ids, n_valid, ncand, lo, hi, dpw, nchunks, fhat)
   if (nbits == 2 && TQP == 32) CHIMERA_RS(2, 1);
   else if (nbits == 2) CHIMERA_RS(2, 2);
   else if (TQP == 32) CHIMERA_RS(4, 1);

@@ -37,6 +37,9 @@ def test_null_arguments_are_rejected_without_gpu():
                                    None) == chimera.E_INVAL
     assert L.chimera_prune_refine(None, None, 0, 1, 32, 128, 2, 10, chimera.REFINE_TOKEN, None, None, None,
                                   None) == chimera.E_INVAL
+    assert L.chimera_search_collab(None, None, 0, 1, 32, 128, 2, 256, 40, 4, 10, None, None, None, 0,
+                                   None) == chimera.E_INVAL
+    assert L.chimera_fullbit_attach(None, None, 0) == chimera.E_INVAL
     assert L.chimera_index_info_get(None, None) == chimera.E_INVAL
     assert L.chimera_index_load(None, 0, None) == chimera.E_INVAL
     assert L.chimera_stage_times(None, None) == chimera.E_INVAL

@@ -368,3 +368,62 @@ def test_tiny_negated_queries(refine):
     q, _ = c.queries(4, 32, query_seed=18)
     check_search(idx, oi, (-q.astype(np.int32)).astype(np.int16), 2, 256, 10, "bf16",
                  f"tiny negated refine={refine}", refine=refine)
+
+
+# ------------------------------------- CPU-GPU collaborative scoring (Alg. 3)
+def check_collab(name, idx, oi, k_, qk, nprobe, ncand, kfb, chunks, k, nthreads=0):
+    say("collab", name, qk.shape, nprobe, ncand, kfb, chunks, k)
+    gi, gs, gn = idx.search_collab(q_tensor(qk, "bf16"), nprobe, ncand, kfb, chunks, k, nthreads=nthreads)
+    ref = oi.search_collab(qk, k_, nprobe, ncand, kfb, chunks, k)
+    assert np.array_equal(gi, ref["ids"]), f"{name}: ids differ"
+    assert np.array_equal(gs, ref["scores"]), f"{name}: scores differ"
+    assert np.array_equal(gn, ref["n_full"]), f"{name}: full-precision counts differ"
+    return gi, gs, gn
+
+
+@pytest.mark.parametrize("kfb_mult,chunks", [(1, 1), (2, 3), (4, 4), (3, 64)])
+def test_tiny_collab_search(kfb_mult, chunks):
+    w, c, k_, cl, oi, idx = setup("tiny")
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    q, src = c.queries(8, 32)
+    gi, _, gn = check_collab("tiny", idx, oi, k_, q, w.nprobe, w.ncand, kfb_mult * w.k, chunks, w.k)
+    assert np.all(gi[:, 0] == src)
+    assert np.all(gn >= min(kfb_mult * w.k, w.ncand))
+
+
+def test_tiny_collab_edges():
+    """More chunks than candidates (empty chunks), a budget above ncand, k =
+    kfb, one host thread, and a query batch split into sub-batches."""
+    w, c, k_, cl, oi, idx = setup("tiny")
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    q, _ = c.queries(5, 32)
+    check_collab("tiny ncand 5, 8 chunks", idx, oi, k_, q, w.nprobe, 5, 5, 8, 3)
+    check_collab("tiny kfb > ncand", idx, oi, k_, q, w.nprobe, 20, 50, 3, 20)
+    check_collab("tiny one thread", idx, oi, k_, q, w.nprobe, w.ncand, 30, 4, w.k, nthreads=1)
+    check_collab("tiny ragged Tq", idx, oi, k_, q[:, :7], w.nprobe, w.ncand, 30, 4, w.k)
+
+
+def test_collab_rejects_bad_arguments():
+    w, c, k_, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(2, 32)
+    Q = q_tensor(q, "bf16")
+    idx.attach_fullbit(None)
+    with pytest.raises(ChimeraError) as e:
+        idx.search_collab(Q, w.nprobe, w.ncand, 20, 2, w.k)
+    assert e.value.code == chimera.E_INVAL
+    with pytest.raises(ChimeraError):
+        idx.attach_fullbit(synth.k_to_bf16_bits(k_)[:-1])
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    for kfb, chunks, k in [(5, 2, 10), (20, 0, 10), (20, 65, 10)]:
+        with pytest.raises(ChimeraError) as e:
+            idx.search_collab(Q, w.nprobe, w.ncand, kfb, chunks, k)
+        assert e.value.code == chimera.E_INVAL
+
+
+def test_100k_collab_search():
+    w, c, k_, cl, oi, idx = setup("100k")
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    q, src = c.queries(8, 32)
+    gi, _, gn = check_collab("100k", idx, oi, k_, q, w.nprobe, w.ncand, 100, 4, w.k)
+    assert np.all(gi[:, 0] == src)
+    say("100k collab full-precision scores per query", gn.tolist())
