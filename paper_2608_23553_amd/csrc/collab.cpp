@@ -14,10 +14,14 @@
 // them), so a product is an integer in units of 2^-22, a 128-term dot
 // product fits int32, and the sum over query tokens is int64.
 #include <hip/hip_runtime.h>
+#include <immintrin.h>
 
 #include <algorithm>
 #include <cmath>
 #include <atomic>
+#include <chrono>
+#include <cstdio>
+#include <cstdlib>
 #include <condition_variable>
 #include <cstring>
 #include <functional>
@@ -112,7 +116,7 @@ struct Collab {
   std::vector<std::vector<uint64_t>> ranked;              // GPU order keys of the candidates seen so far
   std::vector<std::vector<uint8_t>> done;                 // candidate has a full-precision score
   std::vector<std::vector<std::pair<int64_t, int32_t>>> full;  // (F, doc id)
-  std::vector<int16_t> qk;                                // [nb][Tq][dim] query grid integers
+  std::vector<int16_t> qk;                                // [nb][dim/2][TqP][2] query grid integers
 };
 
 static void free_pinned(void *&p) {
@@ -147,36 +151,149 @@ static int grow_pinned(T *&p, size_t &cap, size_t n) {
   return CHIMERA_OK;
 }
 
+// ------------------------------------------------ full-precision scores
 // F(V) = sum_j max_t <Q_j, v_t> in units of 2^-22 (Def. 1 on the
-// full-precision tokens); an empty document scores INT64_MIN.  A bf16 value
-// v reads as the grid integer nearbyint(2048 v), which is what the builder
-// makes of it (an integer already when |v| >= 2^-4).  Grid integers are at
-// most 2^11 in magnitude (|value| <= 1), so a product is below 2^22 and a
-// 128-term dot product below 2^29.  One function, so that the conversion
-// and the dot products vectorise together (AVX2 where the host has it).
-__attribute__((target_clones("avx2", "default"))) static int64_t full_score(const int16_t *qk, int Tq, int dim,
-                                                                             const uint16_t *tok, int64_t t0,
-                                                                             int64_t t1, int16_t *buf) {
-  if (t1 <= t0) return INT64_MIN;
-  const int64_t n = (t1 - t0) * dim;
-  const uint16_t *src = tok + t0 * dim;
+// full-precision tokens).  A bf16 value v reads as the grid integer
+// nearbyint(2048 v), which is what the builder makes of it (an integer
+// already when |v| >= 2^-4).  Grid integers are at most 2^11 in magnitude
+// (|value| <= 1), so a product is below 2^22 and a 128-term dot product below
+// 2^29 (int32); the sum over query tokens is int64.
+//
+// The query is kept pair-interleaved and token-minor, qp[p][j][2] = (Q_j[2p],
+// Q_j[2p+1]) with j padded to a multiple of 16, so that one multiply-add
+// instruction takes 8 (AVX2) or 16 (AVX-512) query tokens times two
+// dimensions of one document token, broadcast, and no horizontal sums are
+// needed: each lane accumulates one query token's dot product.
+constexpr int kQBlock = 16;
+static_assert(CHIMERA_DIM == 128, "the full-precision kernels take 64 dimension pairs per token");
+
+static inline __attribute__((always_inline)) void to_grid(const uint16_t *src, int64_t n, int16_t *dst) {
   for (int64_t i = 0; i < n; ++i) {
     const uint32_t u = (uint32_t)src[i] << 16;
     float v;
     std::memcpy(&v, &u, 4);
     const float k = std::nearbyint(v * 2048.0f);
-    buf[i] = (int16_t)(int32_t)std::fmin(std::fmax(k, -32768.0f), 32767.0f);
+    dst[i] = (int16_t)(int32_t)std::fmin(std::fmax(k, -32768.0f), 32767.0f);
   }
-  int32_t best[CHIMERA_MAX_TQ];
-  for (int j = 0; j < Tq; ++j) best[j] = INT32_MIN;
-  for (const int16_t *v = buf; v < buf + n; v += dim) {
-    for (int j = 0; j < Tq; ++j) {
-      const int16_t *q = qk + (size_t)j * dim;
+}
+
+// best[j] = max over the L tokens of v of <qp_j, v_t>, for j < TqP
+typedef void (*MaxDotFn)(const int16_t *qp, int TqP, const int16_t *v, int64_t L, int32_t *best);
+
+__attribute__((target("avx512f,avx512bw,avx512vnni"))) static void maxdot_vnni(const int16_t *qp, int TqP,
+                                                                               const int16_t *v, int64_t L,
+                                                                               int32_t *best) {
+  const int32_t *v2 = (const int32_t *)v;  // dimension pairs
+  for (int jb = 0; jb < TqP; jb += 16) {
+    __m512i bm = _mm512_set1_epi32(INT32_MIN);
+    int64_t t = 0;
+    for (; t + 4 <= L; t += 4) {
+      __m512i a0 = _mm512_setzero_si512(), a1 = a0, a2 = a0, a3 = a0;
+      const int32_t *w = v2 + t * 64;
+      for (int p = 0; p < 64; ++p) {
+        const __m512i q = _mm512_loadu_si512((const void *)(qp + ((size_t)p * TqP + jb) * 2));
+        a0 = _mm512_dpwssd_epi32(a0, q, _mm512_set1_epi32(w[p]));
+        a1 = _mm512_dpwssd_epi32(a1, q, _mm512_set1_epi32(w[64 + p]));
+        a2 = _mm512_dpwssd_epi32(a2, q, _mm512_set1_epi32(w[128 + p]));
+        a3 = _mm512_dpwssd_epi32(a3, q, _mm512_set1_epi32(w[192 + p]));
+      }
+      bm = _mm512_max_epi32(bm, _mm512_max_epi32(_mm512_max_epi32(a0, a1), _mm512_max_epi32(a2, a3)));
+    }
+    for (; t < L; ++t) {
+      __m512i a0 = _mm512_setzero_si512();
+      for (int p = 0; p < 64; ++p)
+        a0 = _mm512_dpwssd_epi32(a0, _mm512_loadu_si512((const void *)(qp + ((size_t)p * TqP + jb) * 2)),
+                                 _mm512_set1_epi32(v2[t * 64 + p]));
+      bm = _mm512_max_epi32(bm, a0);
+    }
+    _mm512_storeu_si512((void *)(best + jb), bm);
+  }
+}
+
+__attribute__((target("avx2"))) static void maxdot_avx2(const int16_t *qp, int TqP, const int16_t *v, int64_t L,
+                                                        int32_t *best) {
+  const int32_t *v2 = (const int32_t *)v;
+  for (int jb = 0; jb < TqP; jb += 8) {
+    __m256i bm = _mm256_set1_epi32(INT32_MIN);
+    int64_t t = 0;
+    for (; t + 4 <= L; t += 4) {
+      __m256i a0 = _mm256_setzero_si256(), a1 = a0, a2 = a0, a3 = a0;
+      const int32_t *w = v2 + t * 64;
+      for (int p = 0; p < 64; ++p) {
+        const __m256i q = _mm256_loadu_si256((const __m256i *)(qp + ((size_t)p * TqP + jb) * 2));
+        a0 = _mm256_add_epi32(a0, _mm256_madd_epi16(q, _mm256_set1_epi32(w[p])));
+        a1 = _mm256_add_epi32(a1, _mm256_madd_epi16(q, _mm256_set1_epi32(w[64 + p])));
+        a2 = _mm256_add_epi32(a2, _mm256_madd_epi16(q, _mm256_set1_epi32(w[128 + p])));
+        a3 = _mm256_add_epi32(a3, _mm256_madd_epi16(q, _mm256_set1_epi32(w[192 + p])));
+      }
+      bm = _mm256_max_epi32(bm, _mm256_max_epi32(_mm256_max_epi32(a0, a1), _mm256_max_epi32(a2, a3)));
+    }
+    for (; t < L; ++t) {
+      __m256i a0 = _mm256_setzero_si256();
+      for (int p = 0; p < 64; ++p)
+        a0 = _mm256_add_epi32(a0, _mm256_madd_epi16(_mm256_loadu_si256((const __m256i *)(qp + ((size_t)p * TqP + jb) * 2)),
+                                                    _mm256_set1_epi32(v2[t * 64 + p])));
+      bm = _mm256_max_epi32(bm, a0);
+    }
+    _mm256_storeu_si256((__m256i *)(best + jb), bm);
+  }
+}
+
+static void maxdot_plain(const int16_t *qp, int TqP, const int16_t *v, int64_t L, int32_t *best) {
+  for (int j = 0; j < TqP; ++j) best[j] = INT32_MIN;
+  for (int64_t t = 0; t < L; ++t)
+    for (int j = 0; j < TqP; ++j) {
       int32_t s = 0;
-      for (int d = 0; d < dim; ++d) s += (int32_t)q[d] * (int32_t)v[d];
+      for (int p = 0; p < 64; ++p)
+        s += (int32_t)qp[((size_t)p * TqP + j) * 2] * v[t * 128 + 2 * p] +
+             (int32_t)qp[((size_t)p * TqP + j) * 2 + 1] * v[t * 128 + 2 * p + 1];
       best[j] = s > best[j] ? s : best[j];
     }
+}
+
+// to_grid compiled for AVX2 (a vector round-to-nearest-even) where the host
+// has it; the baseline build rounds value by value through the C library
+typedef void (*ToGridFn)(const uint16_t *src, int64_t n, int16_t *dst);
+__attribute__((target("avx2"))) static void to_grid_avx2(const uint16_t *src, int64_t n, int16_t *dst) {
+  const __m256 scale = _mm256_set1_ps(2048.0f);
+  int64_t i = 0;
+  for (; i + 16 <= n; i += 16) {
+    const __m256i b = _mm256_loadu_si256((const __m256i *)(src + i));
+    // bf16 -> f32: the 16 bits become the high half of each 32-bit lane
+    const __m256i lo = _mm256_unpacklo_epi16(_mm256_setzero_si256(), b);
+    const __m256i hi = _mm256_unpackhi_epi16(_mm256_setzero_si256(), b);
+    const __m256 flo = _mm256_round_ps(_mm256_mul_ps(_mm256_castsi256_ps(lo), scale),
+                                       _MM_FROUND_TO_NEAREST_INT | _MM_FROUND_NO_EXC);
+    const __m256 fhi = _mm256_round_ps(_mm256_mul_ps(_mm256_castsi256_ps(hi), scale),
+                                       _MM_FROUND_TO_NEAREST_INT | _MM_FROUND_NO_EXC);
+    // the saturating pack clamps to int16 and undoes the unpack's lane order
+    _mm256_storeu_si256((__m256i *)(dst + i), _mm256_packs_epi32(_mm256_cvtps_epi32(flo), _mm256_cvtps_epi32(fhi)));
   }
+  to_grid(src + i, n - i, dst + i);
+}
+static void to_grid_plain(const uint16_t *src, int64_t n, int16_t *dst) { to_grid(src, n, dst); }
+static ToGridFn pick_to_grid() {
+  __builtin_cpu_init();
+  return __builtin_cpu_supports("avx2") ? to_grid_avx2 : to_grid_plain;
+}
+static const ToGridFn g_to_grid = pick_to_grid();
+
+static MaxDotFn pick_maxdot() {
+  __builtin_cpu_init();
+  if (__builtin_cpu_supports("avx512vnni") && __builtin_cpu_supports("avx512bw")) return maxdot_vnni;
+  if (__builtin_cpu_supports("avx2")) return maxdot_avx2;
+  return maxdot_plain;
+}
+
+// F(V) for the document of tokens [t0, t1); an empty document scores
+// INT64_MIN.  buf holds at least (t1 - t0) * 128 values.
+static int64_t full_score(const int16_t *qp, int Tq, int TqP, const uint16_t *tok, int64_t t0, int64_t t1,
+                          int16_t *buf) {
+  static const MaxDotFn maxdot = pick_maxdot();
+  if (t1 <= t0) return INT64_MIN;
+  g_to_grid(tok + t0 * 128, (t1 - t0) * 128, buf);
+  int32_t best[CHIMERA_MAX_TQ + kQBlock];
+  maxdot(qp, TqP, buf, t1 - t0, best);
   int64_t F = 0;
   for (int j = 0; j < Tq; ++j) F += best[j];
   return F;
@@ -222,25 +339,40 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     CHIMERA_HIP(hipEventRecord(C.ev[i], s));
   }
 
-  // host side
+  // host side; CHIMERA_COLLAB_TRACE=1 prints where the host time goes
+  static const bool trace = std::getenv("CHIMERA_COLLAB_TRACE") != nullptr;
+  using clk = std::chrono::steady_clock;
+  auto tp = clk::now();
+  double t_wait = 0, t_work = 0;
+  auto lap = [&](double &acc) {
+    const auto now = clk::now();
+    acc += std::chrono::duration<double, std::milli>(now - tp).count();
+    tp = now;
+  };
   CHIMERA_HIP(hipEventSynchronize(C.ev_sel));
+  lap(t_wait);
   C.ranked.resize(nb);
   C.done.resize(nb);
   C.full.resize(nb);
-  C.qk.resize((size_t)nb * Tq * dim);
+  const int TqP = (Tq + kQBlock - 1) / kQBlock * kQBlock;
+  C.qk.assign((size_t)nb * TqP * dim, 0);
   C.pool->run(nb, [&](int64_t q) {
     C.ranked[q].clear();
     C.done[q].assign(ncand, 0);
     C.full[q].clear();
-    for (int j = 0; j < Tq; ++j)
-      for (int d = 0; d < dim; ++d)
-        C.qk[((size_t)q * Tq + j) * dim + d] =
-            (int16_t)grid_k_of_float(float_of_bf16(C.h_qs[((size_t)q * TQP + j) * dim + d]));
+    int16_t *qp = C.qk.data() + (size_t)q * TqP * dim;  // [dim/2][TqP][2]
+    int16_t row[CHIMERA_DIM];
+    for (int j = 0; j < Tq; ++j) {
+      g_to_grid(C.h_qs + ((size_t)q * TQP + j) * dim, dim, row);
+      for (int d = 0; d < dim; ++d) qp[((size_t)(d >> 1) * TqP + j) * 2 + (d & 1)] = row[d];
+    }
   });
   const uint16_t *tok = idx->fullbit;
   const int64_t *doc_off = idx->h_doc_off.data();
+  lap(t_work);
   for (int i = 0; i < c; ++i) {
     CHIMERA_HIP(hipEventSynchronize(C.ev[i]));
+    lap(t_wait);
     const int lo = (int)((int64_t)i * ncand / c), hi = (int)((int64_t)(i + 1) * ncand / c);
     const int64_t budget = ((int64_t)(i + 1) * o.kfb + c - 1) / c;  // ceil((i+1) kfb / c)
     C.pool->run(nb, [&](int64_t q) {
@@ -262,11 +394,12 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
         const int32_t V = cq[u];
         const int64_t L = doc_off[V + 1] - doc_off[V];
         if ((int64_t)buf.size() < L * dim) buf.resize((size_t)L * dim);
-        const int64_t F = full_score(C.qk.data() + (size_t)q * Tq * dim, Tq, dim, tok, doc_off[V], doc_off[V + 1],
+        const int64_t F = full_score(C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V], doc_off[V + 1],
                                      buf.data());
         C.full[q].emplace_back(F, V);
       }
     });
+    lap(t_work);
   }
   C.pool->run(nb, [&](int64_t q) {
     auto &Fq = C.full[q];
@@ -283,6 +416,10 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     }
     o.n_full[q0 + q] = (int32_t)Fq.size();
   });
+  lap(t_work);
+  if (trace)
+    std::fprintf(stderr, "[collab] %lld queries, %d chunks, %d threads: waiting on the GPU %.3f ms, host work %.3f ms\n",
+                 (long long)nb, c, C.pool->threads(), t_wait, t_work);
   return CHIMERA_OK;
 }
 
