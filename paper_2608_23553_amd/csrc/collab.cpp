@@ -272,28 +272,31 @@ __attribute__((target("avx2"))) static void to_grid_avx2(const uint16_t *src, in
   to_grid(src + i, n - i, dst + i);
 }
 static void to_grid_plain(const uint16_t *src, int64_t n, int16_t *dst) { to_grid(src, n, dst); }
-static ToGridFn pick_to_grid() {
+// The widest instruction set the host has, capped by CHIMERA_COLLAB_ISA
+// (plain, avx2 or vnni; read at every search, so tests can run each path).
+struct HostKernels {
+  ToGridFn to_grid;
+  MaxDotFn maxdot;
+};
+static HostKernels pick_kernels() {
   __builtin_cpu_init();
-  return __builtin_cpu_supports("avx2") ? to_grid_avx2 : to_grid_plain;
-}
-static const ToGridFn g_to_grid = pick_to_grid();
-
-static MaxDotFn pick_maxdot() {
-  __builtin_cpu_init();
-  if (__builtin_cpu_supports("avx512vnni") && __builtin_cpu_supports("avx512bw")) return maxdot_vnni;
-  if (__builtin_cpu_supports("avx2")) return maxdot_avx2;
-  return maxdot_plain;
+  const bool avx2 = __builtin_cpu_supports("avx2");
+  const bool vnni = avx2 && __builtin_cpu_supports("avx512vnni") && __builtin_cpu_supports("avx512bw");
+  const char *cap = std::getenv("CHIMERA_COLLAB_ISA");
+  const int level = !cap ? 2 : !std::strcmp(cap, "plain") ? 0 : !std::strcmp(cap, "avx2") ? 1 : 2;
+  if (vnni && level >= 2) return {to_grid_avx2, maxdot_vnni};
+  if (avx2 && level >= 1) return {to_grid_avx2, maxdot_avx2};
+  return {to_grid_plain, maxdot_plain};
 }
 
 // F(V) for the document of tokens [t0, t1); an empty document scores
 // INT64_MIN.  buf holds at least (t1 - t0) * 128 values.
-static int64_t full_score(const int16_t *qp, int Tq, int TqP, const uint16_t *tok, int64_t t0, int64_t t1,
-                          int16_t *buf) {
-  static const MaxDotFn maxdot = pick_maxdot();
+static int64_t full_score(const HostKernels &K, const int16_t *qp, int Tq, int TqP, const uint16_t *tok, int64_t t0,
+                          int64_t t1, int16_t *buf) {
   if (t1 <= t0) return INT64_MIN;
-  g_to_grid(tok + t0 * 128, (t1 - t0) * 128, buf);
+  K.to_grid(tok + t0 * 128, (t1 - t0) * 128, buf);
   int32_t best[CHIMERA_MAX_TQ + kQBlock];
-  maxdot(qp, TqP, buf, t1 - t0, best);
+  K.maxdot(qp, TqP, buf, t1 - t0, best);
   int64_t F = 0;
   for (int j = 0; j < Tq; ++j) F += best[j];
   return F;
@@ -310,6 +313,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     C.pool = new Pool(nthreads);
   }
   const int dim = idx->dim, c = o.chunks;
+  const HostKernels K = pick_kernels();
   if (int rc = grow_pinned(C.h_cand, C.cap_cand, (size_t)nb * ncand)) return rc;
   if (int rc = grow_pinned(C.h_fhat, C.cap_fhat, (size_t)nb * ncand)) return rc;
   if (int rc = grow_pinned(C.h_nval, C.cap_q, (size_t)nb)) return rc;
@@ -363,7 +367,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     int16_t *qp = C.qk.data() + (size_t)q * TqP * dim;  // [dim/2][TqP][2]
     int16_t row[CHIMERA_DIM];
     for (int j = 0; j < Tq; ++j) {
-      g_to_grid(C.h_qs + ((size_t)q * TQP + j) * dim, dim, row);
+      K.to_grid(C.h_qs + ((size_t)q * TQP + j) * dim, dim, row);
       for (int d = 0; d < dim; ++d) qp[((size_t)(d >> 1) * TqP + j) * 2 + (d & 1)] = row[d];
     }
   });
@@ -394,8 +398,8 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
         const int32_t V = cq[u];
         const int64_t L = doc_off[V + 1] - doc_off[V];
         if ((int64_t)buf.size() < L * dim) buf.resize((size_t)L * dim);
-        const int64_t F = full_score(C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V], doc_off[V + 1],
-                                     buf.data());
+        const int64_t F = full_score(K, C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V],
+                                     doc_off[V + 1], buf.data());
         C.full[q].emplace_back(F, V);
       }
     });

@@ -403,6 +403,18 @@ def test_tiny_collab_edges():
     check_collab("tiny ragged Tq", idx, oi, k_, q[:, :7], w.nprobe, w.ncand, 30, 4, w.k)
 
 
+@pytest.mark.parametrize("isa", ["plain", "avx2", "vnni"])
+def test_tiny_collab_each_host_instruction_set(isa, monkeypatch):
+    """The host half's kernels for each instruction set (capped by
+    CHIMERA_COLLAB_ISA; a host without it runs the next one down)."""
+    w, c, k_, cl, oi, idx = setup("tiny")
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    monkeypatch.setenv("CHIMERA_COLLAB_ISA", isa)
+    q, _ = c.queries(6, 32)
+    check_collab(f"tiny {isa}", idx, oi, k_, q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    check_collab(f"tiny {isa} Tq 19", idx, oi, k_, q[:, :19], w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+
+
 def test_collab_rejects_bad_arguments():
     w, c, k_, cl, oi, idx = setup("tiny")
     q, _ = c.queries(2, 32)
