@@ -5,6 +5,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <new>
 
 #include "internal.h"
 
@@ -141,6 +142,19 @@ static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype
 }
 
 static const int kMaxK = 8192;
+
+// No C++ exception leaves the C ABI: host allocations inside a call that fail
+// report E_NOMEM.
+template <class F>
+static int guarded(F &&f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc &) {
+    return fail(CHIMERA_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(CHIMERA_E_INVAL, "internal error");
+  }
+}
 
 // ------------------------------------------------------------- pipeline
 enum Stop { STOP_PROBE = 1, STOP_CANDIDATES = 2, STOP_PRUNE = 3, STOP_FULL = 4, STOP_COLLAB = 5 };
@@ -410,7 +424,9 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
   Outs o;
   o.ids = ids;
   o.scores = scores;
-  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine);
+  return guarded([&] {
+    return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine);
+  });
 }
 
 int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
@@ -444,7 +460,7 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
   Outs o;
   o.collab = &co;
   hipStream_t s = (hipStream_t)hip_stream;
-  rc = run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_COLLAB, o, s);
+  rc = guarded([&] { return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_COLLAB, o, s); });
   if (rc) return rc;
   CHIMERA_HIP(hipStreamSynchronize(s));
   return CHIMERA_OK;
@@ -463,7 +479,9 @@ int chimera_probe(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, in
   Outs o;
   o.cent_ids = cent_ids;
   o.cent_keys = cent_keys;
-  return run(idx, Q, q_dtype, nq, Tq, nprobe, 1, 1, STOP_PROBE, o, (hipStream_t)hip_stream);
+  return guarded([&] {
+    return run(idx, Q, q_dtype, nq, Tq, nprobe, 1, 1, STOP_PROBE, o, (hipStream_t)hip_stream);
+  });
 }
 
 int chimera_candidates(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
@@ -484,7 +502,9 @@ int chimera_candidates(chimera_index *idx, const void *Q, int q_dtype, int64_t n
   o.offsets = offsets;
   o.doc_ids = doc_ids;
   o.capacity = capacity;
-  return run(idx, Q, q_dtype, nq, Tq, nprobe, 1, 1, STOP_CANDIDATES, o, (hipStream_t)hip_stream);
+  return guarded([&] {
+    return run(idx, Q, q_dtype, nq, Tq, nprobe, 1, 1, STOP_CANDIDATES, o, (hipStream_t)hip_stream);
+  });
 }
 
 int chimera_prune(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,
@@ -512,7 +532,9 @@ int chimera_prune_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t
   o.cand_ids = cand_ids;
   o.cand_keys = cand_keys;
   o.n_valid = n_valid;
-  return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_PRUNE, o, (hipStream_t)hip_stream, refine);
+  return guarded([&] {
+    return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_PRUNE, o, (hipStream_t)hip_stream, refine);
+  });
 }
 
 int chimera_stage_times(chimera_index *idx, float *ms6) {

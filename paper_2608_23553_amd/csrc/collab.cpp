@@ -50,8 +50,9 @@ class Pool {
     for (auto &t : th_) t.join();
   }
   int threads() const { return nworkers_ + 1; }
-  void run(int64_t n, const std::function<void(int64_t)> &fn) {
-    if (n <= 0) return;
+  // false if some fn(i) threw (the others still ran)
+  bool run(int64_t n, const std::function<void(int64_t)> &fn) {
+    if (n <= 0) return true;
     {
       std::lock_guard<std::mutex> lk(mu_);
       fn_ = &fn;
@@ -65,11 +66,18 @@ class Pool {
     std::unique_lock<std::mutex> lk(mu_);
     done_.wait(lk, [this] { return pending_ == 0; });
     fn_ = nullptr;
+    return !failed_.exchange(false);
   }
 
  private:
   void drain(const std::function<void(int64_t)> &fn, int64_t n) {
-    for (int64_t i = next_.fetch_add(1); i < n; i = next_.fetch_add(1)) fn(i);
+    for (int64_t i = next_.fetch_add(1); i < n; i = next_.fetch_add(1)) {
+      try {
+        fn(i);
+      } catch (...) {
+        failed_.store(true);
+      }
+    }
   }
   void work() {
     uint64_t seen = 0;
@@ -98,6 +106,7 @@ class Pool {
   const std::function<void(int64_t)> *fn_ = nullptr;
   int64_t n_ = 0;
   std::atomic<int64_t> next_{0};
+  std::atomic<bool> failed_{false};
   int pending_ = 0;
   uint64_t gen_ = 0;
   bool stop_ = false;
@@ -230,9 +239,10 @@ __attribute__((target("avx2"))) static void maxdot_avx2(const int16_t *qp, int T
     }
     for (; t < L; ++t) {
       __m256i a0 = _mm256_setzero_si256();
-      for (int p = 0; p < 64; ++p)
-        a0 = _mm256_add_epi32(a0, _mm256_madd_epi16(_mm256_loadu_si256((const __m256i *)(qp + ((size_t)p * TqP + jb) * 2)),
-                                                    _mm256_set1_epi32(v2[t * 64 + p])));
+      for (int p = 0; p < 64; ++p) {
+        const __m256i q = _mm256_loadu_si256((const __m256i *)(qp + ((size_t)p * TqP + jb) * 2));
+        a0 = _mm256_add_epi32(a0, _mm256_madd_epi16(q, _mm256_set1_epi32(v2[t * 64 + p])));
+      }
       bm = _mm256_max_epi32(bm, a0);
     }
     _mm256_storeu_si256((__m256i *)(best + jb), bm);
@@ -302,6 +312,13 @@ static int64_t full_score(const HostKernels &K, const int16_t *qp, int Tq, int T
   return F;
 }
 
+// A host task failed (an allocation): drain the stream, whose copies still
+// target the pinned buffers, then report.
+static int host_failed(hipStream_t s) {
+  (void)hipStreamSynchronize(s);
+  return fail(CHIMERA_E_NOMEM, "collaborative scoring: host allocation failed");
+}
+
 int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64_t nb, int64_t q0, int Tq, int TQP,
                     const float *ST, const int32_t *cand, const int32_t *nval, int ncand, int32_t *fhat,
                     const CollabOut &o) {
@@ -360,7 +377,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
   C.full.resize(nb);
   const int TqP = (Tq + kQBlock - 1) / kQBlock * kQBlock;
   C.qk.assign((size_t)nb * TqP * dim, 0);
-  C.pool->run(nb, [&](int64_t q) {
+  if (!C.pool->run(nb, [&](int64_t q) {
     C.ranked[q].clear();
     C.done[q].assign(ncand, 0);
     C.full[q].clear();
@@ -370,7 +387,8 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
       K.to_grid(C.h_qs + ((size_t)q * TQP + j) * dim, dim, row);
       for (int d = 0; d < dim; ++d) qp[((size_t)(d >> 1) * TqP + j) * 2 + (d & 1)] = row[d];
     }
-  });
+  }))
+    return host_failed(s);
   const uint16_t *tok = idx->fullbit;
   const int64_t *doc_off = idx->h_doc_off.data();
   lap(t_work);
@@ -379,7 +397,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     lap(t_wait);
     const int lo = (int)((int64_t)i * ncand / c), hi = (int)((int64_t)(i + 1) * ncand / c);
     const int64_t budget = ((int64_t)(i + 1) * o.kfb + c - 1) / c;  // ceil((i+1) kfb / c)
-    C.pool->run(nb, [&](int64_t q) {
+    if (!C.pool->run(nb, [&](int64_t q) {
       thread_local std::vector<int16_t> buf;
       const int nv = std::min(C.h_nval[q], hi);
       std::vector<uint64_t> &R = C.ranked[q];
@@ -402,10 +420,11 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
                                      doc_off[V + 1], buf.data());
         C.full[q].emplace_back(F, V);
       }
-    });
+    }))
+      return host_failed(s);
     lap(t_work);
   }
-  C.pool->run(nb, [&](int64_t q) {
+  if (!C.pool->run(nb, [&](int64_t q) {
     auto &Fq = C.full[q];
     const int kk = std::min<int>(o.k, (int)Fq.size());
     auto better = [](const std::pair<int64_t, int32_t> &a, const std::pair<int64_t, int32_t> &b) {
@@ -419,11 +438,12 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
       sc[r] = r < kk ? (float)Fq[r].first * (1.0f / 4194304.0f) : -INFINITY;
     }
     o.n_full[q0 + q] = (int32_t)Fq.size();
-  });
+  }))
+    return host_failed(s);
   lap(t_work);
   if (trace)
-    std::fprintf(stderr, "[collab] %lld queries, %d chunks, %d threads: waiting on the GPU %.3f ms, host work %.3f ms\n",
-                 (long long)nb, c, C.pool->threads(), t_wait, t_work);
+    std::fprintf(stderr, "[collab] %lld queries, %d chunks, %d threads: waiting on the GPU %.3f ms, "
+                 "host work %.3f ms\n", (long long)nb, c, C.pool->threads(), t_wait, t_work);
   return CHIMERA_OK;
 }
 
