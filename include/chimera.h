@@ -209,12 +209,13 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
  *
  * chimera_fullbit_attach: tokens is a HOST array [ntok][dim] of bf16 bit
  * patterns, in the index's token order (document-major, the order the
- * builder was given).  The library keeps the pointer, not a copy: the
- * caller keeps the memory alive and unchanged until chimera_index_free or
- * another attach (tokens == NULL detaches).  Each value is read as the
- * builder reads it (snapped onto the value grid), so with the builder's own
- * input the full-precision scores are the exact Chamfer scores of the
- * indexed tokens.  E_INVAL if ntok differs from the index's token count.
+ * builder was given).  The library reads every value onto the value grid,
+ * as the builder does, into a host copy that the index owns (2 bytes per
+ * value, the size of the input), so the caller may free its array after
+ * the call; tokens == NULL drops the copy.  With the builder's own input
+ * the full-precision scores are the exact Chamfer scores of the indexed
+ * tokens.  E_INVAL if ntok differs from the index's token count, E_NOMEM if
+ * the copy cannot be allocated, E_BUSY during another call on the index.
  *
  * chimera_search_collab: steps 1-3 of chimera_search, then Alg. 3 over each
  * query's kept candidates S_refine, taken in ascending document id:

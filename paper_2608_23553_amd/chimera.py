@@ -256,17 +256,15 @@ class Index:
 
     def attach_fullbit(self, tokens_bf16):
         """Attaches the full-precision store: host uint16 [ntok, d] bf16 bits
-        in the index's token order (chimera_fullbit_attach).  The index keeps
-        a reference to the array; None detaches."""
+        in the index's token order (chimera_fullbit_attach, which keeps its own
+        grid-integer copy).  None drops it."""
         if tokens_bf16 is None:
             _check(lib().chimera_fullbit_attach(self._h, None, 0))
-            self._fullbit = None
             return
         a = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
         if a.ndim != 2:
             raise ValueError("tokens must be [ntok, d]")
         _check(lib().chimera_fullbit_attach(self._h, _np(a), a.shape[0]))
-        self._fullbit = a
 
     def search_collab(self, Q, nprobe: int, ncand: int, kfb: int, chunks: int, k: int, nthreads: int = 0,
                       stream=None):

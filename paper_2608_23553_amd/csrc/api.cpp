@@ -434,7 +434,7 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
                           float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream) {
   int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
   if (rc) return rc;
-  if (!idx->fullbit) return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
+  if (idx->fullbit.empty()) return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
   if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
   if (kfb < k) return fail(CHIMERA_E_INVAL, "kfb (%d) must be >= k (%d)", kfb, k);
   if (ncand < 1) return fail(CHIMERA_E_INVAL, "ncand must be >= 1");

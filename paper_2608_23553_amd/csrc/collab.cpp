@@ -26,6 +26,7 @@
 #include <cstring>
 #include <functional>
 #include <mutex>
+#include <new>
 #include <thread>
 #include <vector>
 
@@ -299,14 +300,13 @@ static HostKernels pick_kernels() {
   return {to_grid_plain, maxdot_plain};
 }
 
-// F(V) for the document of tokens [t0, t1); an empty document scores
-// INT64_MIN.  buf holds at least (t1 - t0) * 128 values.
-static int64_t full_score(const HostKernels &K, const int16_t *qp, int Tq, int TqP, const uint16_t *tok, int64_t t0,
-                          int64_t t1, int16_t *buf) {
+// F(V) for the document of tokens [t0, t1) of the grid-integer store; an
+// empty document scores INT64_MIN.
+static int64_t full_score(const HostKernels &K, const int16_t *qp, int Tq, int TqP, const int16_t *tok, int64_t t0,
+                          int64_t t1) {
   if (t1 <= t0) return INT64_MIN;
-  K.to_grid(tok + t0 * 128, (t1 - t0) * 128, buf);
   int32_t best[CHIMERA_MAX_TQ + kQBlock];
-  K.maxdot(qp, TqP, buf, t1 - t0, best);
+  K.maxdot(qp, TqP, tok + t0 * 128, t1 - t0, best);
   int64_t F = 0;
   for (int j = 0; j < Tq; ++j) F += best[j];
   return F;
@@ -389,7 +389,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     }
   }))
     return host_failed(s);
-  const uint16_t *tok = idx->fullbit;
+  const int16_t *tok = idx->fullbit.data();
   const int64_t *doc_off = idx->h_doc_off.data();
   lap(t_work);
   for (int i = 0; i < c; ++i) {
@@ -398,7 +398,6 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     const int lo = (int)((int64_t)i * ncand / c), hi = (int)((int64_t)(i + 1) * ncand / c);
     const int64_t budget = ((int64_t)(i + 1) * o.kfb + c - 1) / c;  // ceil((i+1) kfb / c)
     if (!C.pool->run(nb, [&](int64_t q) {
-      thread_local std::vector<int16_t> buf;
       const int nv = std::min(C.h_nval[q], hi);
       std::vector<uint64_t> &R = C.ranked[q];
       const int32_t *cq = C.h_cand + q * ncand;
@@ -414,10 +413,8 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
         if (C.done[q][u]) continue;
         C.done[q][u] = 1;
         const int32_t V = cq[u];
-        const int64_t L = doc_off[V + 1] - doc_off[V];
-        if ((int64_t)buf.size() < L * dim) buf.resize((size_t)L * dim);
         const int64_t F = full_score(K, C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V],
-                                     doc_off[V + 1], buf.data());
+                                     doc_off[V + 1]);
         C.full[q].emplace_back(F, V);
       }
     }))
@@ -456,6 +453,33 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
   if (tokens && ntok != idx->ntok)
     return fail(CHIMERA_E_INVAL, "full-precision store has %lld tokens, the index %lld", (long long)ntok,
                 (long long)idx->ntok);
-  idx->fullbit = tokens;
-  return CHIMERA_OK;
+  // the same exclusion as every other call on the index
+  if (idx->busy.exchange(1) != 0) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  if (!tokens) {
+    std::vector<int16_t>().swap(idx->fullbit);
+    idx->busy.store(0);
+    return CHIMERA_OK;
+  }
+  int rc = CHIMERA_OK;
+  try {
+    // read every value onto the grid once, here, in parallel slices
+    std::vector<int16_t> store((size_t)ntok * CHIMERA_DIM);
+    const HostKernels K = pick_kernels();
+    const int64_t n = ntok * CHIMERA_DIM;
+    const unsigned nt = std::max(1u, std::min(32u, std::thread::hardware_concurrency()));
+    std::vector<std::thread> th;
+    for (unsigned w = 0; w < nt; ++w)
+      th.emplace_back([&, w] {
+        const int64_t b = n * w / nt, e = n * (w + 1) / nt;
+        K.to_grid(tokens + b, e - b, store.data() + b);
+      });
+    for (auto &t : th) t.join();
+    idx->fullbit.swap(store);
+  } catch (const std::bad_alloc &) {
+    rc = fail(CHIMERA_E_NOMEM, "full-precision store of %lld tokens", (long long)ntok);
+  } catch (...) {
+    rc = fail(CHIMERA_E_NOMEM, "full-precision store: host threads unavailable");
+  }
+  idx->busy.store(0);
+  return rc;
 }

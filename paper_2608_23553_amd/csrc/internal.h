@@ -176,7 +176,7 @@ struct chimera_index {
   std::atomic<int> busy{0};
   // CPU-GPU collaborative scoring (collab.cpp)
   std::vector<int64_t> h_doc_off;      // host copy of doc_off [ndocs + 1]
-  const uint16_t *fullbit = nullptr;   // caller-owned host tokens [ntok][dim] bf16
+  std::vector<int16_t> fullbit;        // full-precision tokens [ntok][dim], grid integers
   chimera::Collab *collab = nullptr;   // pinned staging, events, host threads
   // per-stage timing
   bool timing = false;
