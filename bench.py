@@ -323,7 +323,8 @@ def main():
         tk, _ = corpus.tokens()
         fb = synth.k_to_bf16_bits(tk)
         del tk
-        idx.attach_fullbit(fb)
+        idx.attach_fullbit(fb)  # the index keeps its own grid copy
+        del fb
         runs = {}
         for c in (args.chunks, 1):
             idx.search_collab(Q, w.nprobe, w.ncand, kfb, c, w.k, nthreads=threads)  # warm-up
@@ -334,7 +335,6 @@ def main():
             log(f"  chunks {c}: {runs[c][0]:.0f} QPS, full-precision scores per query "
                 f"mean {nfull.mean():.2f} max {nfull.max()}")
         idx.attach_fullbit(None)
-        del fb
         qc, cids, nfull = runs[args.chunks]
         collab = {"qps": qc, "qps_one_chunk": runs[1][0], "kfb": kfb, "chunks": args.chunks, "host_threads": threads,
                   "k_hat_full_bit_mean": float(nfull.mean()), "k_hat_full_bit_max": int(nfull.max()),
