@@ -12,17 +12,19 @@
 // Full-precision scores are exact: query and document values are grid
 // integers (multiples of 2^-11, as the builder and the query rounding make
 // them), so a product is an integer in units of 2^-22, a 128-term dot
-// product fits int32, and the sum over query tokens is int64.
+// product fits int32, and the sum over query tokens is int64.  The document
+// tokens are read onto the grid once, when the store is attached, into an
+// int16 copy the index owns; the queries are read per search.
 #include <hip/hip_runtime.h>
 #include <immintrin.h>
 
 #include <algorithm>
-#include <cmath>
 #include <atomic>
 #include <chrono>
+#include <cmath>
+#include <condition_variable>
 #include <cstdio>
 #include <cstdlib>
-#include <condition_variable>
 #include <cstring>
 #include <functional>
 #include <mutex>
