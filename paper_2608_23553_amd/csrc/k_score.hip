@@ -149,7 +149,7 @@ struct RsWave {
   // S^T[id(row of register v)][32cb + c]; rows past the document take the
   // sentinel row
   __device__ __forceinline__ void gather(float (&st)[NCB][16], int32_t x, const RsCur &cu) const {
-    x = cu.base + idrow < cu.len ? x : sentinel;
+    x = idrow < cu.len - cu.base ? x : sentinel;  // the row count is scalar
     // byte offset of row x plus this lane's 16-lane group's first column;
     // lane l reads that of lane 16*(l/16) + V and adds its own 4 * (l%16)
     const uint32_t y = (uint32_t)x * (TQP * 4) + hcol;
@@ -304,7 +304,11 @@ __global__ __launch_bounds__(256) void k_residual_score(
       int key = 0;
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb) {
-        const float m = fmaxf(mx[cb], shfl_xor(mx[cb], 32));
+        // the two half waves hold the maxima of different rows: one
+        // permlane32 swap puts both in every lane
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx[cb]), __float_as_uint(mx[cb]), false,
+                                                         false);
+        const float m = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         if (32 * cb + c < Tq) key += to_key(m);
         mx[cb] = -INFINITY;
       }
