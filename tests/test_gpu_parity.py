@@ -432,10 +432,15 @@ def test_collab_rejects_bad_arguments():
         assert e.value.code == chimera.E_INVAL
 
 
-def test_100k_collab_search():
+def test_100k_collab_search(monkeypatch):
     w, c, k_, cl, oi, idx = setup("100k")
     idx.attach_fullbit(synth.k_to_bf16_bits(k_))
     q, src = c.queries(8, 32)
-    gi, _, gn = check_collab("100k", idx, oi, k_, q, w.nprobe, w.ncand, 100, 4, w.k)
+    gi, gs, gn = check_collab("100k", idx, oi, k_, q, w.nprobe, w.ncand, 100, 4, w.k)
     assert np.all(gi[:, 0] == src)
     say("100k collab full-precision scores per query", gn.tolist())
+    # a 16 MB scratch budget runs the 8 queries as sub-batches of 4, each
+    # writing its own rows of the host outputs
+    monkeypatch.setenv("CHIMERA_SCRATCH_MB", "16")
+    si, ss, sn = idx.search_collab(q_tensor(q, "bf16"), w.nprobe, w.ncand, 100, 4, w.k)
+    assert np.array_equal(si, gi) and np.array_equal(ss, gs) and np.array_equal(sn, gn)
