@@ -415,6 +415,16 @@ def test_tiny_collab_each_host_instruction_set(isa, monkeypatch):
     check_collab(f"tiny {isa} Tq 19", idx, oi, k_, q[:, :19], w.nprobe, w.ncand, 3 * w.k, 3, w.k)
 
 
+def test_collab_long_doc_4bit_64_query_tokens():
+    """4-bit codes and 64 query tokens: the two-column-block scorer run chunk
+    by chunk, and the host kernels' 64-token query layout."""
+    w, c, k_, cl, oi, idx = setup("2m-long", ndocs=800)
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    q, src = c.queries(4, w.Tq)
+    gi, _, _ = check_collab("2m-long recipe, 800 docs", idx, oi, k_, q, w.nprobe, 512, 300, 4, 200)
+    assert np.all(gi[:, 0] == src)
+
+
 def test_collab_rejects_bad_arguments():
     w, c, k_, cl, oi, idx = setup("tiny")
     q, _ = c.queries(2, 32)
