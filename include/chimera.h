@@ -240,7 +240,10 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
  *   nthreads host threads for the full-precision scores (0: all cores)
  * Returns when the results are written (the stream is synchronised).
  * E_INVAL without an attached store, or for k > kfb, chunks out of range;
- * other arguments as chimera_search.
+ * other arguments as chimera_search.  Environment, read at each call:
+ * CHIMERA_COLLAB_ISA caps the host instruction set (plain, avx2, vnni; the
+ * results are the same), CHIMERA_COLLAB_TRACE=1 prints the host's waiting
+ * and working time per sub-batch to stderr.
  * ===================================================================== */
 int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens, int64_t ntok);
 int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
