@@ -195,7 +195,7 @@ static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int npr
   }
   if (stop == STOP_CANDIDATES) b += align_up((size_t)(nb + 1) * 8);  // counts
   if (stop >= STOP_PRUNE)  // cand, keys, F^, n, select state
-    b += 3 * align_up((size_t)nb * ncand * 4) + align_up((size_t)nb * 4) + align_up(select_scratch_bytes(nb, idx->ndocs));
+    b += 3 * align_up((size_t)nb * ncand * 4) + align_up((size_t)nb * 4) + align_up(select_scratch_bytes(nb, idx->ndocs, ncand));
   return b;
 }
 
@@ -321,7 +321,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     int32_t *fhat = stop >= STOP_FULL ? cv.take<int32_t>((size_t)nb * ncand) : nullptr;
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
-    char *selw = cv.take<char>(select_scratch_bytes(nb, idx->ndocs));
+    char *selw = cv.take<char>(select_scratch_bytes(nb, idx->ndocs, ncand));
     if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     launch_select(fp, hist, nb, idx->ndocs, ncand, selw, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());

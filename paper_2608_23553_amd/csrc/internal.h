@@ -99,7 +99,7 @@ void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t
 // written in ascending V order; n_valid [nq].  scratch holds
 // select_scratch_bytes(nq, ndocs) bytes (no initial contents needed).
 int select_chunks(int64_t nq, int64_t ndocs);
-size_t select_scratch_bytes(int64_t nq, int64_t ndocs);
+size_t select_scratch_bytes(int64_t nq, int64_t ndocs, int ncand);
 void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, void *scratch,
                    int32_t *cand_ids, int32_t *cand_keys, int32_t *n_valid, hipStream_t s);
 // Candidate-set tap: counts [nq] of S_Q; then each S_Q in ascending order.

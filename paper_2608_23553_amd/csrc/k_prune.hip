@@ -643,36 +643,70 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_next(const uint32_t *__re
 // k_sel_hist, plus the chunk's own record: chunk_hist [256] of those keys and
 // chunk_above, the number of keys above the prefix (every hit when all are
 // kept).
+// The last histogram pass also lists, per chunk and in document order, the
+// documents whose 24-bit key prefix reaches the bin being resolved (those
+// above it and those in it), so that the write pass reads these lists
+// instead of F' again.  A list longer than cap is not kept (the write pass
+// then reads the chunk's F').
+constexpr int SEL_LAST_ITEMS = 16;  // contiguous F' entries per thread and step
+constexpr uint32_t SEL_NO_LIST = 0xFFFFFFFFu;
+
+__host__ __device__ inline int sel_list_cap(int64_t ndocs, int P, int ncand) {
+  const int64_t per = (ndocs + P - 1) / P;
+  return (int)std::min<int64_t>(per, 4 * ((int64_t)ncand / P) + 4096);
+}
+
 __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__restrict__ fp, int64_t ndocs, int P,
                                                             const SelState *__restrict__ st,
                                                             uint32_t *__restrict__ hout,
                                                             uint32_t *__restrict__ chunk_hist,
-                                                            uint32_t *__restrict__ chunk_above) {
+                                                            uint32_t *__restrict__ chunk_above, int cap,
+                                                            int2 *__restrict__ clist, uint32_t *__restrict__ clen) {
   __shared__ uint32_t h[256];
   __shared__ uint32_t s_above;
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot;
   const int64_t q = blockIdx.x / P;
   const int c = blockIdx.x % P;
-  const bool all = st[q].T == 0;  // uniform: every hit is kept
+  const bool all = st[q].T == 0;  // uniform: every hit is kept (no list: the write pass reads F')
   const uint32_t prefix = st[q].prefix;
   for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) h[i] = 0;
   if (threadIdx.x == 0) s_above = 0;
   __syncthreads();
   const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
   const int32_t *f = fp + q * ndocs;
+  int2 *L = clist + ((int64_t)q * P + c) * cap;
   uint32_t above = 0;
-  for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += SPLIT_THREADS * SEL_UNROLL) {
-    int32_t x[SEL_UNROLL];
+  long long nlist = 0;  // uniform
+  const int64_t step = (int64_t)SPLIT_THREADS * SEL_LAST_ITEMS;
+  for (int64_t vb = v0; vb < v1; vb += step) {
+    const int64_t vt = vb + (int64_t)threadIdx.x * SEL_LAST_ITEMS;
+    int32_t x[SEL_LAST_ITEMS];
 #pragma unroll
-    for (int i = 0; i < SEL_UNROLL; ++i) {
-      const int64_t v = vb + (int64_t)i * SPLIT_THREADS;
-      x[i] = v < v1 ? f[v] : NO_HIT;
-    }
+    for (int i = 0; i < SEL_LAST_ITEMS; ++i) x[i] = vt + i < v1 ? f[vt + i] : NO_HIT;
+    int flags = 0;
 #pragma unroll
-    for (int i = 0; i < SEL_UNROLL; ++i) {
+    for (int i = 0; i < SEL_LAST_ITEMS; ++i) {
       if (x[i] == NO_HIT) continue;
       const uint32_t u = fp_key(x[i]);
-      if (all || (u >> 8) > prefix) ++above;
-      else if ((u >> 8) == prefix) atomicAdd(&h[u & 255u], 1u);
+      if (all || (u >> 8) > prefix) {
+        ++above;
+        flags |= 1 << i;
+      } else if ((u >> 8) == prefix) {
+        atomicAdd(&h[u & 255u], 1u);
+        flags |= 1 << i;
+      }
+    }
+    if (!all) {
+      long long pos = block_exclusive_scan(__popc(flags), wsum, &s_tot);
+      const long long tot = s_tot;
+#pragma unroll
+      for (int i = 0; i < SEL_LAST_ITEMS; ++i)
+        if (flags & (1 << i)) {
+          if (nlist + pos < cap) L[nlist + pos] = make_int2((int)(vt + i), x[i]);
+          ++pos;
+        }
+      nlist += tot;
     }
   }
   atomicAdd(&s_above, above);
@@ -682,7 +716,10 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__res
     ch[i] = h[i];
     if (h[i]) atomicAdd(&o[i], h[i]);
   }
-  if (threadIdx.x == 0) chunk_above[(int64_t)q * P + c] = s_above;
+  if (threadIdx.x == 0) {
+    chunk_above[(int64_t)q * P + c] = s_above;
+    clen[(int64_t)q * P + c] = !all && nlist <= cap ? (uint32_t)nlist : SEL_NO_LIST;
+  }
 }
 
 // Per query: every chunk's kept (key > T) and tied (key == T) counts from its
@@ -745,10 +782,13 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_scan(int P, int ncand, Se
   }
 }
 
-// Per chunk: the ordered compaction of its kept documents.
+// Per chunk: the ordered compaction of its kept documents, from the chunk's
+// list when the last pass kept one, else from F'.
 __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__restrict__ fp, int64_t ndocs, int P,
                                                              int ncand, const SelState *__restrict__ st,
-                                                             const long long *__restrict__ counts,
+                                                             const long long *__restrict__ counts, int cap,
+                                                             const int2 *__restrict__ clist,
+                                                             const uint32_t *__restrict__ clen,
                                                              int32_t *__restrict__ out_ids,
                                                              int32_t *__restrict__ out_keys) {
   __shared__ long long wsum[SPLIT_THREADS / 64];
@@ -760,17 +800,28 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__re
   const long long *cc = counts + 3 * (q * P + c);
   if (cc[2] == 0 || cc[0] >= ncand) return;  // uniform: the chunk keeps nothing that fits
   long long written = cc[0], ties_seen = cc[1];
+  const uint32_t nl = clen[q * P + c];
+  const bool from_list = nl != SEL_NO_LIST;  // uniform
+  const int2 *L = clist + (q * P + c) * (int64_t)cap;
   const int64_t per = (ndocs + P - 1) / P, vb = c * per, ve = min(ndocs, vb + per);
+  const int64_t b0 = from_list ? 0 : vb, b1 = from_list ? (int64_t)nl : ve;
   const int32_t *f = fp + q * ndocs;
   const int64_t step = (int64_t)SPLIT_THREADS * SEL_ITEMS;
-  for (int64_t c0 = vb; c0 < ve; c0 += step) {
-    const int64_t v0 = c0 + (int64_t)threadIdx.x * SEL_ITEMS;
+  for (int64_t c0 = b0; c0 < b1; c0 += step) {
+    const int64_t j0 = c0 + (int64_t)threadIdx.x * SEL_ITEMS;
     int take_flags = 0, tie_flags = 0, ntie = 0;
-    int32_t xs[SEL_ITEMS];
+    int32_t xs[SEL_ITEMS], vs[SEL_ITEMS];
 #pragma unroll
     for (int i = 0; i < SEL_ITEMS; ++i) {
-      const int64_t v = v0 + i;
-      xs[i] = v < ve ? f[v] : NO_HIT;
+      const int64_t j = j0 + i;
+      if (from_list) {
+        const int2 e = j < b1 ? L[j] : make_int2(-1, NO_HIT);
+        vs[i] = e.x;
+        xs[i] = e.y;
+      } else {
+        vs[i] = (int32_t)j;
+        xs[i] = j < b1 ? f[j] : NO_HIT;
+      }
       if (xs[i] != NO_HIT) {
         const uint32_t u = fp_key(xs[i]);
         if (u > T) take_flags |= 1 << i;
@@ -791,7 +842,7 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__re
     for (int i = 0; i < SEL_ITEMS; ++i)
       if (take_flags & (1 << i)) {
         if (written + pos < ncand) {
-          out_ids[q * ncand + written + pos] = (int32_t)(v0 + i);
+          out_ids[q * ncand + written + pos] = vs[i];
           out_keys[q * ncand + written + pos] = xs[i];
         }
         ++pos;
@@ -807,9 +858,11 @@ int select_chunks(int64_t nq, int64_t ndocs) {
   return (int)std::max<int64_t>(1, std::min(by_q, by_docs));
 }
 
-size_t select_scratch_bytes(int64_t nq, int64_t ndocs) {
+size_t select_scratch_bytes(int64_t nq, int64_t ndocs, int ncand) {
   const int P = select_chunks(nq, ndocs);
-  return (size_t)nq * (sizeof(SelState) + (SEL_BINS + 256) * 4 + (size_t)P * (24 + 256 * 4 + 4)) + 512;
+  const size_t cap = (size_t)sel_list_cap(ndocs, P, ncand);
+  return (size_t)nq * (sizeof(SelState) + (SEL_BINS + 256) * 4 + (size_t)P * (24 + 256 * 4 + 4 + 4 + cap * 8)) +
+         512;
 }
 
 void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, void *scratch,
@@ -830,15 +883,19 @@ void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t 
   long long *counts = (long long *)(((uintptr_t)(hist3 + nq * 256) + 15) & ~(uintptr_t)15);
   uint32_t *chunk_hist = (uint32_t *)(counts + 3 * nq * P);
   uint32_t *chunk_above = chunk_hist + (size_t)nq * P * 256;
+  uint32_t *clen = chunk_above + (size_t)nq * P;
+  const int cap = sel_list_cap(ndocs, P, ncand);
+  int2 *clist = (int2 *)(((uintptr_t)(clen + (size_t)nq * P) + 15) & ~(uintptr_t)15);
   const dim3 gq((unsigned)nq), gc((unsigned)(nq * P)), tb(SPLIT_THREADS);
   hipLaunchKernelGGL(k_sel_first, gq, tb, 0, s, hist, ncand, hist2, hist3, st);
   hipLaunchKernelGGL((k_sel_hist<8, 12>), gc, tb, 0, s, fp, ndocs, P, st, hist2);
   hipLaunchKernelGGL((k_sel_next<12, false>), gq, tb, 0, s, hist2, st);
-  hipLaunchKernelGGL(k_sel_last, gc, tb, 0, s, fp, ndocs, P, st, hist3, chunk_hist, chunk_above);
+  hipLaunchKernelGGL(k_sel_last, gc, tb, 0, s, fp, ndocs, P, st, hist3, chunk_hist, chunk_above, cap, clist, clen);
   hipLaunchKernelGGL((k_sel_next<8, true>), gq, tb, 0, s, hist3, st);
   hipLaunchKernelGGL(k_sel_scan, gq, tb, 0, s, P, ncand, st, chunk_hist, chunk_above, counts, cand_ids, cand_keys,
                      n_valid);
-  hipLaunchKernelGGL(k_sel_write, gc, tb, 0, s, fp, ndocs, P, ncand, st, counts, cand_ids, cand_keys);
+  hipLaunchKernelGGL(k_sel_write, gc, tb, 0, s, fp, ndocs, P, ncand, st, counts, cap, clist, clen, cand_ids,
+                     cand_keys);
 }
 
 __global__ __launch_bounds__(256) void k_count_hits(const int32_t *__restrict__ fp, int64_t ndocs,
