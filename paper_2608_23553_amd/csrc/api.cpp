@@ -238,11 +238,16 @@ static void stage_mark(chimera_index *idx, hipStream_t s, bool on) {
 static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int Tq, int nprobe, int ncand, int k,
                Stop stop, Outs o, hipStream_t s, int refine = CHIMERA_REFINE_CENTROID) {
   const int TQP = Tq <= 32 ? 32 : 64;
-  // sub-batch size from the scratch budget
-  const size_t perq = carve_bytes(idx, 1, TQP, nprobe, ncand, stop);
-  int64_t B = std::max<int64_t>(1, (int64_t)(scratch_budget() / perq));
-  B = std::min<int64_t>(B, nq);
-  B = std::min<int64_t>(B, 65535);
+  // sub-batch size: the largest that fits the scratch budget (carve_bytes
+  // grows with nb, but not in proportion: the select's chunking depends on nb)
+  const size_t budget = scratch_budget();
+  int64_t lo = 1, hi = std::min<int64_t>(nq, 65535);
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo + 1) / 2;
+    if (carve_bytes(idx, mid, TQP, nprobe, ncand, stop) <= budget) lo = mid;
+    else hi = mid - 1;
+  }
+  int64_t B = lo;
   // equal sub-batches: the same number of passes, without a short last one
   const int64_t npass = (nq + B - 1) / B;
   B = (nq + npass - 1) / npass;

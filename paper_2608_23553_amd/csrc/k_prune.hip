@@ -653,7 +653,7 @@ constexpr uint32_t SEL_NO_LIST = 0xFFFFFFFFu;
 
 __host__ __device__ inline int sel_list_cap(int64_t ndocs, int P, int ncand) {
   const int64_t per = (ndocs + P - 1) / P;
-  return (int)std::min<int64_t>(per, 4 * ((int64_t)ncand / P) + 4096);
+  return (int)std::min<int64_t>(per, 4 * ((int64_t)ncand / P) + 1024);
 }
 
 __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__restrict__ fp, int64_t ndocs, int P,
