@@ -214,8 +214,12 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
  * value, the size of the input), so the caller may free its array after
  * the call; tokens == NULL drops the copy.  With the builder's own input
  * the full-precision scores are the exact Chamfer scores of the indexed
- * tokens.  E_INVAL if ntok differs from the index's token count, E_NOMEM if
- * the copy cannot be allocated, E_BUSY during another call on the index.
+ * tokens.  Every value must be finite and within [-8, 8]: with query tokens
+ * of L2 norm <= 2 that keeps each full-precision dot product exact in 32-bit
+ * integers.  E_INVAL if ntok differs from the index's token count or a
+ * value breaks that bound (the message names the first such token; the
+ * previous copy, if any, is kept), E_NOMEM if the copy cannot be allocated,
+ * E_BUSY during another call on the index.
  *
  * chimera_search_collab: steps 1-3 of chimera_search, then Alg. 3 over each
  * query's kept candidates S_refine, taken in ascending document id:

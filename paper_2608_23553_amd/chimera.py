@@ -262,8 +262,9 @@ class Index:
             _check(lib().chimera_fullbit_attach(self._h, None, 0))
             return
         a = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
-        if a.ndim != 2:
-            raise ValueError("tokens must be [ntok, d]")
+        dim = self._info["dim"]
+        if a.ndim != 2 or a.shape[1] != dim:
+            raise ValueError(f"tokens must be [ntok, {dim}], got {list(a.shape)}")
         _check(lib().chimera_fullbit_attach(self._h, _np(a), a.shape[0]))
 
     def search_collab(self, Q, nprobe: int, ncand: int, kfb: int, chunks: int, k: int, nthreads: int = 0,

@@ -167,9 +167,9 @@ static int grow_pinned(T *&p, size_t &cap, size_t n) {
 // F(V) = sum_j max_t <Q_j, v_t> in units of 2^-22 (Def. 1 on the
 // full-precision tokens).  A bf16 value v reads as the grid integer
 // nearbyint(2048 v), which is what the builder makes of it (an integer
-// already when |v| >= 2^-4).  Grid integers are at most 2^11 in magnitude
-// (|value| <= 1), so a product is below 2^22 and a 128-term dot product below
-// 2^29 (int32); the sum over query tokens is int64.
+// already when |v| >= 2^-4).  Query values are at most 2 in magnitude (L2
+// norm <= 2) and attached document values at most 8 (grid_in_range), so
+// every partial dot product fits int32; the sum over query tokens is int64.
 //
 // The query is kept pair-interleaved and token-minor, qp[p][j][2] = (Q_j[2p],
 // Q_j[2p+1]) with j padded to a multiple of 16, so that one multiply-add
@@ -187,6 +187,17 @@ static inline __attribute__((always_inline)) void to_grid(const uint16_t *src, i
     const float k = std::nearbyint(v * 2048.0f);
     dst[i] = (int16_t)(int32_t)std::fmin(std::fmax(k, -32768.0f), 32767.0f);
   }
+}
+
+// Attached document values are held to |v| <= 8 (grid integers within
+// +-2^14).  With a query token of L2 norm <= 2, every partial sum of a dot
+// product is then at most 2 * 8 * sqrt(128) < 182 in magnitude, below 2^31
+// in units of 2^-22.  NaN and infinities convert to -2^15 or 2^15 - 1 and
+// fail the test too.
+static bool grid_in_range(const int16_t *g, int64_t n) {
+  int bad = 0;
+  for (int64_t i = 0; i < n; ++i) bad |= (g[i] > 16384) | (g[i] < -16384);
+  return !bad;
 }
 
 // best[j] = max over the L tokens of v of <qp_j, v_t>, for j < TqP
@@ -464,19 +475,38 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
   }
   int rc = CHIMERA_OK;
   try {
-    // read every value onto the grid once, here, in parallel slices
+    // read every value onto the grid once, here, in parallel slices of
+    // whole tokens, and find the first token out of range
     std::vector<int16_t> store((size_t)ntok * CHIMERA_DIM);
     const HostKernels K = pick_kernels();
-    const int64_t n = ntok * CHIMERA_DIM;
     const unsigned nt = std::max(1u, std::min(32u, std::thread::hardware_concurrency()));
+    std::atomic<int64_t> first_bad{ntok};
     std::vector<std::thread> th;
     for (unsigned w = 0; w < nt; ++w)
       th.emplace_back([&, w] {
-        const int64_t b = n * w / nt, e = n * (w + 1) / nt;
-        K.to_grid(tokens + b, e - b, store.data() + b);
+        const int64_t b = ntok * w / nt, e = ntok * (w + 1) / nt;
+        constexpr int64_t kBlock = 64;  // tokens converted, then checked while cached
+        for (int64_t t = b; t < e; t += kBlock) {
+          const int64_t n = std::min(kBlock, e - t);
+          int16_t *g = store.data() + t * CHIMERA_DIM;
+          K.to_grid(tokens + t * CHIMERA_DIM, n * CHIMERA_DIM, g);
+          if (grid_in_range(g, n * CHIMERA_DIM)) continue;
+          for (int64_t u = 0; u < n; ++u)
+            if (!grid_in_range(g + u * CHIMERA_DIM, CHIMERA_DIM)) {
+              int64_t cur = first_bad.load();
+              while (t + u < cur && !first_bad.compare_exchange_weak(cur, t + u)) {
+              }
+              break;
+            }
+          return;
+        }
       });
     for (auto &t : th) t.join();
-    idx->fullbit.swap(store);
+    if (first_bad.load() < ntok)
+      rc = fail(CHIMERA_E_INVAL, "full-precision token %lld has a value that is not finite or outside [-8, 8]",
+                (long long)first_bad.load());
+    else
+      idx->fullbit.swap(store);
   } catch (const std::bad_alloc &) {
     rc = fail(CHIMERA_E_NOMEM, "full-precision store of %lld tokens", (long long)ntok);
   } catch (...) {

@@ -442,6 +442,29 @@ def test_collab_rejects_bad_arguments():
         assert e.value.code == chimera.E_INVAL
 
 
+def test_collab_store_out_of_range_is_refused():
+    """A store value that is not finite or lies outside [-8, 8] could overflow
+    the host's 32-bit dot products: attach refuses it, names the first such
+    token and keeps the copy it had; a wrong width is refused before the
+    library reads the array."""
+    w, c, k_, cl, oi, idx = setup("tiny")
+    good = synth.k_to_bf16_bits(k_)
+    idx.attach_fullbit(good)
+    q, _ = c.queries(3, 32)
+    before = check_collab("tiny before", idx, oi, k_, q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    for bad in [9.0, -8.0625, float("inf"), float("nan")]:
+        b = good.copy()
+        b[[123, 4567], 7] = np.array([bad], np.float32).view(np.uint32)[0] >> 16
+        with pytest.raises(ChimeraError) as e:
+            idx.attach_fullbit(b)
+        assert e.value.code == chimera.E_INVAL and "token 123 " in str(e.value)
+    with pytest.raises(ValueError):
+        idx.attach_fullbit(good[:, :64])
+    after = idx.search_collab(q_tensor(q, "bf16"), w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    for x, y in zip(before, after):
+        assert np.array_equal(x, y)
+
+
 def test_100k_collab_search(monkeypatch):
     w, c, k_, cl, oi, idx = setup("100k")
     idx.attach_fullbit(synth.k_to_bf16_bits(k_))
