@@ -439,7 +439,6 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
                           float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream) {
   int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
   if (rc) return rc;
-  if (idx->fullbit.empty()) return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
   if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
   if (kfb < k) return fail(CHIMERA_E_INVAL, "kfb (%d) must be >= k (%d)", kfb, k);
   if (ncand < 1) return fail(CHIMERA_E_INVAL, "ncand must be >= 1");
@@ -450,6 +449,8 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
   if (nq == 0) return CHIMERA_OK;
   BusyGuard bg(idx);
   if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  // read under the guard: attach swaps the store while it holds it
+  if (idx->fullbit.empty()) return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
   DeviceGuard dg(idx->device);
   if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
   int nc = (int)std::min<int64_t>(ncand, idx->ndocs);
