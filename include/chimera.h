@@ -117,7 +117,9 @@ const char *chimera_last_error(void);
  * 128; nbits 2 or 4; ncent >= 1.  *out receives the builder. */
 int chimera_builder_create(const uint16_t *centroids_bf16, int32_t ncent, int32_t dim, int32_t nbits,
                            chimera_builder **out);
-/* Pass 1: tokens_bf16 host [ntok][dim], cids host [ntok] in [0, ncent). */
+/* Pass 1: tokens_bf16 host [ntok][dim], cids host [ntok] in [0, ncent).
+ * Token and centroid components must lie in [-1, 1] (unit vectors satisfy
+ * it), else E_INVAL. */
 int chimera_builder_add_residuals(chimera_builder *b, const uint16_t *tokens_bf16, const int32_t *cids,
                                   int64_t ntok);
 /* Ends pass 1: fixes cutoffs and bucket weights.  E_INVAL if no residual. */
@@ -214,9 +216,9 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
  * value, the size of the input), so the caller may free its array after
  * the call; tokens == NULL drops the copy.  With the builder's own input
  * the full-precision scores are the exact Chamfer scores of the indexed
- * tokens.  Every value must be finite and within [-8, 8]: with query tokens
- * of L2 norm <= 2 that keeps each full-precision dot product exact in 32-bit
- * integers.  E_INVAL if ntok differs from the index's token count or a
+ * tokens.  Every value must lie in [-1, 1], as for the builder: with query
+ * tokens of L2 norm <= 2 that keeps each full-precision dot product exact in
+ * 32-bit integers.  E_INVAL if ntok differs from the index's token count or a
  * value breaks that bound (the message names the first such token; the
  * previous copy, if any, is kept), E_NOMEM if the copy cannot be allocated,
  * E_BUSY during another call on the index.

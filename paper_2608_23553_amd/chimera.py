@@ -119,9 +119,20 @@ class Builder:
             _lib.chimera_builder_free(self._h)
             self._h = None
 
+    def _rows(self, t: np.ndarray, c: np.ndarray, n: int):
+        """The library reads n rows of tokens and cids: check the arrays
+        hold exactly that many."""
+        if c.shape != (n,):
+            raise ValueError(f"cids must be [{n}], got {list(c.shape)}")
+        if t.shape != (n, self.dim):
+            raise ValueError(f"tokens must be [{n}, {self.dim}], got {list(t.shape)}")
+
     def add_residuals(self, tokens_bf16: np.ndarray, cids: np.ndarray):
         t = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
         c = np.ascontiguousarray(cids, dtype=np.int32)
+        if c.ndim != 1:
+            raise ValueError(f"cids must be [ntok], got {list(c.shape)}")
+        self._rows(t, c, c.shape[0])
         _check(lib().chimera_builder_add_residuals(self._h, _np(t), _np(c), c.shape[0]))
 
     def freeze(self):
@@ -131,6 +142,9 @@ class Builder:
         t = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
         c = np.ascontiguousarray(cids, dtype=np.int32)
         l = np.ascontiguousarray(doc_lens, dtype=np.int32)
+        if l.ndim != 1:
+            raise ValueError("doc_lens must be [ndocs]")
+        self._rows(t, c, int(l.astype(np.int64).sum()))
         _check(lib().chimera_builder_add_docs(self._h, _np(t), _np(c), _np(l), l.shape[0]))
 
     def quantizer(self) -> Tuple[np.ndarray, np.ndarray]:

@@ -168,7 +168,7 @@ static int grow_pinned(T *&p, size_t &cap, size_t n) {
 // full-precision tokens).  A bf16 value v reads as the grid integer
 // nearbyint(2048 v), which is what the builder makes of it (an integer
 // already when |v| >= 2^-4).  Query values are at most 2 in magnitude (L2
-// norm <= 2) and attached document values at most 8 (grid_in_range), so
+// norm <= 2) and attached document values at most 1 (grid_in_range), so
 // every partial dot product fits int32; the sum over query tokens is int64.
 //
 // The query is kept pair-interleaved and token-minor, qp[p][j][2] = (Q_j[2p],
@@ -189,14 +189,14 @@ static inline __attribute__((always_inline)) void to_grid(const uint16_t *src, i
   }
 }
 
-// Attached document values are held to |v| <= 8 (grid integers within
-// +-2^14).  With a query token of L2 norm <= 2, every partial sum of a dot
-// product is then at most 2 * 8 * sqrt(128) < 182 in magnitude, below 2^31
-// in units of 2^-22.  NaN and infinities convert to -2^15 or 2^15 - 1 and
-// fail the test too.
+// Attached document values lie in [-1, 1], as the builder requires of the
+// tokens it indexes (grid integers within +-2^11).  With a query token of L2
+// norm <= 2, every partial sum of a dot product is then at most
+// 2 * sqrt(128) < 23 in magnitude, far below 2^31 in units of 2^-22.  NaN and
+// infinities convert to -2^15 or 2^15 - 1 and fail the test too.
 static bool grid_in_range(const int16_t *g, int64_t n) {
   int bad = 0;
-  for (int64_t i = 0; i < n; ++i) bad |= (g[i] > 16384) | (g[i] < -16384);
+  for (int64_t i = 0; i < n; ++i) bad |= (g[i] > 2048) | (g[i] < -2048);
   return !bad;
 }
 
@@ -503,7 +503,7 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
       });
     for (auto &t : th) t.join();
     if (first_bad.load() < ntok)
-      rc = fail(CHIMERA_E_INVAL, "full-precision token %lld has a value that is not finite or outside [-8, 8]",
+      rc = fail(CHIMERA_E_INVAL, "full-precision token %lld has a value that is not finite or outside [-1, 1]",
                 (long long)first_bad.load());
     else
       idx->fullbit.swap(store);

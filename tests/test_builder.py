@@ -52,6 +52,25 @@ def test_builder_rejects_bad_input():
         b.add_residuals(big, np.zeros(1, np.int32))
 
 
+def test_builder_binding_checks_row_counts():
+    """The library reads as many rows as cids (pass 1) or sum(doc_lens) (pass
+    2) says: the binding refuses arrays of another shape before the call."""
+    b = Builder(np.zeros((4, 128), np.uint16), 2)
+    tok = np.zeros((6, 128), np.uint16)
+    for t, c in [(tok[:5], np.zeros(6, np.int32)), (tok[:, :64], np.zeros(6, np.int32)),
+                 (tok, np.zeros((6, 1), np.int32))]:
+        with pytest.raises(ValueError):
+            b.add_residuals(t, c)
+    b.add_residuals(tok, np.zeros(6, np.int32))
+    b.freeze()
+    for t, c, lens in [(tok, np.zeros(6, np.int32), [2, 3]), (tok, np.zeros(5, np.int32), [2, 4]),
+                       (tok[:5], np.zeros(6, np.int32), [2, 4]), (tok, np.zeros(6, np.int32), [[2, 4]])]:
+        with pytest.raises(ValueError):
+            b.add_docs(t, c, np.array(lens, np.int32))
+    b.add_docs(tok, np.zeros(6, np.int32), np.array([2, 4], np.int32))
+    assert b.info()["ndocs"] == 2 and b.info()["ntokens"] == 6
+
+
 def _read_header(path):
     raw = open(path, "rb").read()
     magic, ver, hb, dim, nbits, ncent, maxlen, ndocs, ntok, nnz, nsec = struct.unpack_from("<8sIIiiiiqqqI", raw, 0)

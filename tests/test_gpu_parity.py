@@ -443,16 +443,16 @@ def test_collab_rejects_bad_arguments():
 
 
 def test_collab_store_out_of_range_is_refused():
-    """A store value that is not finite or lies outside [-8, 8] could overflow
-    the host's 32-bit dot products: attach refuses it, names the first such
-    token and keeps the copy it had; a wrong width is refused before the
-    library reads the array."""
+    """A store value that is not finite or lies outside [-1, 1] (the
+    builder's rule, which bounds the host's 32-bit dot products) is refused:
+    attach names the first such token and keeps the copy it had; a wrong
+    width is refused before the library reads the array."""
     w, c, k_, cl, oi, idx = setup("tiny")
     good = synth.k_to_bf16_bits(k_)
     idx.attach_fullbit(good)
     q, _ = c.queries(3, 32)
     before = check_collab("tiny before", idx, oi, k_, q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
-    for bad in [9.0, -8.0625, float("inf"), float("nan")]:
+    for bad in [1.0078125, -2.0, float("inf"), float("nan")]:
         b = good.copy()
         b[[123, 4567], 7] = np.array([bad], np.float32).view(np.uint32)[0] >> 16
         with pytest.raises(ChimeraError) as e:
