@@ -241,6 +241,14 @@ class Index:
         _check(lib().chimera_index_info_get(self._h, ctypes.byref(st)))
         return _info(st)
 
+    def _q(self, Q):
+        """Q as the library takes it, on the index's own GPU (the library
+        receives a bare device pointer and cannot check that)."""
+        Q, dt = _q_args(Q)
+        if Q.device.index != self._info["device"]:
+            raise ValueError(f"Q is on {Q.device}, the index on cuda:{self._info['device']}")
+        return Q, dt
+
     @property
     def device(self):
         import torch
@@ -251,13 +259,16 @@ class Index:
         refine: REFINE_CENTROID (chimera_search) or REFINE_TOKEN
         (chimera_search_refine)."""
         import torch
-        Q, dt = _q_args(Q)
+        Q, dt = self._q(Q)
         nq, Tq, d = Q.shape
         if out is None:
             ids = torch.empty((nq, k), dtype=torch.int32, device=Q.device)
             scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
         else:
             ids, scores = out
+            for t, dtype, name in ((ids, torch.int32, "ids"), (scores, torch.float32, "scores")):
+                if tuple(t.shape) != (nq, k) or t.dtype != dtype or t.device != Q.device or not t.is_contiguous():
+                    raise ValueError(f"out {name} must be a contiguous {dtype} tensor [{nq}, {k}] on {Q.device}")
         if refine == REFINE_CENTROID:
             _check(lib().chimera_search(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, k,
                                         ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(scores.data_ptr()),
@@ -285,7 +296,7 @@ class Index:
                       stream=None):
         """CPU-GPU collaborative scoring (chimera_search_collab): host numpy
         (ids int32 [nq,k], scores float32 [nq,k], n_full int32 [nq])."""
-        Q, dt = _q_args(Q)
+        Q, dt = self._q(Q)
         nq, Tq, d = Q.shape
         ids = np.empty((nq, k), dtype=np.int32)
         scores = np.empty((nq, k), dtype=np.float32)
@@ -303,7 +314,7 @@ class Index:
 
     def probe(self, Q, nprobe: int, stream=None):
         import torch
-        Q, dt = _q_args(Q)
+        Q, dt = self._q(Q)
         nq, Tq, d = Q.shape
         ids = torch.empty((nq, Tq, nprobe), dtype=torch.int32, device=Q.device)
         keys = torch.empty((nq, Tq, nprobe), dtype=torch.int32, device=Q.device)
@@ -314,7 +325,7 @@ class Index:
 
     def candidates(self, Q, nprobe: int, capacity: int | None = None, stream=None):
         import torch
-        Q, dt = _q_args(Q)
+        Q, dt = self._q(Q)
         nq, Tq, d = Q.shape
         if capacity is None:
             capacity = nq * self._info["ndocs"]
@@ -327,7 +338,7 @@ class Index:
 
     def prune(self, Q, nprobe: int, ncand: int, stream=None, refine: int = REFINE_CENTROID):
         import torch
-        Q, dt = _q_args(Q)
+        Q, dt = self._q(Q)
         nq, Tq, d = Q.shape
         nc = min(ncand, self._info["ndocs"])
         cand = torch.empty((nq, nc), dtype=torch.int32, device=Q.device)

@@ -337,6 +337,34 @@ def test_zipf_small_hot_lists(refine):
 
 
 # ------------------------------------------------------ degenerate queries
+def test_binding_checks_out_tensors():
+    """Caller-supplied outputs are written by the kernels through bare
+    pointers: the binding refuses a wrong shape, dtype, device or layout, and
+    a correct pair gives the same answer as the binding's own outputs."""
+    w, c, k_, cl, oi, idx = setup("tiny")
+    q, _ = c.queries(3, 32)
+    Q = q_tensor(q, "bf16")
+    nq, k = 3, w.k
+    dev = Q.device
+    good_i = torch.empty((nq, k), dtype=torch.int32, device=dev)
+    good_s = torch.empty((nq, k), dtype=torch.float32, device=dev)
+    bad = [(torch.empty((nq, k - 1), dtype=torch.int32, device=dev), good_s),
+           (good_i, torch.empty((nq + 1, k), dtype=torch.float32, device=dev)),
+           (torch.empty((nq, k), dtype=torch.int64, device=dev), good_s),
+           (good_i, torch.empty((nq, k), dtype=torch.bfloat16, device=dev)),
+           (torch.empty((nq, k), dtype=torch.int32), good_s),
+           (torch.empty((k, nq), dtype=torch.int32, device=dev).t(), good_s)]
+    for o in bad:
+        with pytest.raises(ValueError):
+            idx.search(Q, w.nprobe, w.ncand, k, out=o)
+    with pytest.raises(ValueError):
+        idx.search(Q.cpu(), w.nprobe, w.ncand, k)
+    ri, rs = idx.search(Q, w.nprobe, w.ncand, k)
+    idx.search(Q, w.nprobe, w.ncand, k, out=(good_i, good_s))
+    torch.cuda.synchronize()
+    assert torch.equal(ri, good_i) and torch.equal(rs, good_s)
+
+
 @pytest.mark.parametrize("refine", [False, True])
 def test_tiny_zero_queries_break_every_tie_by_lowest_id(refine):
     """All-zero queries: every centroid and document score is 0, so the
