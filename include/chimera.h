@@ -245,8 +245,11 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
  *            kfb (Sec. 4)
  *   nthreads host threads for the full-precision scores (0: all cores)
  * Returns when the results are written (the stream is synchronised).
- * E_INVAL without an attached store (when nq > 0), or for k > kfb, chunks
- * out of range;
+ * E_INVAL without an attached store (when nq > 0), for k > kfb, chunks
+ * out of range, or a query component that is not finite or lies outside
+ * [-2, 2] (implied by the L2 norm <= 2 that exact scores assume; the host's
+ * 32-bit sums rely on it; found after the GPU has run, the stream is
+ * synchronised first and the outputs are undefined);
  * other arguments as chimera_search.  Environment, read at each call:
  * CHIMERA_COLLAB_ISA caps the host instruction set (plain, avx2, vnni; the
  * results are the same), CHIMERA_COLLAB_TRACE=1 prints the host's waiting

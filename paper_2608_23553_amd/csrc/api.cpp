@@ -256,6 +256,16 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
   int rc = ensure_scratch(idx, need);
   if (rc) return rc;
   if (idx->scratch_pending) CHIMERA_HIP(hipStreamWaitEvent(s, idx->scratch_done, 0));
+  // Every exit from here on, error returns included, marks the scratch as in
+  // use by the work queued on s, so a later call on another stream waits for
+  // that work before it reuses the scratch.
+  struct ScratchDone {
+    chimera_index *idx;
+    hipStream_t s;
+    ~ScratchDone() {
+      if (hipEventRecord(idx->scratch_done, s) == hipSuccess) idx->scratch_pending = true;
+    }
+  } scratch_done_on_exit{idx, s};
   const bool mark = stop == STOP_FULL;
 
   std::vector<int64_t> host_counts;
@@ -344,8 +354,6 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     stage_mark(idx, s, mark);
     CHIMERA_HIP(hipGetLastError());
   }
-  CHIMERA_HIP(hipEventRecord(idx->scratch_done, s));
-  idx->scratch_pending = true;
   if (stop == STOP_CANDIDATES) {
     std::vector<int64_t> offs(nq + 1, 0);
     for (int64_t i = 0; i < nq; ++i) offs[i + 1] = offs[i] + host_counts[i];

@@ -194,10 +194,23 @@ static inline __attribute__((always_inline)) void to_grid(const uint16_t *src, i
 // norm <= 2, every partial sum of a dot product is then at most
 // 2 * sqrt(128) < 23 in magnitude, far below 2^31 in units of 2^-22.  NaN and
 // infinities convert to -2^15 or 2^15 - 1 and fail the test too.
-static bool grid_in_range(const int16_t *g, int64_t n) {
+static bool grid_within(const int16_t *g, int64_t n, int lim) {
   int bad = 0;
-  for (int64_t i = 0; i < n; ++i) bad |= (g[i] > 2048) | (g[i] < -2048);
+  for (int64_t i = 0; i < n; ++i) bad |= (g[i] > lim) | (g[i] < -lim);
   return !bad;
+}
+static bool grid_in_range(const int16_t *g, int64_t n) { return grid_within(g, n, 2048); }
+// Queries are held to components in [-2, 2] (implied by L2 norm <= 2): with
+// document values in [-1, 1] a dot product is then below 128 * 2^12 * 2^11 =
+// 2^30 in magnitude whatever the norm, so no input overflows the host's
+// 32-bit sums.
+static bool query_in_range(const int16_t *g, int64_t n) { return grid_within(g, n, 4096); }
+
+// a = min(a, v), from several threads
+static void atomic_min(std::atomic<int64_t> &a, int64_t v) {
+  int64_t cur = a.load();
+  while (v < cur && !a.compare_exchange_weak(cur, v)) {
+  }
 }
 
 // best[j] = max over the L tokens of v of <qp_j, v_t>, for j < TqP
@@ -390,6 +403,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
   C.full.resize(nb);
   const int TqP = (Tq + kQBlock - 1) / kQBlock * kQBlock;
   C.qk.assign((size_t)nb * TqP * dim, 0);
+  std::atomic<int64_t> bad_query{INT64_MAX};
   if (!C.pool->run(nb, [&](int64_t q) {
     C.ranked[q].clear();
     C.done[q].assign(ncand, 0);
@@ -399,9 +413,15 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
     for (int j = 0; j < Tq; ++j) {
       K.to_grid(C.h_qs + ((size_t)q * TQP + j) * dim, dim, row);
       for (int d = 0; d < dim; ++d) qp[((size_t)(d >> 1) * TqP + j) * 2 + (d & 1)] = row[d];
+      if (!query_in_range(row, dim)) atomic_min(bad_query, q0 + q);
     }
   }))
     return host_failed(s);
+  if (bad_query.load() != INT64_MAX) {
+    (void)hipStreamSynchronize(s);  // the chunk copies still target the pinned buffers
+    return fail(CHIMERA_E_INVAL, "query %lld has a component that is not finite or outside [-2, 2]",
+                (long long)bad_query.load());
+  }
   const int16_t *tok = idx->fullbit.data();
   const int64_t *doc_off = idx->h_doc_off.data();
   lap(t_work);
@@ -493,9 +513,7 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
           if (grid_in_range(g, n * CHIMERA_DIM)) continue;
           for (int64_t u = 0; u < n; ++u)
             if (!grid_in_range(g + u * CHIMERA_DIM, CHIMERA_DIM)) {
-              int64_t cur = first_bad.load();
-              while (t + u < cur && !first_bad.compare_exchange_weak(cur, t + u)) {
-              }
+              atomic_min(first_bad, t + u);
               break;
             }
           return;

@@ -493,6 +493,26 @@ def test_collab_store_out_of_range_is_refused():
         assert np.array_equal(x, y)
 
 
+def test_collab_query_out_of_range_is_refused():
+    """A query component outside [-2, 2] (no query token of L2 norm <= 2 has
+    one) is refused with the lowest such query named; a component of exactly
+    2 is taken and scored exactly; the index keeps working after the error."""
+    w, c, k_, cl, oi, idx = setup("tiny")
+    idx.attach_fullbit(synth.k_to_bf16_bits(k_))
+    q, _ = c.queries(4, 32)
+    bad = q.copy()
+    bad[1, 5, 7] = 3 * 2048
+    bad[3, 0, 0] = -3 * 2048
+    with pytest.raises(ChimeraError) as e:
+        idx.search_collab(q_tensor(bad, "bf16"), w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    assert e.value.code == chimera.E_INVAL and "query 1 " in str(e.value)
+    edge = q.copy()
+    edge[2, 3] = 0
+    edge[2, 3, 9] = 2 * 2048  # a token of norm exactly 2
+    check_collab("tiny component 2", idx, oi, k_, edge, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    check_collab("tiny after the error", idx, oi, k_, q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+
+
 def test_100k_collab_search(monkeypatch):
     w, c, k_, cl, oi, idx = setup("100k")
     idx.attach_fullbit(synth.k_to_bf16_bits(k_))
