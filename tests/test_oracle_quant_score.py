@@ -135,8 +135,14 @@ def test_search_composes_stage_definitions():
 
 
 def test_key_to_score_single_rounding():
+    """The score is the key's value rounded once to fp32.  The comparison is
+    made in float64 against that fp32 value: a Python float compared with an
+    np.float32 is first cast to fp32, which would let an unrounded result
+    pass."""
     for key in (0, 1, -1, 2**24 + 1, 2**27 + 3, -(2**26) - 5, 123456789):
-        assert oracle.key_to_score(key) == np.float32(key) * np.float32(2.0 ** -22)
+        want = float(np.float32(key) * np.float32(2.0 ** -22))
+        assert oracle.key_to_score(key) == want
+    assert oracle.key_to_score(2**24 + 1) == 4.0  # 2^24 + 1 is not an fp32 value
 
 
 def test_synthetic_clusters_are_nearest_centroid():
