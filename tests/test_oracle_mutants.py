@@ -17,11 +17,13 @@ import test_oracle_collab as PC
 import test_oracle_grid_probe as PG
 import test_oracle_prune as PP
 import test_oracle_quant_score as PQ
+import test_oracle_refine as PR
 from util_corpus import corpus, oracle_index
 
 REAL = {name: getattr(oracle, name) for name in (
     "grid_k", "grid_f32", "centroid_scores", "probe", "candidates", "partial_scores", "topk", "encode",
-    "quantizer", "pack", "doc_scores", "exact_chamfer", "key_to_score", "collaborative_scoring", "ivf_docs")}
+    "quantizer", "pack", "doc_scores", "exact_chamfer", "key_to_score", "collaborative_scoring", "ivf_docs",
+    "partial_scores_res", "ivf_tokens", "token_docs")}
 
 
 # ----------------------------------------------------------------- grid
@@ -179,6 +181,41 @@ def ivf_one_entry_per_token(cid, doc_off, ncent):
     return off, oracle.token_docs(doc_off)[tok]
 
 
+# ------------------------------------------ refinement from token scores
+def pres_no_residual(S, ci, q, w, off, tok, tdoc, codes, ndocs):
+    return REAL["partial_scores_res"](S, ci, q, np.zeros_like(w), off, tok, tdoc, codes, ndocs)
+
+
+def pres_residual_negated(S, ci, q, w, off, tok, tdoc, codes, ndocs):
+    return REAL["partial_scores_res"](S, ci, q, -np.asarray(w), off, tok, tdoc, codes, ndocs)
+
+
+def pres_no_centroid_term(S, ci, q, w, off, tok, tdoc, codes, ndocs):
+    return REAL["partial_scores_res"](np.zeros_like(S), ci, q, w, off, tok, tdoc, codes, ndocs)
+
+
+def pres_first_probe_only(S, ci, q, w, off, tok, tdoc, codes, ndocs):
+    return REAL["partial_scores_res"](S, np.ascontiguousarray(ci[:, :1]), q, w, off, tok, tdoc, codes, ndocs)
+
+
+def pres_token_to_next_doc(S, ci, q, w, off, tok, tdoc, codes, ndocs):
+    return REAL["partial_scores_res"](S, ci, q, w, off, tok, np.minimum(np.asarray(tdoc) + 1, ndocs - 1), codes,
+                                      ndocs)
+
+
+def ivf_tokens_descending(cid, ncent):
+    off, tok = REAL["ivf_tokens"](cid, ncent)
+    tok = tok.copy()
+    for c in range(ncent):
+        tok[off[c]:off[c + 1]] = tok[off[c]:off[c + 1]][::-1]
+    return off, tok
+
+
+def token_docs_off_by_one(doc_off):
+    doc_off = np.asarray(doc_off, np.int64)
+    return np.repeat(np.arange(1, doc_off.shape[0], dtype=np.int32), np.diff(doc_off))
+
+
 MUTANTS = [
     ("grid_k", grid_k_ties_away, [PG.test_grid_examples_and_ties]),
     ("grid_k", grid_k_truncates, [PG.test_grid_examples_and_ties]),
@@ -212,6 +249,14 @@ MUTANTS = [
     ("collaborative_scoring", collab_ranks_by_exact, [lambda: PC.test_one_chunk_is_the_non_concurrent_strategy(True)]),
     ("collaborative_scoring", collab_returns_approx, [lambda: PC.test_one_chunk_is_the_non_concurrent_strategy(True)]),
     ("ivf_docs", ivf_one_entry_per_token, [PP.test_ivf_lists_match_sets]),
+    ("partial_scores_res", pres_no_residual, [PR.test_refined_fprime_matches_definition]),
+    ("partial_scores_res", pres_residual_negated, [PR.test_refined_fprime_matches_definition]),
+    ("partial_scores_res", pres_no_centroid_term, [PR.test_refined_fprime_matches_definition,
+                                                   PR.test_refined_fprime_negative_maximum_is_kept]),
+    ("partial_scores_res", pres_first_probe_only, [PR.test_refined_fprime_matches_definition]),
+    ("partial_scores_res", pres_token_to_next_doc, [PR.test_refined_fprime_matches_definition]),
+    ("ivf_tokens", ivf_tokens_descending, [PR.test_token_lists_match_sets]),
+    ("token_docs", token_docs_off_by_one, [PR.test_token_docs]),
 ]
 
 
