@@ -38,6 +38,19 @@ def test_grid_matches_library_bf16_rounding():
     assert np.array_equal(bits, k.astype(np.int16))
 
 
+def test_grid_bf16_rounds_off_grid_values():
+    """bf16 inputs below 2^-4 in magnitude lie between grid points: each reads
+    as the nearest multiple of 2^-11, ties to even (numpy's rint on the exact
+    value); from 2^-4 up every bf16 value is on the grid already."""
+    rng = np.random.default_rng(20)
+    x = np.concatenate([rng.standard_normal(100_000) * 0.02, rng.standard_normal(20_000) * 0.3,
+                        (np.arange(-64, 65) + 0.5) / 2048]).astype(np.float32)
+    bits = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    v = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert np.any(v * 2048 != np.rint(v * 2048))  # off-grid inputs are present
+    assert np.array_equal(oracle.grid_bf16(bits).astype(np.float64), np.rint(v * 2048))
+
+
 def test_centroid_scores_exact_against_fp64_matmul():
     rng = np.random.default_rng(1)
     cent = rand_grid(rng, (300, 128))

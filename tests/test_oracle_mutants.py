@@ -23,7 +23,7 @@ from util_corpus import corpus, oracle_index
 REAL = {name: getattr(oracle, name) for name in (
     "grid_k", "grid_f32", "centroid_scores", "probe", "candidates", "partial_scores", "topk", "encode",
     "quantizer", "pack", "doc_scores", "exact_chamfer", "key_to_score", "collaborative_scoring", "ivf_docs",
-    "partial_scores_res", "ivf_tokens", "token_docs")}
+    "partial_scores_res", "ivf_tokens", "token_docs", "grid_bf16", "assign", "residual_hist", "unpack")}
 
 
 # ----------------------------------------------------------------- grid
@@ -216,6 +216,32 @@ def token_docs_off_by_one(doc_off):
     return np.repeat(np.arange(1, doc_off.shape[0], dtype=np.int32), np.diff(doc_off))
 
 
+# -------------------------------------------------- reading and building
+def grid_bf16_floor(bits):
+    """Off-grid bf16 values floored to the grid instead of rounded."""
+    v = (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.floor(v * 2048).astype(np.int16)
+
+
+def assign_farthest(tok, cent, nthreads=0):
+    return REAL["assign"](tok, -np.asarray(cent, np.int16), nthreads)
+
+
+def residual_hist_negated(tok, cid, cent, hist=None):
+    """Residuals taken as centroid minus token."""
+    h = REAL["residual_hist"](tok, cid, cent)[::-1].copy()
+    if hist is not None:
+        hist += h
+        return hist
+    return h
+
+
+def unpack_reversed_in_byte(packed, dim, nbits):
+    c = REAL["unpack"](packed, dim, nbits)
+    per = 8 // nbits
+    return np.ascontiguousarray(c.reshape(c.shape[0], -1, per)[:, :, ::-1].reshape(c.shape))
+
+
 MUTANTS = [
     ("grid_k", grid_k_ties_away, [PG.test_grid_examples_and_ties]),
     ("grid_k", grid_k_truncates, [PG.test_grid_examples_and_ties]),
@@ -257,6 +283,10 @@ MUTANTS = [
     ("partial_scores_res", pres_token_to_next_doc, [PR.test_refined_fprime_matches_definition]),
     ("ivf_tokens", ivf_tokens_descending, [PR.test_token_lists_match_sets]),
     ("token_docs", token_docs_off_by_one, [PR.test_token_docs]),
+    ("grid_bf16", grid_bf16_floor, [PG.test_grid_bf16_rounds_off_grid_values]),
+    ("assign", assign_farthest, [PQ.test_synthetic_clusters_are_nearest_centroid]),
+    ("residual_hist", residual_hist_negated, [PQ.test_histogram_quantiles_match_sorted_array]),
+    ("unpack", unpack_reversed_in_byte, [PQ.test_pack_layout_and_round_trip]),
 ]
 
 
