@@ -242,6 +242,18 @@ def unpack_reversed_in_byte(packed, dim, nbits):
     return np.ascontiguousarray(c.reshape(c.shape[0], -1, per)[:, :, ::-1].reshape(c.shape))
 
 
+# ------------------------------------------------- the oracle index's search
+REAL_SEARCH = oracle.OracleIndex.search
+
+
+def search_ncand_short(self, q_k, nprobe, ncand, k, nthreads=0, refine=False):
+    return REAL_SEARCH(self, q_k, nprobe, max(ncand - 1, 1), k, nthreads, refine)
+
+
+def search_ignores_refine(self, q_k, nprobe, ncand, k, nthreads=0, refine=False):
+    return REAL_SEARCH(self, q_k, nprobe, ncand, k, nthreads, False)
+
+
 MUTANTS = [
     ("grid_k", grid_k_ties_away, [PG.test_grid_examples_and_ties]),
     ("grid_k", grid_k_truncates, [PG.test_grid_examples_and_ties]),
@@ -287,6 +299,8 @@ MUTANTS = [
     ("assign", assign_farthest, [PQ.test_synthetic_clusters_are_nearest_centroid]),
     ("residual_hist", residual_hist_negated, [PQ.test_histogram_quantiles_match_sorted_array]),
     ("unpack", unpack_reversed_in_byte, [PQ.test_pack_layout_and_round_trip]),
+    ("OracleIndex.search", search_ncand_short, [PQ.test_search_composes_stage_definitions]),
+    ("OracleIndex.search", search_ignores_refine, [PR.test_refined_search_composes_stage_definitions]),
 ]
 
 
@@ -300,7 +314,8 @@ def _caches_built_unmutated():
 def test_pins_catch_planted_mistake(target, mutant, pins, monkeypatch):
     for pin in pins:  # the pins hold for the oracle as it is
         pin()
-    monkeypatch.setattr(oracle, target, mutant)
+    owner, name = (oracle.OracleIndex, target.split(".")[1]) if "." in target else (oracle, target)
+    monkeypatch.setattr(owner, name, mutant)
     caught = 0
     for pin in pins:
         try:
