@@ -5,7 +5,8 @@ operand), and at least one of the named pins must then fail.  This checks
 that the pins bind the oracle, not only that the oracle passes them.
 
 The wrappers change what the real function receives or returns; none
-re-implements the method.  Cached corpora and oracle indexes are built
+re-implements the method, and every input they pass stays within the
+arrays the oracle reads.  Cached corpora and oracle indexes are built
 before any mutant is active, so no mutant leaks into another test."""
 import math
 
@@ -136,7 +137,10 @@ def ds_residual_negated(S, q, w, b, n, cid, codes):
 
 
 def ds_window_shifted(S, q, w, b, n, cid, codes):
-    return REAL["doc_scores"](S, q, w, np.asarray(b) + 1, n, cid, codes)
+    """Each document's tokens read from one place early (the previous
+    document's last token in, its own last token out); shifting later would
+    read past the last document."""
+    return REAL["doc_scores"](S, q, w, np.maximum(np.asarray(b) - 1, 0), n, cid, codes)
 
 
 def chamfer_transposed(q, tok, doc_off):
@@ -307,7 +311,7 @@ MUTANTS = [
 @pytest.fixture(scope="module", autouse=True)
 def _caches_built_unmutated():
     corpus("tiny")
-    oracle_index("tiny")
+    oracle_index("tiny").token_lists()
 
 
 @pytest.mark.parametrize("target,mutant,pins", MUTANTS, ids=[m[1].__name__ for m in MUTANTS])
