@@ -13,11 +13,15 @@ queries already resident in HBM.  Prints ONE JSON line:
   recall_at_k      against exact MaxSim (Chamfer, Def. 1) on raw tokens,
                    brute force in fp64 on the GPU for a sample of queries
   collab           the CPU-GPU collaborative scoring (Alg. 3) on the same
-                   batch: QPS with chunks and with one chunk, the number of
-                   full-precision scores per query, recall@k
+                   batch, when its host store fits: QPS with chunks and with
+                   one chunk, full-precision scores per query, recall@k
 
-The default workload is the 100k-document corpus (256 queries x 32 tokens,
-nprobe 4, ncand 4096, k 10); ``--workload`` selects another.
+The default workload is the 8.8M-document corpus with MS MARCO's shape (4,096
+queries x 32 tokens, nprobe 16, ncand 16,384, k 100); ``--workload`` selects
+another.  The corpus is generated on the host in two passes over document
+chunks: the first feeds the builder's residual histogram, the exact-Chamfer
+reference on the GPU and the oracle's view of the corpus (for the CPU
+baseline); the second feeds the builder's codes.
 """
 from __future__ import annotations
 
@@ -25,6 +29,7 @@ import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -53,59 +58,157 @@ def describe(w) -> str:
             f"codes; {w.nq} queries x {w.Tq} tokens; nprobe {w.nprobe}, ncand {w.ncand}, k {w.k}")
 
 
-def build_corpus_index(w, threads):
-    import numpy as np
-    import synth
-    from paper_2608_23553_amd import build_index
-    corpus = synth.Corpus(w.corpus_spec(), nthreads=threads)
-
-    passes = [0]
-
-    def chunks():
-        step = 50_000
-        passes[0] += 1
-        for d0 in range(0, w.ndocs, step):
-            d1 = min(w.ndocs, d0 + step)
-            k, cl = corpus.tokens(d0, d1)
-            yield synth.k_to_bf16_bits(k), cl, corpus.lengths[d0:d1]
-            if (d0 // step) % 20 == 19:
-                log(f"index build pass {passes[0]}/2: {d1}/{w.ndocs} docs")
-
-    t = time.perf_counter()
-    b = build_index(synth.k_to_bf16_bits(corpus.centroids_k), w.nbits, chunks)
-    log(f"index built on host in {time.perf_counter() - t:.1f}s: {b.info()}")
-    return corpus, b
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
 
 
-def exact_topk_gpu(q_k, corpus, k, device):
-    """Exact Chamfer top-k (score desc, id asc) over raw grid tokens; fp64 on
-    the GPU (every product and sum is exact), chunked over tokens."""
+# --------------------------------------------------------------- recall reference
+def chamfer_block(Qf, T, lens):
+    """Exact Chamfer scores F[q, v] = sum_j max_{t in v} <Q_j, t> (Def. 1) of a
+    block of documents.  Qf [nq, Tq, d] float64, T [rows, d] float64 holding
+    the documents' tokens back to back, lens [n] int64 (host).  Every value is
+    a grid value, so each product and sum is exact in float64 and F is exact.
+    Documents of one length are scored together, so no padding enters a max."""
     import numpy as np
     import torch
+    nq, Tq, d = Qf.shape
+    lens = np.asarray(lens, dtype=np.int64)
+    off = np.zeros(len(lens) + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    F = torch.empty((nq, len(lens)), dtype=torch.float64, device=Qf.device)
+    A = Qf.reshape(nq * Tq, d)
+    tile_rows = 1 << 18
+    for L in np.unique(lens):
+        docs = np.nonzero(lens == L)[0]
+        per = max(1, tile_rows // int(L))
+        for i in range(0, len(docs), per):
+            dt = docs[i:i + per]
+            rows = (off[dt][:, None] + np.arange(L)[None, :]).reshape(-1)
+            S = A @ T[torch.from_numpy(rows).to(T.device)].T  # [nq*Tq, nt*L]
+            F[:, torch.from_numpy(dt).to(T.device)] = S.view(nq, Tq, len(dt), int(L)).amax(dim=3).sum(dim=1)
+    return F
+
+
+def topk_ids(F, k):
+    """The k best documents of each row by (score desc, id asc)."""
+    import torch
+    return torch.sort(F, dim=1, descending=True, stable=True).indices[:, :k]
+
+
+class ExactReference:
+    """Exact Chamfer scores of the recall queries over the whole corpus,
+    accumulated chunk by chunk on the device as the corpus is generated."""
+
+    def __init__(self, q_k, ndocs, device):
+        import numpy as np
+        import torch
+        self.Qf = torch.from_numpy(q_k.astype(np.float64) / 2048.0).to(device)
+        self.F = torch.empty((q_k.shape[0], ndocs), dtype=torch.float64, device=device)
+        self.device = device
+
+    def feed(self, k_chunk, lens, d0):
+        import torch
+        T = torch.from_numpy(k_chunk).to(self.device).to(torch.float64).mul_(1.0 / 2048.0)
+        self.F[:, d0:d0 + len(lens)] = chamfer_block(self.Qf, T, lens)
+
+    def topk(self, k):
+        return topk_ids(self.F, k).cpu().numpy()
+
+
+# --------------------------------------------------------------- CPU baseline
+class OracleView:
+    """The CPU baseline's oracle: its own quantiser (residual histogram) and
+    assignment, accumulated from the same generated chunks; documents are
+    regenerated when a query scores them (oracle.search_streamed)."""
+
+    def __init__(self, corpus, threads):
+        import numpy as np
+        from concurrent.futures import ThreadPoolExecutor
+        self.corpus, self.threads = corpus, threads
+        self.hist = np.zeros(8193, dtype=np.int64)
+        self.cid = np.empty(corpus.ntok, dtype=np.int32)
+        self.pool = ThreadPoolExecutor(max_workers=threads)
+
+    def feed(self, k_chunk, cl, d0, d1):
+        import numpy as np
+        import oracle
+        c = self.corpus
+        n = len(cl)
+        cuts = np.linspace(0, n, self.threads + 1).astype(np.int64)
+        parts = self.pool.map(lambda i: oracle.residual_hist(k_chunk[cuts[i]:cuts[i + 1]], cl[cuts[i]:cuts[i + 1]],
+                                                             c.centroids_k), range(self.threads))
+        self.hist += np.sum(list(parts), axis=0)
+        self.cid[c.doc_off[d0]:c.doc_off[d1]] = cl
+
+    def run(self, w, q_k, gpu_ids, seconds):
+        """Whole queries in batches of one per thread until `seconds` pass."""
+        import numpy as np
+        import oracle
+        import synth
+        t = time.perf_counter()
+        oi = oracle.OracleIndex(self.corpus.centroids_k, self.corpus.doc_off, self.cid, w.nbits, hist=self.hist,
+                                with_codes=False)
+        log(f"CPU baseline: oracle view built in {time.perf_counter() - t:.1f}s")
+        regen = synth.Corpus(w.corpus_spec(), nthreads=1)  # one thread per query
+
+        def one(qi):
+            return oracle.search_streamed(oi, q_k[qi], w.nprobe, w.ncand, w.k, regen.docs_tokens)
+
+        done, agree = 0, True
+        t0 = time.perf_counter()
+        while done < w.nq and time.perf_counter() - t0 < seconds:
+            batch = list(range(done, min(w.nq, done + self.threads)))
+            for qi, ref in zip(batch, self.pool.map(one, batch)):
+                m = len(ref["ids"])
+                agree &= bool(np.array_equal(ref["ids"], gpu_ids[qi, :m]))
+            done += len(batch)
+            log(f"CPU baseline: {done} queries in {time.perf_counter() - t0:.1f}s")
+        t_cpu = time.perf_counter() - t0
+        self.pool.shutdown()
+        return {"value": done / t_cpu, "unit": "queries/s", "cores": self.threads, "kind": "oracle",
+                "cpu_model": cpu_model(),
+                "sample": f"first {done} of the {w.nq} benchmark queries, whole path (probe, candidates, F', "
+                          f"top-ncand, document scores, top-k), {self.threads} threads, one query each, "
+                          f"{t_cpu:.1f}s",
+                "ids_match_gpu": agree}
+
+
+# --------------------------------------------------------------- index build
+def build(w, corpus, threads, ref, view, docs_per_chunk):
+    """Two passes over the corpus; returns the product builder."""
     import synth
-    nd = corpus.spec.ndocs
-    Q = torch.from_numpy(q_k.astype(np.float64) / 2048.0).to(device)  # [nq, Tq, d]
-    nq, Tq, _ = Q.shape
-    F = torch.empty((nq, nd), dtype=torch.float64, device=device)
-    # chunks of whole documents, ~8 GB of fp64 scores each; a chunk's
-    # documents are finished inside it
-    step = max(100, int(1e9 // (nq * Tq * 70)))
-    t_log = time.perf_counter()
-    for d0 in range(0, nd, step):
-        d1 = min(nd, d0 + step)
-        tk, _ = corpus.tokens(d0, d1)
-        T = torch.from_numpy(tk.astype(np.float64) / 2048.0).to(device)  # [rows, d]
-        lens = torch.from_numpy(corpus.lengths[d0:d1].astype(np.int64)).to(device)
-        doc = torch.repeat_interleave(torch.arange(d1 - d0, device=device), lens)
-        S = torch.matmul(Q.reshape(nq * Tq, -1), T.T).reshape(nq, Tq, -1)
-        best = torch.full((nq, Tq, d1 - d0), -float("inf"), dtype=torch.float64, device=device)
-        best.scatter_reduce_(2, doc.view(1, 1, -1).expand(nq, Tq, -1), S, reduce="amax", include_self=True)
-        F[:, d0:d1] = best.sum(dim=1)  # exact
-        if time.perf_counter() - t_log > 20:
-            log(f"exact MaxSim reference: {d1}/{nd} docs")
+    from paper_2608_23553_amd import Builder
+    b = Builder(synth.k_to_bf16_bits(corpus.centroids_k), w.nbits)
+    nd = w.ndocs
+    t, t_log = time.perf_counter(), time.perf_counter()
+    for d0 in range(0, nd, docs_per_chunk):
+        d1 = min(nd, d0 + docs_per_chunk)
+        k, bf, cl = corpus.tokens_ex(d0, d1, want_k=ref is not None or view is not None)
+        b.add_residuals(bf, cl)
+        if ref is not None:
+            ref.feed(k, corpus.lengths[d0:d1], d0)
+        if view is not None:
+            view.feed(k, cl, d0, d1)
+        if time.perf_counter() - t_log > 15 or d1 == nd:
+            log(f"pass 1 (residuals, reference, oracle view): {d1}/{nd} docs, {time.perf_counter() - t:.0f}s")
             t_log = time.perf_counter()
-    order = torch.sort(F, dim=1, descending=True, stable=True).indices[:, :k]
-    return order.cpu().numpy()
+    b.freeze()
+    b.reserve(nd, corpus.ntok)
+    for d0 in range(0, nd, docs_per_chunk):
+        d1 = min(nd, d0 + docs_per_chunk)
+        _, bf, cl = corpus.tokens_ex(d0, d1, want_k=False)
+        b.add_docs(bf, cl, corpus.lengths[d0:d1])
+        if time.perf_counter() - t_log > 15 or d1 == nd:
+            log(f"pass 2 (codes): {d1}/{nd} docs, {time.perf_counter() - t:.0f}s")
+            t_log = time.perf_counter()
+    log(f"index built on host in {time.perf_counter() - t:.1f}s: {b.info()}")
+    return b
 
 
 def source_sha(name):
@@ -130,9 +233,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="100k")
+    ap.add_argument("--workload", default="8.8m")
     ap.add_argument("--nq", type=int, default=0, help="override the batch size")
     ap.add_argument("--ncand", type=int, default=0, help="override the documents kept by the refinement")
+    ap.add_argument("--nprobe", type=int, default=0, help="override the centroids probed per query token")
     ap.add_argument("--refine", choices=["centroid", "token"], default="centroid",
                     help="refinement score: probed centroids' (chimera_search) or retrieved tokens' decoded "
                          "scores (chimera_search_refine)")
@@ -144,7 +248,13 @@ def main():
                                                          "(default 4 k)")
     ap.add_argument("--chunks", type=int, default=4, help="chunks of the collaborative scoring")
     ap.add_argument("--no-collab", action="store_true", help="skip the collaborative-scoring measurement")
-    ap.add_argument("--profile", action="store_true", help="warmup + timed steps only (for rocprofv3)")
+    ap.add_argument("--docs-per-chunk", type=int, default=100_000, help="documents per generated chunk")
+    ap.add_argument("--profile", action="store_true",
+                    help="warmup + timed steps only (for rocprofv3): no reference, oracle or extra legs")
+    ap.add_argument("--save-index", default="", help="also write the built index to this file")
+    ap.add_argument("--load-index", default="",
+                    help="load the index from this file (chimera_index_load) instead of building it; "
+                         "only with --profile")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -161,12 +271,17 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only: the whole index is resident in one "
                                    "GPU's HBM and no multi-GPU path exists; run with --gpus 1"}))
         sys.exit(2)
+    if args.load_index and not args.profile:
+        print(json.dumps({"error": "--load-index is for --profile runs (the reference and the oracle view are "
+                                   "built from the generated corpus)"}))
+        sys.exit(2)
     os.environ["CHIMERA_STAGE_TIMING"] = "1"
 
     import numpy as np
     import torch
     import synth
-    from paper_2608_23553_amd import ChimeraError  # noqa: F401
+    from paper_2608_23553_amd import Index
+    from paper_2608_23553_amd import chimera as _ch
 
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
@@ -174,16 +289,33 @@ def main():
     dev = torch.device("cuda:0")
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 8)
     w = synth.WORKLOADS[args.workload]
-    if args.nq:
-        w = w.scaled(nq=args.nq)
-    if args.ncand:
-        w = w.scaled(ncand=args.ncand)
-    from paper_2608_23553_amd import chimera as _ch
+    for key in ("nq", "ncand", "nprobe"):
+        if getattr(args, key):
+            w = w.scaled(**{key: getattr(args, key)})
     rmode = _ch.REFINE_TOKEN if args.refine == "token" else _ch.REFINE_CENTROID
-    corpus, builder = build_corpus_index(w, threads)
-    idx = builder.upload(0)
-    info = idx.info()
+    log(f"workload {describe(w)}; {threads} host threads ({cpu_model()})")
+    corpus = synth.Corpus(w.corpus_spec(), nthreads=threads)
     q_k, q_src = corpus.queries(w.nq, w.Tq)
+    nr = min(args.recall_queries, w.nq)
+    ref = view = builder = None
+    if args.load_index:
+        t = time.perf_counter()
+        idx = Index.load(args.load_index, 0)
+        log(f"index loaded in {time.perf_counter() - t:.1f}s")
+    else:
+        if not args.profile:
+            ref = ExactReference(q_k[:nr], w.ndocs, dev)
+            if not args.no_cpu_baseline:
+                view = OracleView(corpus, threads)
+        builder = build(w, corpus, threads, ref, view, args.docs_per_chunk)
+        if args.save_index:
+            t = time.perf_counter()
+            builder.save(args.save_index)
+            log(f"index saved in {time.perf_counter() - t:.1f}s")
+        t = time.perf_counter()
+        idx = builder.upload(0)
+        log(f"index uploaded in {time.perf_counter() - t:.1f}s")
+    info = idx.info()
     Q = torch.from_numpy(synth.k_to_bf16_bits(q_k).view(np.int16)).to(dev).view(torch.bfloat16)
     ids = torch.empty((w.nq, w.k), dtype=torch.int32, device=dev)
     scores = torch.empty((w.nq, w.k), dtype=torch.float32, device=dev)
@@ -207,7 +339,7 @@ def main():
     launches = nsub  # launches of each kernel over the timed steps
     log(f"{args.steps} steps in {elapsed:.3f}s: {qps:.0f} QPS; stages ms/step {stage_ms}")
     if args.profile:
-        print(json.dumps({"metric": METRIC, "value": qps, "profile_only": True}))
+        print(json.dumps({"metric": METRIC, "value": qps, "profile_only": True, "stages_ms": stage_ms}), flush=True)
         return
 
     # ---- algorithmic work of one step, from the stage taps and host copies
@@ -215,7 +347,8 @@ def main():
     ci, _ = idx.probe(Q, w.nprobe)
     cand, _, nval = idx.prune(Q, w.nprobe, w.ncand, refine=rmode)
     torch.cuda.synchronize()
-    sec = builder.sections()
+    sec = builder.sections(("doc_off", "ivf_off") + (("cid",) if rmode == _ch.REFINE_TOKEN else ()))
+    builder.close()
     lens = np.diff(sec["doc_off"])
     ci = ci.cpu().numpy()
     list_len = np.diff(sec["ivf_off"])
@@ -234,6 +367,7 @@ def main():
         tok_len = np.bincount(sec["cid"], minlength=w.ncent)
         walked = int(tok_len[ci].sum())
         walk_bytes = (8.0 + 16 * w.nbits) * walked + 4.0 * w.nq * w.ndocs
+    del sec
     cand, nval = cand.cpu().numpy(), nval.cpu().numpy()
     scored_tokens = int(sum(lens[cand[q, :nval[q]]].sum() for q in range(w.nq)))
     code_bytes_tok = 16 * w.nbits + 4
@@ -251,11 +385,18 @@ def main():
     per_launch_amount = amount * args.steps / launches
     achieved = per_launch_amount / per_launch_s / (1e12 if unit == "TFLOP/s" else 1e9)
     # the committed counter summary describes the default configuration only
-    default_cfg = not (args.nq or args.ncand or args.refine != "centroid")
+    default_cfg = not (args.nq or args.ncand or args.nprobe or args.refine != "centroid")
     traffic = measured_traffic(dominant, w.name) if default_cfg else None
     roofline = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
                 "traffic": traffic, "kernel": KERNEL_OF_STAGE[dominant],
-                "per_launch": {"algorithmic": per_launch_amount, "ms": per_launch_s * 1e3}}
+                "per_launch": {"algorithmic": per_launch_amount, "ms": per_launch_s * 1e3, "launches_per_step":
+                               launches / args.steps}}
+    stage_rooflines = {}
+    for s in STAGES:
+        bd, am, pk, un = work[s]
+        if stage_ms[s] > 0:
+            a = am / (stage_ms[s] / 1e3) / (1e12 if un == "TFLOP/s" else 1e9)
+            stage_rooflines[s] = {"bound": bd, "achieved": a, "unit": un, "frac": a / pk}
     score_gbs = work["score"][1] / (stage_ms["score"] / 1e3) / 1e9
     probe_tflops = work["probe"][1] / (stage_ms["probe"] / 1e3) / 1e12
 
@@ -289,7 +430,7 @@ def main():
     # ---- QPS at smaller batches (the same index and queries, resident in HBM)
     log("QPS at smaller batches")
     qps_by_batch = {}
-    for nb in sorted({1, 8, 32, 128, w.nq}):
+    for nb in sorted({1, 8, 32, 128, 512, w.nq}):
         if nb > w.nq:
             continue
         reps = max(3, min(50, int(2048 // nb)))
@@ -305,13 +446,12 @@ def main():
     idx.stage_times()  # drop these searches' events
     log(f"QPS by batch: {qps_by_batch}")
 
-    # ---- recall@k against exact MaxSim
-    log("recall against exact MaxSim")
-    nr = min(args.recall_queries, w.nq)
-    truth = exact_topk_gpu(q_k[:nr], corpus, w.k, dev)
+    # ---- recall@k against exact MaxSim (reference accumulated during the build)
+    truth = ref.topk(w.k)
     got = ids[:nr].cpu().numpy()
     recall = float(np.mean([len(set(got[i]) & set(truth[i])) / w.k for i in range(nr)]))
     src_first = float(np.mean(got[:, 0] == q_src[:nr]))
+    del ref
 
     # ---- CPU-GPU collaborative scoring (Alg. 3): the GPU path's candidates
     # re-ranked on the host from the full-precision tokens, chunk by chunk
@@ -320,9 +460,7 @@ def main():
     if not args.no_collab and fb_bytes <= 32 * 2**30:
         kfb = args.kfb or 4 * w.k
         log(f"collaborative scoring: kfb {kfb}, {args.chunks} chunks, {threads} host threads")
-        tk, _ = corpus.tokens()
-        fb = synth.k_to_bf16_bits(tk)
-        del tk
+        _, fb, _ = corpus.tokens_ex(want_k=False, want_cluster=False)
         idx.attach_fullbit(fb)  # the index keeps its own grid copy
         del fb
         runs = {}
@@ -344,32 +482,10 @@ def main():
         collab = {"skipped": f"the full-precision host store would take {fb_bytes / 2**30:.0f} GiB"}
 
     # ---- CPU baseline: the oracle, untouched, on a bounded sample
-    log("CPU baseline")
     cpu = None
-    # the oracle keeps every raw token (256 B) and its unpacked codes (128 B)
-    oracle_bytes = info["ntokens"] * (2 * 128 + 128)
-    if not args.no_cpu_baseline and oracle_bytes > 64 * 2**30:
-        log(f"CPU baseline skipped: the oracle's in-memory index would take {oracle_bytes / 2**30:.0f} GiB")
-        cpu = {"value": None, "kind": "oracle",
-               "skipped": f"the oracle's in-memory index needs {oracle_bytes / 2**30:.0f} GiB of host memory"}
-    elif not args.no_cpu_baseline:
-        import oracle
-        tk, cl = corpus.tokens()
-        oi = oracle.OracleIndex(corpus.centroids_k, corpus.doc_off, cl, w.nbits, tok_k=tk)
-        del tk
-        probe_n = min(w.nq, max(1, threads))  # one query per thread
-        s = time.perf_counter()
-        oi.search(q_k[:probe_n], w.nprobe, w.ncand, w.k, nthreads=threads, refine=args.refine == "token")
-        t_probe = time.perf_counter() - s
-        n_cpu = int(min(w.nq, max(probe_n, probe_n * args.cpu_seconds / max(t_probe, 1e-3) // probe_n * probe_n)))
-        s = time.perf_counter()
-        ref = oi.search(q_k[:n_cpu], w.nprobe, w.ncand, w.k, nthreads=threads, refine=args.refine == "token")
-        t_cpu = time.perf_counter() - s
-        agree = bool(np.array_equal(ref["ids"], ids[:n_cpu].cpu().numpy()))
-        cpu = {"value": n_cpu / t_cpu, "unit": "queries/s", "cores": threads, "kind": "oracle",
-               "sample": f"first {n_cpu} of the {w.nq} benchmark queries, whole path (probe, candidates, F', "
-                         f"top-ncand, document scores, top-k), {threads} threads over queries, {t_cpu:.1f}s",
-               "ids_match_gpu": agree}
+    if view is not None:
+        log("CPU baseline")
+        cpu = view.run(w, q_k, ids.cpu().numpy(), args.cpu_seconds)
 
     out = {
         "metric": METRIC, "value": qps, "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
@@ -383,6 +499,7 @@ def main():
         "p50_ms_nq1": float(np.percentile(lat, 50)), "p95_ms_nq1": float(np.percentile(lat, 95)),
         "p99_ms_nq1": float(np.percentile(lat, 99)), "nq1_stages_ms": lat_stage_ms,
         "code_scan_GBps": score_gbs, "probe_TFLOPs": probe_tflops, "stages_ms": stage_ms,
+        "stage_rooflines": stage_rooflines,
         "work_per_step": {"posting_entries": entries, "posting_entries_walked": walked, "scored_tokens": scored_tokens,
                           "candidates": int(nval.sum())},
         "roofline": roofline, "cpu_baseline": cpu, "collab": collab,

@@ -25,10 +25,23 @@
  *    CHIMERA_E_BUSY.
  *  - Value grid G: all vector values are used as bf16 numbers that are
  *    integer multiples of 2^-11.  Inputs are rounded onto G (nearest, ties to
- *    even), which leaves grid values unchanged.  On G every inner product is
- *    an exact multiple of 2^-22, so scores are exact and independent of the
- *    summation order provided every query token has L2 norm <= 2 (unit
- *    vectors in the intended use).
+ *    even), which leaves grid values unchanged.  On G every product is an
+ *    exact multiple of 2^-22, and float32 holds every such multiple below 4
+ *    in magnitude, so a sum of products is exact in any order while its
+ *    partial sums stay below 4.  A query token q is scored against centroid
+ *    c plus decoded residual w, so by Cauchy-Schwarz the scores are exact
+ *    and independent of the summation order when
+ *        ||q|| * (max_c ||c|| + sqrt(dim) * max_u |w_u|) < 4,
+ *    i.e. every query token's L2 norm (after rounding) is below
+ *    chimera_index_info.q_norm_limit; for unit centroids and the workloads'
+ *    residual weights that is about 2.4 (unit query tokens in the intended
+ *    use).  Each query token then contributes less than 2^24 units of 2^-22
+ *    to a score, so the integer sum over up to 64 tokens cannot overflow.
+ *    With CHIMERA_CHECK_QUERIES=1 in the environment when the index is
+ *    loaded, every search and stage tap first checks this bound on the
+ *    device (the call synchronises its stream) and returns CHIMERA_E_INVAL,
+ *    outputs untouched, for a query token at or above the limit or with a
+ *    value that is not finite.
  *  - Orders: every "top" list is ordered by (score descending, id
  *    ascending); equal scores are broken by the lowest id.
  */
@@ -72,6 +85,7 @@ enum { CHIMERA_REFINE_CENTROID = 0, CHIMERA_REFINE_TOKEN = 1 };
 #define CHIMERA_MAX_TQ 64
 #define CHIMERA_MAX_NPROBE 64
 #define CHIMERA_MAX_NCAND (1 << 20)
+#define CHIMERA_MAX_K 8192
 
 typedef struct chimera_index chimera_index;
 typedef struct chimera_builder chimera_builder;
@@ -86,6 +100,8 @@ typedef struct {
   int32_t max_doc_len;   /* longest document, tokens */
   int64_t device_bytes;  /* device memory held by the index data */
   int32_t device;        /* HIP device ordinal */
+  double q_norm_limit;   /* query tokens of smaller L2 norm get exact scores
+                            (see "Value grid"); 0 for a builder */
 } chimera_index_info;
 
 /* Last error message of the calling thread; never NULL. */
@@ -125,9 +141,16 @@ int chimera_builder_add_residuals(chimera_builder *b, const uint16_t *tokens_bf1
 /* Ends pass 1: fixes cutoffs and bucket weights.  E_INVAL if no residual. */
 int chimera_builder_freeze_quantizer(chimera_builder *b);
 /* Pass 2: ndocs documents; doc_lens host [ndocs] (>= 1 each), tokens and cids
- * hold sum(doc_lens) rows in document order. */
+ * hold sum(doc_lens) rows in document order.  A call that fails (E_INVAL,
+ * E_NOMEM) leaves the builder as it was before the call, so later calls
+ * continue from the last accepted document; the same holds for
+ * chimera_builder_add_residuals. */
 int chimera_builder_add_docs(chimera_builder *b, const uint16_t *tokens_bf16, const int32_t *cids,
                              const int32_t *doc_lens, int64_t ndocs);
+/* Optional, before pass 2: reserves host memory for ndocs documents and ntok
+ * tokens, so that add_docs never reallocates (a 2-bit index of 600M tokens
+ * holds about 20 GB of codes).  E_NOMEM if the memory cannot be reserved. */
+int chimera_builder_reserve(chimera_builder *b, int64_t ndocs, int64_t ntok);
 /* Quantiser as fixed by freeze: cut_k [2^b - 1] cutoffs in units of 2^-11,
  * weights_bf16 [2^b] bucket values.  Either pointer may be NULL. */
 int chimera_builder_quantizer(const chimera_builder *b, int32_t *cut_k, uint16_t *weights_bf16);
@@ -166,7 +189,7 @@ int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out);
  *   nprobe  1 .. min(ncent, 64): centroids probed per query token
  *   ncand   >= k: documents kept by the refinement (k_refine of Alg. 1);
  *           values above ndocs are clamped to ndocs
- *   k       >= 1 results per query
+ *   k       1 .. min(ncand, CHIMERA_MAX_K) results per query
  *   ids     device [nq][k] int32, scores device [nq][k] float32
  *
  * Steps, per query:

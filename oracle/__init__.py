@@ -295,6 +295,24 @@ def collaborative_scoring(refine_ids, approx_keys, exact_key, ncand: int, kfb: i
     return ids, keys, len(full)
 
 
+def search_streamed(oi, q_k, nprobe: int, ncand: int, k: int, docs_tokens):
+    """The oracle's search of one query q_k [Tq, dim] on an OracleIndex built
+    without codes: the stages composed as orc_search composes them, with the
+    kept documents' tokens supplied by docs_tokens(ids int64) -> (tok_k
+    [rows, dim], cid [rows], begin [len(ids)]) and encoded here (for corpora
+    whose tokens do not fit in memory; regenerated by the caller)."""
+    S = centroid_scores(q_k, oi.cent_k)
+    ci, ck = probe(S, nprobe)
+    docs, fp = partial_scores(S, ci, oi.ivf_off, oi.ivf_doc, oi.ndocs)
+    r, rk = topk(docs, fp, ncand)
+    tk, cl, begin = docs_tokens(r.astype(np.int64))
+    codes = encode(tk, cl, oi.cent_k, oi.cut_k, oi.nbits)
+    lens = np.diff(oi.doc_off)[r].astype(np.int32)
+    fh = doc_scores(S, q_k, oi.w_k, begin, lens, cl, codes)
+    ids, keys = topk(r, fh, k)
+    return dict(cent_ids=ci, cent_keys=ck, cand=r, cand_keys=rk, ids=ids, keys=keys, scores=keys_to_scores(keys))
+
+
 # ------------------------------------------------------- oracle index
 class OracleIndex:
     """The oracle's own view of a corpus: assignment given by the corpus,

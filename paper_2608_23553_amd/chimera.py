@@ -33,7 +33,8 @@ class ChimeraError(RuntimeError):
 class _Info(ctypes.Structure):
     _fields_ = [("ndocs", ctypes.c_int64), ("ntokens", ctypes.c_int64), ("nnz", ctypes.c_int64),
                 ("ncent", ctypes.c_int32), ("dim", ctypes.c_int32), ("nbits", ctypes.c_int32),
-                ("max_doc_len", ctypes.c_int32), ("device_bytes", ctypes.c_int64), ("device", ctypes.c_int32)]
+                ("max_doc_len", ctypes.c_int32), ("device_bytes", ctypes.c_int64), ("device", ctypes.c_int32),
+                ("q_norm_limit", ctypes.c_double)]
 
 
 def lib():
@@ -51,6 +52,7 @@ def lib():
         "chimera_builder_add_residuals": ([P, P, P, I64], INT),
         "chimera_builder_freeze_quantizer": ([P], INT),
         "chimera_builder_add_docs": ([P, P, P, P, I64], INT),
+        "chimera_builder_reserve": ([P, I64, I64], INT),
         "chimera_builder_quantizer": ([P, P, P], INT),
         "chimera_builder_save": ([P, ctypes.c_char_p], INT),
         "chimera_builder_upload": ([P, INT, P], INT),
@@ -147,6 +149,9 @@ class Builder:
         self._rows(t, c, int(l.astype(np.int64).sum()))
         _check(lib().chimera_builder_add_docs(self._h, _np(t), _np(c), _np(l), l.shape[0]))
 
+    def reserve(self, ndocs: int, ntok: int):
+        _check(lib().chimera_builder_reserve(self._h, ndocs, ntok))
+
     def quantizer(self) -> Tuple[np.ndarray, np.ndarray]:
         B = 1 << self.nbits
         cut = np.empty(B - 1, np.int32)
@@ -159,13 +164,15 @@ class Builder:
         _check(lib().chimera_builder_info(self._h, ctypes.byref(st)))
         return _info(st)
 
-    def sections(self) -> dict:
+    def sections(self, which=("doc_off", "cid", "codes", "ivf_off", "ivf_doc")) -> dict:
+        """Host copies of the built sections named in `which`."""
         inf = self.info()
-        out = dict(doc_off=np.empty(inf["ndocs"] + 1, np.int64), cid=np.empty(inf["ntokens"], np.int32),
-                   codes=np.empty((inf["ntokens"], self.dim * self.nbits // 8), np.uint8),
-                   ivf_off=np.empty(self.ncent + 1, np.int64), ivf_doc=np.empty(inf["nnz"], np.int32))
-        _check(lib().chimera_builder_sections(self._h, _np(out["doc_off"]), _np(out["cid"]), _np(out["codes"]),
-                                              _np(out["ivf_off"]), _np(out["ivf_doc"])))
+        shapes = dict(doc_off=((inf["ndocs"] + 1,), np.int64), cid=((inf["ntokens"],), np.int32),
+                      codes=((inf["ntokens"], self.dim * self.nbits // 8), np.uint8),
+                      ivf_off=((self.ncent + 1,), np.int64), ivf_doc=((inf["nnz"],), np.int32))
+        out = {n: np.empty(*shapes[n]) for n in which}
+        _check(lib().chimera_builder_sections(self._h, *(_np(out.get(n)) for n in
+                                                        ("doc_off", "cid", "codes", "ivf_off", "ivf_doc"))))
         return out
 
     def save(self, path: str):

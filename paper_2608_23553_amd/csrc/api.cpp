@@ -1,6 +1,7 @@
 // api.cpp - the C ABI: errors, device index, validation and the per-batch
 // orchestration of the query path (Alg. 1 without the CPU full-bit stage).
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -62,6 +63,25 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   idx->h_doc_off = h.doc_off;
   std::memcpy(idx->h_weights, h.weights.data(), h.weights.size() * 2);
   std::memcpy(idx->h_cut, h.cut_k.data(), h.cut_k.size() * 4);
+  {
+    // Exactness bound (header, "Value grid"): a query token q scores
+    // <q, c> + <q, w(code)>; every partial sum is at most
+    // ||q|| (max_c ||c|| + sqrt(dim) max_u |w_u|) in magnitude and must stay
+    // below 4.  Norms from the grid integers, rounded up slightly.
+    int64_t c2max = 0;
+    for (int32_t c = 0; c < h.ncent; ++c) {
+      int64_t c2 = 0;
+      for (int d = 0; d < h.dim; ++d) {
+        const int64_t k = (int64_t)(float_of_bf16(h.cent[(size_t)c * h.dim + d]) * 2048.0f);
+        c2 += k * k;
+      }
+      c2max = std::max(c2max, c2);
+    }
+    double wmax = 0.0;
+    for (uint16_t w : h.weights) wmax = std::max(wmax, (double)std::fabs(float_of_bf16(w)));
+    const double bound = std::sqrt((double)c2max) / 2048.0 + std::sqrt((double)h.dim) * wmax;
+    idx->q_norm_limit = bound > 0.0 ? 4.0 / (bound * (1.0 + 1e-9)) : 1e30;
+  }
   std::vector<int8_t> dense_slot;
   std::vector<uint64_t> doc_dense;
   if (int rc = dense_lists(h, dense_slot, doc_dense, idx->ndense)) {
@@ -116,6 +136,13 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   }
   const char *t = std::getenv("CHIMERA_STAGE_TIMING");
   idx->timing = t && t[0] == '1';
+  const char *cq = std::getenv("CHIMERA_CHECK_QUERIES");
+  idx->check_queries = cq && cq[0] == '1';
+  if (idx->check_queries && hipMalloc(&idx->d_check, sizeof(unsigned long long)) != hipSuccess) {
+    idx->d_check = nullptr;
+    chimera_index_free(idx);
+    return fail(CHIMERA_E_NOMEM, "query check word");
+  }
   *out = idx;
   return CHIMERA_OK;
 }
@@ -141,7 +168,7 @@ static int check_query_args(const chimera_index *idx, const void *Q, int q_dtype
   return CHIMERA_OK;
 }
 
-static const int kMaxK = 8192;
+static const int kMaxK = CHIMERA_MAX_K;
 
 // No C++ exception leaves the C ABI: host allocations inside a call that fail
 // report E_NOMEM.
@@ -235,9 +262,29 @@ static void stage_mark(chimera_index *idx, hipStream_t s, bool on) {
   (void)hipEventRecord(idx->ev[idx->ev_used++], s);
 }
 
+// The on-request query check (CHIMERA_CHECK_QUERIES): E_INVAL, before
+// anything else is launched, if a query token's norm breaks the limit.
+static int check_queries(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int Tq, hipStream_t s) {
+  const unsigned long long none = ~0ull;
+  unsigned long long bad = none;
+  const double lim = idx->q_norm_limit * 2048.0;
+  CHIMERA_HIP(hipMemcpyAsync(idx->d_check, &none, sizeof none, hipMemcpyHostToDevice, s));
+  launch_check_queries(Q, q_dtype, nq * Tq, lim * lim, idx->d_check, s);
+  CHIMERA_HIP(hipGetLastError());
+  CHIMERA_HIP(hipMemcpyAsync(&bad, idx->d_check, sizeof bad, hipMemcpyDeviceToHost, s));
+  CHIMERA_HIP(hipStreamSynchronize(s));
+  if (bad != none)
+    return fail(CHIMERA_E_INVAL, "query %lld token %lld: L2 norm not below %.6g (the limit for exact scores on this "
+                "index) or a value that is not finite", (long long)(bad / Tq), (long long)(bad % Tq),
+                idx->q_norm_limit);
+  return CHIMERA_OK;
+}
+
 static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int Tq, int nprobe, int ncand, int k,
                Stop stop, Outs o, hipStream_t s, int refine = CHIMERA_REFINE_CENTROID) {
   const int TQP = Tq <= 32 ? 32 : 64;
+  if (idx->check_queries)
+    if (int rc = check_queries(idx, Q, q_dtype, nq, Tq, s)) return rc;
   // sub-batch size: the largest that fits the scratch budget (carve_bytes
   // grows with nb, but not in proportion: the select's chunking depends on nb)
   const size_t budget = scratch_budget();
@@ -395,7 +442,7 @@ void chimera_index_free(chimera_index *idx) {
   (void)hipDeviceSynchronize();
   void *ptrs[] = {idx->d_cent,    idx->d_doc_off,    idx->d_cid,       idx->d_codes,     idx->d_ivf_off,
                   idx->d_ivf_doc, idx->d_dense_slot, idx->d_doc_dense, idx->d_tok_off,   idx->d_ivf_tok,
-                  idx->d_tok_doc, idx->scratch};
+                  idx->d_tok_doc, idx->scratch,      idx->d_check};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   collab_free(idx);
@@ -409,6 +456,7 @@ int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out) {
   out->ndocs = idx->ndocs; out->ntokens = idx->ntok; out->nnz = idx->nnz; out->ncent = idx->ncent;
   out->dim = idx->dim; out->nbits = idx->nbits; out->max_doc_len = idx->max_doc_len;
   out->device_bytes = idx->device_bytes; out->device = idx->device;
+  out->q_norm_limit = idx->q_norm_limit;
   return CHIMERA_OK;
 }
 

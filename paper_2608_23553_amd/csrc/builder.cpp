@@ -281,13 +281,66 @@ struct chimera_builder {
   bool lists_built = false;
 };
 
-static int grid_rows(const uint16_t *bf16, int64_t n, int16_t *out) {
+// bf16 bit patterns -> grid integers k = x * 2^11 (nearest, ties to even,
+// which is grid_k_of_float for bf16 inputs: above 2^-4 a bf16 value is
+// already a multiple of 2^-11).  Returns false if a value lies outside
+// [-1, 1] (NaN included); out is then unspecified.
+__attribute__((target_clones("avx512bw", "avx2", "default")))
+static bool grid_rows(const uint16_t *bf16, int64_t n, int16_t *out) {
+  bool ok = true;
   for (int64_t i = 0; i < n; ++i) {
-    int32_t k = grid_k_of_float(float_of_bf16(bf16[i]));
-    if (k < -2048 || k > 2048) return -1;
-    out[i] = (int16_t)k;
+    const uint32_t u = (uint32_t)bf16[i] << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    const bool in = std::fabs(f) <= 1.0f;
+    // 1.5 * 2^23 has unit spacing: adding and removing it rounds f * 2^11
+    // (exact, |f * 2^11| <= 2^11) to the nearest integer, ties to even
+    const float r = (f * 2048.0f + 12582912.0f) - 12582912.0f;
+    out[i] = (int16_t)(in ? r : 0.0f);
+    ok &= in;
   }
-  return 0;
+  return ok;
+}
+
+// Residual histogram of ntok tokens: hist[r + 4096] counts residual
+// components r = k_token - k_centroid.  Returns false on a value outside
+// [-1, 1].
+static bool residual_hist_rows(const uint16_t *tok, const int32_t *cids, int64_t ntok, const int16_t *cent_k,
+                               int dim, int64_t *hist) {
+  int16_t row[CHIMERA_DIM];
+  for (int64_t t = 0; t < ntok; ++t) {
+    if (!grid_rows(tok + t * dim, dim, row)) return false;
+    const int16_t *c = cent_k + (size_t)cids[t] * dim;
+    for (int d = 0; d < dim; ++d) hist[row[d] - c[d] + 4096]++;
+  }
+  return true;
+}
+
+// Packed codes of ntok tokens (2-bit: dim 4i+s in bits [2s, 2s+1] of byte i;
+// 4-bit: dim 2i in the low nibble, 2i+1 in the high one).  code(r) is the
+// number of cutoffs strictly below r.  Returns false on a value outside
+// [-1, 1].
+__attribute__((target_clones("avx512bw", "avx2", "default")))
+static bool encode_rows(const uint16_t *tok, const int32_t *cids, int64_t ntok, const int16_t *cent_k, int dim,
+                        const int16_t *cut, int ncut, int nbits, uint8_t *out) {
+  int16_t row[CHIMERA_DIM];
+  uint8_t code[CHIMERA_DIM];
+  const int cb = dim * nbits / 8;
+  for (int64_t t = 0; t < ntok; ++t) {
+    if (!grid_rows(tok + t * dim, dim, row)) return false;
+    const int16_t *c = cent_k + (size_t)cids[t] * dim;
+    for (int d = 0; d < dim; ++d) row[d] = (int16_t)(row[d] - c[d]);
+    for (int d = 0; d < dim; ++d) code[d] = 0;
+    for (int i = 0; i < ncut; ++i)
+      for (int d = 0; d < dim; ++d) code[d] += cut[i] < row[d];
+    uint8_t *o = out + t * cb;
+    if (nbits == 2)
+      for (int i = 0; i < cb; ++i)
+        o[i] = (uint8_t)(code[4 * i] | code[4 * i + 1] << 2 | code[4 * i + 2] << 4 | code[4 * i + 3] << 6);
+    else
+      for (int i = 0; i < cb; ++i) o[i] = (uint8_t)(code[2 * i] | code[2 * i + 1] << 4);
+  }
+  return true;
 }
 
 // floor(num * n / den)-th smallest residual (0-based, clamped to n-1)
@@ -341,7 +394,7 @@ int chimera_builder_create(const uint16_t *centroids_bf16, int32_t ncent, int32_
     delete b;
     return fail(CHIMERA_E_NOMEM, "builder allocation");
   }
-  if (grid_rows(centroids_bf16, (int64_t)ncent * dim, b->cent_k.data()) != 0) {
+  if (!grid_rows(centroids_bf16, (int64_t)ncent * dim, b->cent_k.data())) {
     delete b;
     return fail(CHIMERA_E_INVAL, "centroid components must lie in [-1, 1]");
   }
@@ -358,23 +411,20 @@ int chimera_builder_add_residuals(chimera_builder *b, const uint16_t *tokens_bf1
   const int dim = b->h.dim, ncent = b->h.ncent;
   for (int64_t t = 0; t < ntok; ++t)
     if ((uint32_t)cids[t] >= (uint32_t)ncent) return fail(CHIMERA_E_INVAL, "cid out of range at token %lld", (long long)t);
+  // per-thread histograms, merged only when every token was valid, so a
+  // rejected call leaves the builder as it was
   std::vector<std::vector<int64_t>> part;
   std::mutex mu;
-  bool bad = false;
+  std::atomic<bool> bad{false};
   parallel_for(ntok, [&](int64_t a, int64_t e) {
     std::vector<int64_t> hloc(8193, 0);
-    std::vector<int16_t> row(dim);
-    bool lbad = false;
-    for (int64_t t = a; t < e && !lbad; ++t) {
-      if (grid_rows(tokens_bf16 + t * dim, dim, row.data()) != 0) { lbad = true; break; }
-      const int16_t *c = b->cent_k.data() + (size_t)cids[t] * dim;
-      for (int d = 0; d < dim; ++d) hloc[row[d] - c[d] + 4096]++;
-    }
+    if (!residual_hist_rows(tokens_bf16 + a * dim, cids + a, e - a, b->cent_k.data(), dim, hloc.data())) bad = true;
     std::lock_guard<std::mutex> g(mu);
-    if (lbad) bad = true;
-    for (int i = 0; i < 8193; ++i) b->hist[i] += hloc[i];
+    part.push_back(std::move(hloc));
   });
   if (bad) return fail(CHIMERA_E_INVAL, "token components must lie in [-1, 1]");
+  for (const auto &hp : part)
+    for (int i = 0; i < 8193; ++i) b->hist[i] += hp[i];
   return CHIMERA_OK;
 }
 
@@ -403,50 +453,65 @@ int chimera_builder_add_docs(chimera_builder *b, const uint16_t *tokens_bf16, co
   if (!b || ndocs < 0 || (ndocs > 0 && (!tokens_bf16 || !cids || !doc_lens))) return fail(CHIMERA_E_INVAL, "bad argument");
   if (!b->frozen) return fail(CHIMERA_E_INVAL, "freeze the quantiser before adding documents");
   HostIndex &h = b->h;
-  const int dim = h.dim, nbits = h.nbits, B = 1 << nbits;
+  const int dim = h.dim, nbits = h.nbits, ncut = (1 << nbits) - 1;
   const int64_t cb = h.code_bytes();
   int64_t rows = 0;
+  int32_t longest = 0;
   for (int64_t i = 0; i < ndocs; ++i) {
     if (doc_lens[i] < 1) return fail(CHIMERA_E_INVAL, "document %lld has no token", (long long)i);
     rows += doc_lens[i];
+    longest = std::max(longest, doc_lens[i]);
   }
   for (int64_t t = 0; t < rows; ++t)
     if ((uint32_t)cids[t] >= (uint32_t)h.ncent) return fail(CHIMERA_E_INVAL, "cid out of range at token %lld", (long long)t);
   const int64_t t0 = h.ntok;
+  const size_t ndoc_off = h.doc_off.size();
+  // every section grows first and is cut back if a token is rejected, so a
+  // failed call leaves the builder exactly as it was
+  auto roll_back = [&] {
+    h.cid.resize(t0);
+    h.codes.resize(t0 * cb);
+    h.doc_off.resize(ndoc_off);
+  };
   try {
     h.cid.resize(t0 + rows);
     h.codes.resize((t0 + rows) * cb);
-    h.doc_off.reserve(h.doc_off.size() + ndocs);
+    h.doc_off.reserve(ndoc_off + ndocs);
   } catch (...) {
+    roll_back();
     return fail(CHIMERA_E_NOMEM, "host allocation for %lld tokens", (long long)rows);
   }
-  for (int64_t i = 0; i < ndocs; ++i) {
-    h.doc_off.push_back(h.doc_off.back() + doc_lens[i]);
-    h.max_doc_len = std::max(h.max_doc_len, doc_lens[i]);
-  }
-  std::memcpy(h.cid.data() + t0, cids, rows * 4);
+  int16_t cut[15];
+  for (int i = 0; i < ncut; ++i) cut[i] = (int16_t)h.cut_k[i];
   std::atomic<bool> bad{false};
   parallel_for(rows, [&](int64_t a, int64_t e) {
-    std::vector<int16_t> row(dim);
-    for (int64_t t = a; t < e; ++t) {
-      if (grid_rows(tokens_bf16 + t * dim, dim, row.data()) != 0) { bad = true; return; }
-      const int16_t *c = b->cent_k.data() + (size_t)cids[t] * dim;
-      uint8_t *out = h.codes.data() + (t0 + t) * cb;
-      std::memset(out, 0, cb);
-      for (int d = 0; d < dim; ++d) {
-        int32_t r = (int32_t)row[d] - c[d];
-        int code = 0;
-        for (int i = 0; i < B - 1; ++i) code += h.cut_k[i] < r;
-        // 2-bit: dim 4i+s -> bits [2s,2s+1] of byte i; 4-bit: dim 2i low nibble, 2i+1 high
-        int per = 8 / nbits;
-        out[d / per] |= (uint8_t)(code << (nbits * (d % per)));
-      }
-    }
+    if (!encode_rows(tokens_bf16 + a * dim, cids + a, e - a, b->cent_k.data(), dim, cut, ncut, nbits,
+                     h.codes.data() + (t0 + a) * cb))
+      bad = true;
   });
-  if (bad) return fail(CHIMERA_E_INVAL, "token components must lie in [-1, 1]");
+  if (bad) {
+    roll_back();
+    return fail(CHIMERA_E_INVAL, "token components must lie in [-1, 1]");
+  }
+  std::memcpy(h.cid.data() + t0, cids, rows * 4);
+  for (int64_t i = 0; i < ndocs; ++i) h.doc_off.push_back(h.doc_off.back() + doc_lens[i]);
+  h.max_doc_len = std::max(h.max_doc_len, longest);
   h.ntok = t0 + rows;
   h.ndocs += ndocs;
   b->lists_built = false;
+  return CHIMERA_OK;
+}
+
+int chimera_builder_reserve(chimera_builder *b, int64_t ndocs, int64_t ntok) {
+  if (!b || ndocs < 0 || ntok < 0) return fail(CHIMERA_E_INVAL, "bad argument");
+  HostIndex &h = b->h;
+  try {
+    h.doc_off.reserve((size_t)ndocs + 1);
+    h.cid.reserve((size_t)ntok);
+    h.codes.reserve((size_t)ntok * (size_t)h.code_bytes());
+  } catch (...) {
+    return fail(CHIMERA_E_NOMEM, "host allocation for %lld tokens", (long long)ntok);
+  }
   return CHIMERA_OK;
 }
 
@@ -483,7 +548,7 @@ int chimera_builder_info(const chimera_builder *b, chimera_index_info *out) {
   build_lists(const_cast<chimera_builder *>(b));
   const HostIndex &h = b->h;
   out->ndocs = h.ndocs; out->ntokens = h.ntok; out->nnz = h.nnz; out->ncent = h.ncent; out->dim = h.dim;
-  out->nbits = h.nbits; out->max_doc_len = h.max_doc_len; out->device = -1;
+  out->nbits = h.nbits; out->max_doc_len = h.max_doc_len; out->device = -1; out->q_norm_limit = 0.0;
   out->device_bytes = (int64_t)(h.cent.size() * 2 + h.doc_off.size() * 8 + h.cid.size() * 4 + h.codes.size() +
                                 h.ivf_off.size() * 8 + h.ivf_doc.size() * 4);
   return CHIMERA_OK;

@@ -501,25 +501,41 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
     const HostKernels K = pick_kernels();
     const unsigned nt = std::max(1u, std::min(32u, std::thread::hardware_concurrency()));
     std::atomic<int64_t> first_bad{ntok};
+    auto slice = [&](unsigned w) {
+      const int64_t b = ntok * w / nt, e = ntok * (w + 1) / nt;
+      constexpr int64_t kBlock = 64;  // tokens converted, then checked while cached
+      for (int64_t t = b; t < e; t += kBlock) {
+        const int64_t n = std::min(kBlock, e - t);
+        int16_t *g = store.data() + t * CHIMERA_DIM;
+        K.to_grid(tokens + t * CHIMERA_DIM, n * CHIMERA_DIM, g);
+        if (grid_in_range(g, n * CHIMERA_DIM)) continue;
+        for (int64_t u = 0; u < n; ++u)
+          if (!grid_in_range(g + u * CHIMERA_DIM, CHIMERA_DIM)) {
+            atomic_min(first_bad, t + u);
+            break;
+          }
+        return;
+      }
+    };
     std::vector<std::thread> th;
-    for (unsigned w = 0; w < nt; ++w)
-      th.emplace_back([&, w] {
-        const int64_t b = ntok * w / nt, e = ntok * (w + 1) / nt;
-        constexpr int64_t kBlock = 64;  // tokens converted, then checked while cached
-        for (int64_t t = b; t < e; t += kBlock) {
-          const int64_t n = std::min(kBlock, e - t);
-          int16_t *g = store.data() + t * CHIMERA_DIM;
-          K.to_grid(tokens + t * CHIMERA_DIM, n * CHIMERA_DIM, g);
-          if (grid_in_range(g, n * CHIMERA_DIM)) continue;
-          for (int64_t u = 0; u < n; ++u)
-            if (!grid_in_range(g + u * CHIMERA_DIM, CHIMERA_DIM)) {
-              atomic_min(first_bad, t + u);
-              break;
-            }
-          return;
+    th.reserve(nt);
+    {
+      // every started thread is joined, whatever happens after it starts
+      struct JoinAll {
+        std::vector<std::thread> &v;
+        ~JoinAll() {
+          for (auto &t : v)
+            if (t.joinable()) t.join();
         }
-      });
-    for (auto &t : th) t.join();
+      } join_all{th};
+      for (unsigned w = 0; w < nt; ++w) {
+        try {
+          th.emplace_back(slice, w);
+        } catch (...) {
+          slice(w);  // no thread available: this slice runs on the calling thread
+        }
+      }
+    }
     if (first_bad.load() < ntok)
       rc = fail(CHIMERA_E_INVAL, "full-precision token %lld has a value that is not finite or outside [-1, 1]",
                 (long long)first_bad.load());
@@ -528,7 +544,7 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
   } catch (const std::bad_alloc &) {
     rc = fail(CHIMERA_E_NOMEM, "full-precision store of %lld tokens", (long long)ntok);
   } catch (...) {
-    rc = fail(CHIMERA_E_NOMEM, "full-precision store: host threads unavailable");
+    rc = fail(CHIMERA_E_NOMEM, "full-precision store: host allocation failed");
   }
   idx->busy.store(0);
   return rc;

@@ -68,6 +68,12 @@ constexpr int kTokenPad = 64;
 void launch_round_queries(const void *Q, int q_dtype, int64_t nq, int Tq, int TQP, uint16_t *Qs,
                           hipStream_t s);
 
+// Squared-norm check of the nq*Tq query tokens (rounded onto the grid, grid
+// units): *first_bad = min token index with norm^2 >= lim2 (or non-finite);
+// *first_bad must be set to ~0 before.
+void launch_check_queries(const void *Q, int q_dtype, int64_t ntokens, double lim2, unsigned long long *first_bad,
+                          hipStream_t s);
+
 // Probe: S = Qs * cent^T on MFMA, top-nprobe per row.  rows = nq*TQP.
 // part: [nsplit][rows][pmax] u64 partial lists.  ST (optional): [nq][ncent][TQP] f32.
 struct ProbePlan {
@@ -168,6 +174,10 @@ struct chimera_index {
   int32_t *d_tok_doc = nullptr;
   uint16_t h_weights[16] = {0};
   int32_t h_cut[15] = {0};
+  // exact scores need every query token's L2 norm below this (see upload)
+  double q_norm_limit = 0.0;
+  bool check_queries = false;              // CHIMERA_CHECK_QUERIES=1 at load
+  unsigned long long *d_check = nullptr;  // the check's result word
   // scratch arena, grown on demand, ordered across streams by scratch_done
   void *scratch = nullptr;
   size_t scratch_bytes = 0;

@@ -44,6 +44,36 @@ void launch_round_queries(const void *Q, int q_dtype, int64_t nq, int Tq, int TQ
   hipLaunchKernelGGL(k_round_queries, dim3((unsigned)blocks), dim3(256), 0, s, Q, q_dtype, nq, Tq, TQP, Qs);
 }
 
+// Query check (on request): the squared L2 norm, in grid units, of every
+// query token as the search rounds it; *first_bad receives the lowest token
+// index (q * Tq + j) whose norm is not below the index's limit for exact
+// scores, or any non-finite value.  One wave per token.
+__global__ __launch_bounds__(256) void k_check_queries(const void *__restrict__ Q, int q_dtype, int64_t ntokens,
+                                                       double lim2, unsigned long long *__restrict__ first_bad) {
+  const int lane = lane_id();
+  for (int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); tok < ntokens; tok += (int64_t)gridDim.x * 4) {
+    double ss = 0.0;
+    for (int d = lane; d < 128; d += 64) {
+      const int64_t src = tok * 128 + d;
+      const float x = q_dtype == CHIMERA_F32 ? ((const float *)Q)[src]
+                                             : __uint_as_float((uint32_t)((const uint16_t *)Q)[src] << 16);
+      const double k = (double)__uint_as_float((uint32_t)grid_bf16_bits(x) << 16) * 2048.0;  // exact
+      ss += k * k;
+    }
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    if (lane == 0 && !(ss < lim2)) atomicMin(first_bad, (unsigned long long)tok);
+  }
+}
+
+void launch_check_queries(const void *Q, int q_dtype, int64_t ntokens, double lim2, unsigned long long *first_bad,
+                          hipStream_t s) {
+  int64_t blocks = (ntokens + 3) / 4;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) return;
+  hipLaunchKernelGGL(k_check_queries, dim3((unsigned)blocks), dim3(256), 0, s, Q, q_dtype, ntokens, lim2, first_bad);
+}
+
 // --------------------------------------------------------------- probe
 // Insert K into L (sorted descending), dropping the smallest.
 template <int P>

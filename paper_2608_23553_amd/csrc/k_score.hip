@@ -460,6 +460,13 @@ void launch_topk(const int32_t *fhat, const int32_t *cand_ids, const int32_t *n_
                  int32_t *ids, float *scores, hipStream_t s) {
   int kp = 1;
   while (kp < k) kp <<= 1;
+  // k up to 8192: 64 KiB of dynamic LDS beside the static state, above the
+  // default per-workgroup limit
+  static bool attr = [] {
+    return hipFuncSetAttribute((const void *)k_topk, hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024) ==
+           hipSuccess;
+  }();
+  (void)attr;
   hipLaunchKernelGGL(k_topk, dim3((unsigned)nq), dim3(TOPK_THREADS), (size_t)kp * 8, s, fhat, cand_ids, n_valid, ncand,
                      k, kp, ids, scores);
 }

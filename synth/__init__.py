@@ -61,6 +61,7 @@ def _load():
     lib.synth_centroids.restype = ctypes.POINTER(ctypes.c_int16)
     lib.synth_doc_lengths.argtypes = [P, ctypes.c_int64, ctypes.c_int64, P]
     lib.synth_doc_tokens.argtypes = [P, ctypes.c_int64, ctypes.c_int64, P, P, P, P, ctypes.c_int]
+    lib.synth_doc_tokens_ex.argtypes = [P, ctypes.c_int64, ctypes.c_int64, P, P, P, P, P, ctypes.c_int]
     lib.synth_docs_tokens.argtypes = [P, P, ctypes.c_int64, P, P, P, ctypes.c_int]
     lib.synth_queries.argtypes = [P, ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                   P, P, ctypes.c_int]
@@ -136,6 +137,24 @@ class Corpus:
         cl = np.empty(rows, dtype=np.int32)
         _lib.synth_doc_tokens(self._ctx, d0, d1, _ptr(off), _ptr(lens), _ptr(k), _ptr(cl), self.nthreads)
         return k, cl
+
+    def tokens_ex(self, d0: int = 0, d1: int | None = None, want_k: bool = True, want_bf16: bool = True,
+                  want_cluster: bool = True):
+        """Tokens of docs [d0, d1) in one generation: (k int16 [rows, dim],
+        bf16 bit patterns uint16 [rows, dim], cluster int32 [rows]); an output
+        not asked for is None."""
+        if d1 is None:
+            d1 = self.spec.ndocs
+        base = self.doc_off[d0]
+        rows = int(self.doc_off[d1] - base)
+        off = np.ascontiguousarray(self.doc_off[d0:d1] - base)
+        lens = np.ascontiguousarray(self.lengths[d0:d1])
+        k = np.empty((rows, self.dim), dtype=np.int16) if want_k else None
+        b = np.empty((rows, self.dim), dtype=np.uint16) if want_bf16 else None
+        cl = np.empty(rows, dtype=np.int32) if want_cluster else None
+        _lib.synth_doc_tokens_ex(self._ctx, d0, d1, _ptr(off), _ptr(lens), _ptr(k), _ptr(b), _ptr(cl),
+                                 self.nthreads)
+        return k, b, cl
 
     def docs_tokens(self, docs: np.ndarray):
         """Tokens of an arbitrary list of docs, concatenated in list order.

@@ -30,7 +30,12 @@ struct synth_ctx {
   int16_t *cent;  /* [ncent][dim] */
   double *zipf_cdf; /* [ncent], cumulative unnormalised weights (zipf only) */
   int32_t *perm;  /* [ncent] rank -> centroid id (zipf only) */
+  int32_t *zipf_guide; /* [ZIPF_GUIDE + 1]: entry j is the first rank whose
+                          cdf exceeds (j / ZIPF_GUIDE) of the total (zipf only) */
 };
+
+#define ZIPF_GUIDE 65536
+#define SYNTH_MAX_DIM 1024
 
 /* SplitMix64 output function. */
 static inline uint64_t sm_mix(uint64_t z) {
@@ -105,7 +110,8 @@ static void normalise_to_grid(const double *v, int dim, int16_t *out) {
 }
 
 synth_ctx *synth_create(const synth_cfg *cfg) {
-  if (!cfg || cfg->ncent <= 0 || cfg->dim <= 0 || (cfg->dim & 1) || cfg->ndocs < 0) return NULL;
+  if (!cfg || cfg->ncent <= 0 || cfg->dim <= 0 || (cfg->dim & 1) || cfg->dim > SYNTH_MAX_DIM || cfg->ndocs < 0)
+    return NULL;
   if (cfg->len_lo < 1 || cfg->len_hi < cfg->len_lo) return NULL;
   synth_ctx *ctx = (synth_ctx *)calloc(1, sizeof(synth_ctx));
   if (!ctx) return NULL;
@@ -127,11 +133,17 @@ synth_ctx *synth_create(const synth_cfg *cfg) {
   if (cfg->pop_kind == SYNTH_POP_ZIPF) {
     ctx->zipf_cdf = (double *)malloc((size_t)n * sizeof(double));
     ctx->perm = (int32_t *)malloc((size_t)n * sizeof(int32_t));
-    if (!ctx->zipf_cdf || !ctx->perm) { synth_free(ctx); return NULL; }
+    ctx->zipf_guide = (int32_t *)malloc((size_t)(ZIPF_GUIDE + 1) * sizeof(int32_t));
+    if (!ctx->zipf_cdf || !ctx->perm || !ctx->zipf_guide) { synth_free(ctx); return NULL; }
     double acc = 0.0;
     for (int r = 0; r < n; ++r) {
       acc += pow((double)(r + 1), -cfg->zipf_s);
       ctx->zipf_cdf[r] = acc;
+    }
+    for (int j = 0, r = 0; j <= ZIPF_GUIDE; ++j) {
+      const double x = ((double)j / (double)ZIPF_GUIDE) * acc;
+      while (r < n - 1 && !(ctx->zipf_cdf[r] > x)) ++r;
+      ctx->zipf_guide[j] = r;
     }
     for (int i = 0; i < n; ++i) ctx->perm[i] = i;
     uint64_t key = stream_key(cfg->seed, STREAM_PERM, 0);
@@ -151,6 +163,7 @@ void synth_free(synth_ctx *ctx) {
   free(ctx->cent);
   free(ctx->zipf_cdf);
   free(ctx->perm);
+  free(ctx->zipf_guide);
   free(ctx);
 }
 
@@ -180,77 +193,157 @@ void synth_doc_lengths(const synth_ctx *ctx, int64_t d0, int64_t d1, int32_t *ou
   for (int64_t d = d0; d < d1; ++d) out[d - d0] = doc_length(ctx, d);
 }
 
-static int32_t token_cluster(const synth_ctx *ctx, int64_t d, int64_t t) {
+/* First rank r with zipf_cdf[r] > x (the last rank if there is none),
+ * searched between lo and hi, which must bracket that rank. */
+static int zipf_search(const synth_ctx *ctx, double x, int lo, int hi) {
+  while (lo < hi) {
+    int mid = lo + (hi - lo) / 2;
+    if (ctx->zipf_cdf[mid] > x) hi = mid; else lo = mid + 1;
+  }
+  return lo;
+}
+
+static int32_t cluster_of(const synth_ctx *ctx, uint64_t key, int64_t t) {
   const synth_cfg *c = &ctx->cfg;
-  uint64_t key = stream_key(c->seed, STREAM_TOKCLUSTER, (uint64_t)d);
   double u = u01(key, (uint64_t)t);
   if (c->pop_kind == SYNTH_POP_ZIPF) {
     double x = u * ctx->zipf_cdf[c->ncent - 1];
-    int lo = 0, hi = c->ncent - 1; /* first rank r with cdf[r] > x */
-    while (lo < hi) {
-      int mid = lo + (hi - lo) / 2;
-      if (ctx->zipf_cdf[mid] > x) hi = mid; else lo = mid + 1;
-    }
-    return ctx->perm[lo];
+    /* u in [j/G, (j+1)/G) and rounding is monotone, so x lies between the
+     * guide's thresholds j and j+1 and the rank between their entries */
+    int j = (int)(u * (double)ZIPF_GUIDE);
+    if (j >= ZIPF_GUIDE) j = ZIPF_GUIDE - 1;
+    return ctx->perm[zipf_search(ctx, x, ctx->zipf_guide[j], ctx->zipf_guide[j + 1])];
   }
   int32_t k = (int32_t)(u * (double)c->ncent);
   return k >= c->ncent ? c->ncent - 1 : k;
 }
 
-/* Token t of doc d; v is 4 dim doubles of scratch. */
-static void gen_token(const synth_ctx *ctx, int64_t d, int64_t t, double *v, int16_t *out_k, int32_t *out_cl) {
+/* Per-thread scratch of a block of up to GEN_BLOCK tokens. */
+#define GEN_BLOCK 8
+typedef struct {
+  double a[GEN_BLOCK * SYNTH_MAX_DIM / 2], b[GEN_BLOCK * SYNTH_MAX_DIM / 2];
+  double r[GEN_BLOCK * SYNTH_MAX_DIM / 2], t[GEN_BLOCK * SYNTH_MAX_DIM / 2];
+  double z[GEN_BLOCK * SYNTH_MAX_DIM], v[GEN_BLOCK * SYNTH_MAX_DIM];
+  const int16_t *base[GEN_BLOCK];
+} gen_scratch;
+
+/* n (<= GEN_BLOCK) noisy unit vectors: token i is
+ * G(normalise(base[i] / 2^11 + sigma * z_i)), where z_i takes the normals of
+ * pairs pair0 + i * dim/2 .. of the stream key.  Outputs (each may be NULL):
+ * grid integers out_k [n][dim], bf16 bits out_bf16 [n][dim].
+ * The arithmetic is exactly that of the per-token recipe in synth.h (the
+ * same IEEE operations in the same order per token, no contraction); the
+ * loops run over the block so that they vectorise. */
+__attribute__((target_clones("arch=skylake-avx512", "arch=haswell", "default")))
+static void noisy_unit_block(gen_scratch *w, int n, int dim, uint64_t key, uint64_t pair0, double sigma,
+                             int16_t *out_k, uint16_t *out_bf16) {
+  const int np = n * dim / 2, nv = n * dim;
+  for (int p = 0; p < np; ++p) {
+    const uint64_t c = 2 * (pair0 + (uint64_t)p);
+    uint64_t x0 = synth_splitmix64_at(key, c), x1 = synth_splitmix64_at(key, c + 1);
+    w->a[p] = ((double)(x0 >> 11) + 0.5) * (1.0 / 9007199254740992.0);
+    w->b[p] = ((double)(x1 >> 11) + 0.5) * (1.0 / 9007199254740992.0);
+  }
+  synth_box_muller(w->a, w->b, w->r, w->t, w->z, np);
+  for (int i = 0; i < n; ++i) {
+    const int16_t *base = w->base[i];
+    double *v = w->v + (size_t)i * dim;
+    const double *z = w->z + (size_t)i * dim;
+    for (int d = 0; d < dim; ++d) v[d] = base[d] * (1.0 / 2048.0) + sigma * z[d]; /* exact scaling */
+  }
+  double ss[GEN_BLOCK], inv[GEN_BLOCK];
+  for (int i = 0; i < n; ++i) ss[i] = 0.0;
+  for (int d = 0; d < dim; ++d) /* each token's sum in dimension order */
+    for (int i = 0; i < n; ++i) ss[i] += w->v[(size_t)i * dim + d] * w->v[(size_t)i * dim + d];
+  for (int i = 0; i < n; ++i) inv[i] = ss[i] > 0.0 ? 1.0 / sqrt(ss[i]) : 0.0;
+  for (int i = 0; i < n; ++i) {
+    const double s = inv[i];
+    double *v = w->v + (size_t)i * dim;
+    for (int d = 0; d < dim; ++d) {
+      const double x = v[d] * s;
+      /* synth_to_grid without the branch: both roundings, then a select */
+      const double small = (x + 3298534883328.0) - 3298534883328.0;
+      uint64_t bits;
+      memcpy(&bits, &x, sizeof bits);
+      bits += ((uint64_t)1 << 44) - 1 + ((bits >> 45) & 1);
+      bits &= ~(((uint64_t)1 << 45) - 1);
+      double big;
+      memcpy(&big, &bits, sizeof big);
+      v[d] = fabs(x) < 0.0625 ? small : big;
+    }
+  }
+  if (out_k)
+    for (int e = 0; e < nv; ++e) out_k[e] = (int16_t)(w->v[e] * 2048.0); /* exact: a multiple of 2^-11 */
+  if (out_bf16)
+    for (int e = 0; e < nv; ++e) {
+      float f = (float)w->v[e]; /* exact: a bf16 value */
+      uint32_t u;
+      memcpy(&u, &f, sizeof u);
+      out_bf16[e] = (uint16_t)(u >> 16);
+    }
+}
+
+/* Tokens t0 .. t0+n-1 (n <= GEN_BLOCK) of doc d. */
+static void doc_token_block(const synth_ctx *ctx, gen_scratch *w, int64_t d, int64_t t0, int n, int16_t *out_k,
+                            uint16_t *out_bf16, int32_t *out_cl) {
   const synth_cfg *c = &ctx->cfg;
-  int dim = c->dim;
-  int32_t cl = token_cluster(ctx, d, t);
-  if (out_cl) *out_cl = cl;
-  if (!out_k) return;
-  const int16_t *cent = ctx->cent + (size_t)cl * dim;
-  uint64_t key = stream_key(c->seed, STREAM_TOKNOISE, (uint64_t)d);
-  double *z = v + dim;
-  normals(key, (uint64_t)t * (uint64_t)(dim / 2), dim / 2, z, v + 2 * dim);
-  for (int i = 0; i < dim; ++i) v[i] = cent[i] / 2048.0 + c->tok_sigma * z[i];
-  normalise_to_grid(v, dim, out_k);
+  const int dim = c->dim;
+  const uint64_t ckey = stream_key(c->seed, STREAM_TOKCLUSTER, (uint64_t)d);
+  for (int i = 0; i < n; ++i) {
+    int32_t cl = cluster_of(ctx, ckey, t0 + i);
+    if (out_cl) out_cl[i] = cl;
+    w->base[i] = ctx->cent + (size_t)cl * dim;
+  }
+  if (!out_k && !out_bf16) return;
+  const uint64_t key = stream_key(c->seed, STREAM_TOKNOISE, (uint64_t)d);
+  noisy_unit_block(w, n, dim, key, (uint64_t)t0 * (uint64_t)(dim / 2), c->tok_sigma, out_k, out_bf16);
+}
+
+/* All L tokens of doc d to rows starting at row. */
+static void gen_doc(const synth_ctx *ctx, gen_scratch *w, int64_t d, int32_t L, int64_t row, int16_t *out_k,
+                    uint16_t *out_bf16, int32_t *out_cl) {
+  const size_t dim = (size_t)ctx->cfg.dim;
+  for (int32_t t = 0; t < L; t += GEN_BLOCK) {
+    const int n = L - t < GEN_BLOCK ? L - t : GEN_BLOCK;
+    const int64_t r = row + t;
+    doc_token_block(ctx, w, d, t, n, out_k ? out_k + (size_t)r * dim : NULL,
+                    out_bf16 ? out_bf16 + (size_t)r * dim : NULL, out_cl ? out_cl + r : NULL);
+  }
+}
+
+void synth_doc_tokens_ex(const synth_ctx *ctx, int64_t d0, int64_t d1, const int64_t *tok_off,
+                         const int32_t *lens, int16_t *out_k, uint16_t *out_bf16, int32_t *out_cluster,
+                         int nthreads) {
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#endif
+#pragma omp parallel num_threads(nthreads)
+  {
+    gen_scratch *w = (gen_scratch *)malloc(sizeof(gen_scratch));
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t d = d0; d < d1; ++d)
+      gen_doc(ctx, w, d, lens[d - d0], tok_off[d - d0], out_k, out_bf16, out_cluster);
+    free(w);
+  }
 }
 
 void synth_doc_tokens(const synth_ctx *ctx, int64_t d0, int64_t d1, const int64_t *tok_off,
                       const int32_t *lens, int16_t *out_k, int32_t *out_cluster, int nthreads) {
-  int dim = ctx->cfg.dim;
-#ifdef _OPENMP
-  if (nthreads <= 0) nthreads = omp_get_max_threads();
-#endif
-#pragma omp parallel num_threads(nthreads)
-  {
-    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
-#pragma omp for schedule(dynamic, 64)
-    for (int64_t d = d0; d < d1; ++d) {
-      int64_t row = tok_off[d - d0];
-      int32_t L = lens[d - d0];
-      for (int32_t t = 0; t < L; ++t)
-        gen_token(ctx, d, t, v, out_k ? out_k + (size_t)(row + t) * dim : NULL,
-                  out_cluster ? out_cluster + row + t : NULL);
-    }
-    free(v);
-  }
+  synth_doc_tokens_ex(ctx, d0, d1, tok_off, lens, out_k, NULL, out_cluster, nthreads);
 }
 
 void synth_docs_tokens(const synth_ctx *ctx, const int64_t *docs, int64_t n, const int64_t *row_off,
                        int16_t *out_k, int32_t *out_cluster, int nthreads) {
-  int dim = ctx->cfg.dim;
 #ifdef _OPENMP
   if (nthreads <= 0) nthreads = omp_get_max_threads();
 #endif
 #pragma omp parallel num_threads(nthreads)
   {
-    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
+    gen_scratch *w = (gen_scratch *)malloc(sizeof(gen_scratch));
 #pragma omp for schedule(dynamic, 16)
-    for (int64_t i = 0; i < n; ++i) {
-      int64_t d = docs[i], row = row_off[i];
-      int32_t L = doc_length(ctx, d);
-      for (int32_t t = 0; t < L; ++t)
-        gen_token(ctx, d, t, v, out_k ? out_k + (size_t)(row + t) * dim : NULL,
-                  out_cluster ? out_cluster + row + t : NULL);
-    }
-    free(v);
+    for (int64_t i = 0; i < n; ++i)
+      gen_doc(ctx, w, docs[i], doc_length(ctx, docs[i]), row_off[i], out_k, NULL, out_cluster);
+    free(w);
   }
 }
 
@@ -264,8 +357,8 @@ void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_
 #endif
 #pragma omp parallel num_threads(nthreads)
   {
-    double *v = (double *)malloc((size_t)4 * dim * sizeof(double));
-    int16_t *src_tok = (int16_t *)malloc((size_t)dim * sizeof(int16_t));
+    gen_scratch *w = (gen_scratch *)malloc(sizeof(gen_scratch));
+    int16_t *src_tok = (int16_t *)malloc((size_t)GEN_BLOCK * dim * sizeof(int16_t));
 #pragma omp for schedule(dynamic, 4)
     for (int64_t q = q0; q < q1; ++q) {
       uint64_t skey = stream_key(qseed, STREAM_QSRC, (uint64_t)q);
@@ -274,15 +367,17 @@ void synth_queries(const synth_ctx *ctx, uint64_t query_seed, int64_t q0, int64_
       if (out_src) out_src[q - q0] = src;
       int32_t L = doc_length(ctx, src);
       uint64_t nkey = stream_key(qseed, STREAM_QNOISE, (uint64_t)q);
-      for (int32_t j = 0; j < Tq; ++j) {
-        gen_token(ctx, src, j % L, v, src_tok, NULL);
-        double *z = v + dim;
-        normals(nkey, (uint64_t)j * (uint64_t)(dim / 2), dim / 2, z, v + 2 * dim);
-        for (int i = 0; i < dim; ++i) v[i] = src_tok[i] / 2048.0 + c->q_sigma * z[i];
-        normalise_to_grid(v, dim, out_k + ((size_t)(q - q0) * Tq + j) * dim);
+      for (int32_t j0 = 0; j0 < Tq; j0 += GEN_BLOCK) {
+        const int n = Tq - j0 < GEN_BLOCK ? Tq - j0 : GEN_BLOCK;
+        /* query token j is the noised source token j mod L */
+        for (int i = 0; i < n; ++i)
+          doc_token_block(ctx, w, src, (j0 + i) % L, 1, src_tok + (size_t)i * dim, NULL, NULL);
+        for (int i = 0; i < n; ++i) w->base[i] = src_tok + (size_t)i * dim;
+        noisy_unit_block(w, n, dim, nkey, (uint64_t)j0 * (uint64_t)(dim / 2), c->q_sigma,
+                         out_k + ((size_t)(q - q0) * Tq + j0) * dim, NULL);
       }
     }
-    free(v);
+    free(w);
     free(src_tok);
   }
 }

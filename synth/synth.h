@@ -57,7 +57,7 @@ typedef struct synth_ctx synth_ctx;
 
 /* Builds the context: centroids, the Zipf table and the rank->id permutation.
  * Returns NULL on bad configuration or allocation failure. */
-synth_ctx *synth_create(const synth_cfg *cfg);
+synth_ctx *synth_create(const synth_cfg *cfg);  /* dim even and at most 1024 */
 void synth_free(synth_ctx *ctx);
 
 /* Centroids as grid integers, [ncent][dim]. The pointer is owned by ctx. */
@@ -74,6 +74,13 @@ void synth_doc_lengths(const synth_ctx *ctx, int64_t d0, int64_t d1, int32_t *ou
 void synth_doc_tokens(const synth_ctx *ctx, int64_t d0, int64_t d1,
                       const int64_t *tok_off, const int32_t *lens,
                       int16_t *out_k, int32_t *out_cluster, int nthreads);
+
+/* As synth_doc_tokens, with the components also (or only) as bf16 bit
+ * patterns out_bf16 [rows][dim] (every grid value is a bf16 value).  Any
+ * output may be NULL. */
+void synth_doc_tokens_ex(const synth_ctx *ctx, int64_t d0, int64_t d1, const int64_t *tok_off,
+                         const int32_t *lens, int16_t *out_k, uint16_t *out_bf16, int32_t *out_cluster,
+                         int nthreads);
 
 /* Queries [q0, q1) with Tq tokens each: out_k is [q1-q0][Tq][dim] int16,
  * out_src[q1-q0] the source document (may be NULL).  query_seed separates

@@ -1,9 +1,6 @@
 """GPU path against the CPU oracle, element by element (ids bit-exact,
 scores bit-exact: keys are exact on the value grid, so the 1e-3 relative
 tolerance is never needed).  Every call goes through the C ABI."""
-import functools
-import sys
-
 import numpy as np
 import pytest
 import torch
@@ -11,51 +8,9 @@ import torch
 import oracle
 import synth
 from paper_2608_23553_amd import ChimeraError, chimera
-from util_build import product_builder
+from util_gpu import check_search, q_tensor, say, setup
 
 pytestmark = pytest.mark.gpu
-
-
-def say(*a):
-    print("[gpu-parity]", *a, flush=True)
-    sys.stdout.flush()
-
-
-@functools.lru_cache(maxsize=None)
-def setup(name, ndocs=None, nbits=None):
-    w = synth.WORKLOADS[name]
-    if ndocs is not None:
-        w = w.scaled(ndocs=ndocs)
-    if nbits is not None:
-        w = w.scaled(nbits=nbits)
-    c = synth.Corpus(w.corpus_spec())
-    k, cl = c.tokens()
-    oi = oracle.OracleIndex(c.centroids_k, c.doc_off, cl, w.nbits, tok_k=k)
-    b = product_builder(c, w.nbits)
-    idx = b.upload(0)
-    return w, c, k, cl, oi, idx
-
-
-def q_tensor(qk, dtype):
-    if dtype == "f32":
-        return torch.from_numpy(synth.k_to_f32(qk)).cuda()
-    return torch.from_numpy(synth.k_to_bf16_bits(qk).view(np.int16)).cuda().view(torch.bfloat16)
-
-
-def check_search(idx, oi, qk, nprobe, ncand, k, dtype="bf16", label="", refine=False):
-    say("search", label, qk.shape, nprobe, ncand, k, dtype, "refine" if refine else "")
-    ids, scores = idx.search(q_tensor(qk, dtype), nprobe, ncand, k,
-                             refine=chimera.REFINE_TOKEN if refine else chimera.REFINE_CENTROID)
-    torch.cuda.synchronize()
-    ref = oi.search(qk, nprobe, ncand, k, refine=refine)
-    gi, gs = ids.cpu().numpy(), scores.cpu().numpy()
-    bad = np.nonzero((gi != ref["ids"]).any(axis=1))[0]
-    assert bad.size == 0, f"{label}: ids differ for queries {bad[:8]}: gpu {gi[bad[0]][:8]} oracle {ref['ids'][bad[0]][:8]}"
-    assert np.array_equal(gs, ref["scores"]), f"{label}: scores differ"
-    # the judge's bar (relative 1e-3) is implied by bit-exactness; keep the statement explicit
-    fin = np.isfinite(ref["scores"])
-    assert np.all(np.abs(gs[fin] - ref["scores"][fin]) <= 1e-3 * np.abs(ref["scores"][fin]))
-    return gi, gs, ref
 
 
 # ---------------------------------------------------------------- tiny

@@ -5,9 +5,13 @@ and the oracle's search on a few sampled queries.
 The oracle never holds the codes of the whole corpus here.  It keeps the
 assignment, its own quantiser (from a residual histogram accumulated over
 the same chunks the product builder reads) and the posting lists, and
-regenerates the tokens of a query's top-ncand documents to score them.  The
-stage functions are composed exactly as the oracle's own search composes
-them (pinned by test_search_composes_stage_definitions)."""
+regenerates the tokens of a query's top-ncand documents to score them
+(oracle.search_streamed, which composes the stage functions exactly as the
+oracle's own search does; pinned by test_search_composes_stage_definitions
+and test_sampled_oracle_equals_full_oracle)."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 import oracle
@@ -15,26 +19,43 @@ import synth
 from paper_2608_23553_amd import Builder
 
 
+def host_threads() -> int:
+    return int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 8)
+
+
+def hist_parallel(pool, nthreads, k, cl, cent_k):
+    """oracle.residual_hist of one chunk, split over threads (a sum of
+    per-slice histograms)."""
+    n = len(cl)
+    cuts = np.linspace(0, n, nthreads + 1).astype(np.int64)
+    parts = pool.map(lambda i: oracle.residual_hist(k[cuts[i]:cuts[i + 1]], cl[cuts[i]:cuts[i + 1]], cent_k),
+                     range(nthreads))
+    return np.sum(list(parts), axis=0)
+
+
 def build_both(w, nthreads=0, docs_per_chunk=50_000, say=print):
     """Product Builder and OracleIndex (without codes) for workload w."""
+    nthreads = nthreads or host_threads()
     c = synth.Corpus(w.corpus_spec(), nthreads=nthreads)
     b = Builder(synth.k_to_bf16_bits(c.centroids_k), w.nbits)
     hist = np.zeros(8193, dtype=np.int64)
     cid = np.empty(c.ntok, dtype=np.int32)
     nd = w.ndocs
-    for d0 in range(0, nd, docs_per_chunk):  # pass 1: residuals, histogram, assignment
-        d1 = min(nd, d0 + docs_per_chunk)
-        k, cl = c.tokens(d0, d1)
-        b.add_residuals(synth.k_to_bf16_bits(k), cl)
-        oracle.residual_hist(k, cl, c.centroids_k, hist)
-        cid[c.doc_off[d0]:c.doc_off[d1]] = cl
-        if d0 % (20 * docs_per_chunk) == 0:
-            say(f"pass 1: {d1}/{nd} docs")
+    with ThreadPoolExecutor(max_workers=nthreads) as pool:
+        for d0 in range(0, nd, docs_per_chunk):  # pass 1: residuals, histogram, assignment
+            d1 = min(nd, d0 + docs_per_chunk)
+            k, bf, cl = c.tokens_ex(d0, d1)
+            b.add_residuals(bf, cl)
+            hist += hist_parallel(pool, nthreads, k, cl, c.centroids_k)
+            cid[c.doc_off[d0]:c.doc_off[d1]] = cl
+            if d0 % (20 * docs_per_chunk) == 0:
+                say(f"pass 1: {d1}/{nd} docs")
     b.freeze()
+    b.reserve(nd, c.ntok)
     for d0 in range(0, nd, docs_per_chunk):  # pass 2: codes
         d1 = min(nd, d0 + docs_per_chunk)
-        k, cl = c.tokens(d0, d1)
-        b.add_docs(synth.k_to_bf16_bits(k), cl, c.lengths[d0:d1])
+        _, bf, cl = c.tokens_ex(d0, d1, want_k=False)
+        b.add_docs(bf, cl, c.lengths[d0:d1])
         if d0 % (20 * docs_per_chunk) == 0:
             say(f"pass 2: {d1}/{nd} docs")
     oi = oracle.OracleIndex(c.centroids_k, c.doc_off, cid, w.nbits, hist=hist, with_codes=False)
@@ -43,13 +64,6 @@ def build_both(w, nthreads=0, docs_per_chunk=50_000, say=print):
 
 def oracle_search_one(c, oi, q_k, nprobe, ncand, k):
     """The oracle's search of one query [Tq, dim], stage by stage."""
-    S = oracle.centroid_scores(q_k, c.centroids_k)
-    ci, ck = oracle.probe(S, nprobe)
-    docs, fp = oracle.partial_scores(S, ci, oi.ivf_off, oi.ivf_doc, oi.ndocs)
-    r, rk = oracle.topk(docs, fp, ncand)
-    tk, cl, begin = c.docs_tokens(r.astype(np.int64))
-    codes = oracle.encode(tk, cl, oi.cent_k, oi.cut_k, oi.nbits)
-    fh = oracle.doc_scores(S, q_k, oi.w_k, begin, c.lengths[r].astype(np.int32), cl, codes)
-    ids, keys = oracle.topk(r, fh, k)
-    return dict(cent_ids=ci, cent_keys=ck, cand=r, cand_keys=rk, ids=ids, keys=keys,
-                scores=oracle.keys_to_scores(keys))
+    def docs_tokens(ids):
+        return c.docs_tokens(ids)
+    return oracle.search_streamed(oi, q_k, nprobe, ncand, k, docs_tokens)
