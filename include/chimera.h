@@ -225,6 +225,25 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
                           int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
                           void *hip_stream);
 
+/* chimera_search for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same arguments, results and validation as chimera_search, but its
+ * scratch is a fixed device array of CHIMERA_NOALLOC_SCRATCH_MB MiB built
+ * into the library (one per GPU, reserved while the library's code is loaded
+ * on that GPU, until the process ends), so the call allocates no device or
+ * host memory.  The batch runs in as many sub-batches as that array needs.
+ * CHIMERA_E_UNSUPPORTED if a single query needs more scratch than the array
+ * holds (a query needs about 4 (ncent + 1) * 32 bytes of centroid scores
+ * plus 4 ndocs bytes of partial scores: about 70 MB at 262,144 centroids
+ * and 8.8M documents).  Every call on one GPU shares its array: calls that
+ * overlap on a GPU, from any index or stream, race and must be serialised
+ * by the caller.  The array keeps the last call's contents; each call
+ * clears what must start at zero (its histograms) itself.
+ * Stage timing (chimera_stage_times) does not record these calls. */
+#define CHIMERA_NOALLOC_SCRATCH_MB 256
+int chimera_search_noalloc(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                           int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream);
+
 /* ===================================================================== *
  * CPU-GPU collaborative scoring (Sec. 4, document scoring; Alg. 3).
  *

@@ -64,6 +64,7 @@ def lib():
         "chimera_index_info_get": ([P, P], INT),
         "chimera_search": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_search_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, P, P, P], INT),
+        "chimera_search_noalloc": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_probe": ([P, P, INT, I64, I32, I32, I32, P, P, P], INT),
         "chimera_candidates": ([P, P, INT, I64, I32, I32, I32, P, P, I64, P], INT),
         "chimera_prune": ([P, P, INT, I64, I32, I32, I32, I32, P, P, P, P], INT),

@@ -280,14 +280,23 @@ static int check_queries(chimera_index *idx, const void *Q, int q_dtype, int64_t
   return CHIMERA_OK;
 }
 
+// A caller-provided scratch region instead of the index's own arena (the
+// search that allocates nothing): nothing is allocated, no stage events are
+// recorded, and the sub-batches are sized to fit `bytes`.
+struct FixedScratch {
+  char *base = nullptr;
+  size_t bytes = 0;
+};
+
 static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int Tq, int nprobe, int ncand, int k,
-               Stop stop, Outs o, hipStream_t s, int refine = CHIMERA_REFINE_CENTROID) {
+               Stop stop, Outs o, hipStream_t s, int refine = CHIMERA_REFINE_CENTROID, FixedScratch fixed = {}) {
   const int TQP = Tq <= 32 ? 32 : 64;
+  const bool own = fixed.base == nullptr;
   if (idx->check_queries)
     if (int rc = check_queries(idx, Q, q_dtype, nq, Tq, s)) return rc;
   // sub-batch size: the largest that fits the scratch budget (carve_bytes
   // grows with nb, but not in proportion: the select's chunking depends on nb)
-  const size_t budget = scratch_budget();
+  const size_t budget = own ? scratch_budget() : fixed.bytes;
   int64_t lo = 1, hi = std::min<int64_t>(nq, 65535);
   while (lo < hi) {
     const int64_t mid = lo + (hi - lo + 1) / 2;
@@ -298,22 +307,37 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
   // equal sub-batches: the same number of passes, without a short last one
   const int64_t npass = (nq + B - 1) / B;
   B = (nq + npass - 1) / npass;
-  size_t need = carve_bytes(idx, B, TQP, nprobe, ncand, stop);
-  if (nq % B) need = std::max(need, carve_bytes(idx, nq % B, TQP, nprobe, ncand, stop));
-  int rc = ensure_scratch(idx, need);
-  if (rc) return rc;
-  if (idx->scratch_pending) CHIMERA_HIP(hipStreamWaitEvent(s, idx->scratch_done, 0));
-  // Every exit from here on, error returns included, marks the scratch as in
-  // use by the work queued on s, so a later call on another stream waits for
-  // that work before it reuses the scratch.
+  auto need_for = [&](int64_t b) {
+    size_t n = carve_bytes(idx, b, TQP, nprobe, ncand, stop);
+    if (nq % b) n = std::max(n, carve_bytes(idx, nq % b, TQP, nprobe, ncand, stop));
+    return n;
+  };
+  size_t need = need_for(B);
+  if (!own) {
+    while (need > fixed.bytes && B > 1) need = need_for(--B);
+    if (need > fixed.bytes)
+      return fail(CHIMERA_E_UNSUPPORTED, "one query of this search needs %zu bytes of scratch, more than the "
+                  "fixed scratch's %zu", need, fixed.bytes);
+  } else {
+    int rc = ensure_scratch(idx, need);
+    if (rc) return rc;
+    if (idx->scratch_pending) CHIMERA_HIP(hipStreamWaitEvent(s, idx->scratch_done, 0));
+  }
+  char *const scratch = own ? (char *)idx->scratch : fixed.base;
+  const size_t scratch_cap = own ? idx->scratch_bytes : fixed.bytes;
+  // Every exit from here on, error returns included, marks the index's
+  // scratch as in use by the work queued on s, so a later call on another
+  // stream waits for that work before it reuses the scratch.
   struct ScratchDone {
     chimera_index *idx;
     hipStream_t s;
+    bool on;
     ~ScratchDone() {
-      if (hipEventRecord(idx->scratch_done, s) == hipSuccess) idx->scratch_pending = true;
+      if (on && hipEventRecord(idx->scratch_done, s) == hipSuccess) idx->scratch_pending = true;
     }
-  } scratch_done_on_exit{idx, s};
-  const bool mark = stop == STOP_FULL;
+  } scratch_done_on_exit{idx, s, own};
+  const bool mark = stop == STOP_FULL && own;
+  int rc = CHIMERA_OK;
 
   std::vector<int64_t> host_counts;
   int64_t total_hits = 0;
@@ -322,13 +346,13 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     const int64_t nb = std::min<int64_t>(B, nq - q0);
     const int64_t rows = nb * TQP;
     const ProbePlan plan = plan_probe(rows, idx->ncent, nprobe);
-    Carve cv{(char *)idx->scratch};
+    Carve cv{scratch};
     uint16_t *Qs = cv.take<uint16_t>((size_t)rows * 128);
     uint64_t *part = cv.take<uint64_t>(probe_part_bytes(plan, rows) / 8);
     int32_t *ci = cv.take<int32_t>((size_t)rows * nprobe);
     int32_t *ck = cv.take<int32_t>((size_t)rows * nprobe);
     float *ST = stop >= STOP_FULL ? cv.take<float>((size_t)nb * (idx->ncent + 1) * TQP) : nullptr;
-    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     const size_t qbytes = (size_t)Tq * 128 * (q_dtype == CHIMERA_F32 ? 4 : 2);
     const void *Qb = (const char *)Q + (size_t)q0 * qbytes;
 
@@ -347,7 +371,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     }
     int32_t *fp = cv.take<int32_t>((size_t)nb * idx->ndocs);
     uint32_t *hist = cv.take<uint32_t>((size_t)nb * 4096);
-    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
     launch_fill_zero(hist, (size_t)nb * 4096 * 4, s);
     if (refine == CHIMERA_REFINE_TOKEN)
@@ -359,7 +383,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_CANDIDATES) {
       int64_t *cnt = cv.take<int64_t>((size_t)nb + 1);
-      if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+      if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
       launch_count_hits(fp, nb, idx->ndocs, cnt, s);
       std::vector<int64_t> hc(nb);
       CHIMERA_HIP(hipMemcpyAsync(hc.data(), cnt, nb * 8, hipMemcpyDeviceToHost, s));
@@ -381,10 +405,10 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     int32_t *candk = o.cand_keys ? o.cand_keys + q0 * ncand : cv.take<int32_t>((size_t)nb * ncand);
     int32_t *nval = o.n_valid ? o.n_valid + q0 : cv.take<int32_t>((size_t)nb);
     int32_t *fhat = stop >= STOP_FULL ? cv.take<int32_t>((size_t)nb * ncand) : nullptr;
-    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     stage_mark(idx, s, mark);
     char *selw = cv.take<char>(select_scratch_bytes(nb, idx->ndocs, ncand));
-    if (cv.off > idx->scratch_bytes) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+    if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     launch_select(fp, hist, nb, idx->ndocs, ncand, selw, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
@@ -466,9 +490,11 @@ int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, i
                                hip_stream);
 }
 
-int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
-                          int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
-                          void *hip_stream) {
+// Validation and set-up shared by the searches; `fixed` selects the fixed
+// scratch (chimera_search_noalloc).
+static int search_common(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                         int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
+                         void *hip_stream, bool fixed) {
   int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe, refine);
   if (rc) return rc;
   if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
@@ -481,13 +507,32 @@ int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_
   if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
   DeviceGuard dg(idx->device);
   if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  FixedScratch fs;
+  if (fixed) {
+    void *p = nullptr;
+    if ((rc = fixed_scratch(idx->device, &p))) return rc;
+    fs.base = (char *)p;
+    fs.bytes = kFixedScratchBytes - kFixedScratchGuard;
+  }
   int nc = (int)std::min<int64_t>(ncand, idx->ndocs);
   Outs o;
   o.ids = ids;
   o.scores = scores;
   return guarded([&] {
-    return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine);
+    return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine, fs);
   });
+}
+
+int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
+                          void *hip_stream) {
+  return search_common(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, k, refine, ids, scores, hip_stream, false);
+}
+
+int chimera_search_noalloc(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                           int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream) {
+  return search_common(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, k, CHIMERA_REFINE_CENTROID, ids, scores,
+                       hip_stream, true);
 }
 
 int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,

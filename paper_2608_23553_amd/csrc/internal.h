@@ -144,6 +144,14 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
                     const CollabOut &o);
 void collab_free(chimera_index *idx);
 
+// The fixed scratch of chimera_search_noalloc (noalloc.hip): its device
+// address on `device`, which must be current; looked up on the first call
+// per device and kept.
+constexpr size_t kFixedScratchBytes = (size_t)CHIMERA_NOALLOC_SCRATCH_MB << 20;
+// kept unused at the array's end, as the grown arena keeps 1/8 spare
+constexpr size_t kFixedScratchGuard = (size_t)1 << 20;
+int fixed_scratch(int device, void **ptr);
+
 // Final top-k: ids/scores [nq][k].
 void launch_topk(const int32_t *fhat, const int32_t *cand_ids, const int32_t *n_valid, int64_t nq, int ncand,
                  int k, int32_t *ids, float *scores, hipStream_t s);
