@@ -33,49 +33,94 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
   hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, s, (uint4 *)p, n16);
 }
 
-// Workgroup (query q, group g): the doc ranges [d0, d0 + R) of a contiguous
-// group of ranges, one after the other.  The state of a range lives in LDS,
-// so the atomics are LDS atomics and each document's state is written to HBM
-// once.  Every probed list (query token j, rank r) keeps a cursor in LDS
-// across the group's ranges: it is positioned once (by binary search, and
-// not at all for the first group) and then only moves forward, and a list
-// whose next document lies past the current range costs nothing there.  For
-// each rank r (in order, one barrier per rank) every list of that rank is
-// walked up to the range's end by one wave.  Query tokens that probe the same
-// centroid at the same rank share one walk of its list (on the Zipf-popular
-// corpora this halves the entries walked): one atomic OR of the group's token
-// mask tells which of them see the document for the first time.  The
-// workgroup then writes F' (or NO_HIT for documents outside S_Q) and adds the
-// range's histogram of the top 12 bits of the order key to the query's
-// histogram, the first pass of the refinement select.  Workgroup b runs on
-// XCD b % 8; with 8 or more queries all groups of query q run on XCD q % 8,
-// with fewer they spread over every XCD.
+// Workgroup (query q, group g): the document ranges [d0, d0 + R) of a
+// contiguous group of ranges, one after the other.  The state of a range
+// (per document: the mask of query tokens already credited, and F') lives in
+// LDS, so the updates are LDS atomics and each document's F' is written to
+// HBM once.  Query tokens that probe the same centroid at the same rank form
+// a group whose list is walked once, with the group's token mask and score
+// sum (on the Zipf-popular corpora this halves the entries walked).  Ranks
+// are applied in order, one barrier apart, so the first rank whose list
+// holds a document gives each token its maximum: one atomic OR of the
+// group's mask tells which tokens see the document for the first time.
+//
+// Every list's next entries wait in registers, loaded a range ahead:
+//  * a short list (a few entries per range, the usual case) belongs to one
+//    thread for the workgroup's lifetime, with a window of its next WIN
+//    entries;
+//  * a long list (more than WALK_LONG entries expected per range) belongs to
+//    one wave, with a window of its next 64 entries (one per lane);
+//  * a dense list (see dense_lists) is not walked: each thread applies it to
+//    the documents it owns from their 64-bit masks, loaded a range ahead.
+// At the start of a range the windows' entries inside it are copied into
+// per-rank buckets in LDS and the windows are refilled; the ranks then run
+// over the buckets, so they wait on no memory.  Only a list with more
+// entries in one range than its window holds goes on through memory, at its
+// rank.  The workgroup then writes F' (or NO_HIT for documents outside S_Q)
+// and adds the range's histogram of the top 12 bits of the order key to the
+// query's histogram, the first pass of the refinement select.  Workgroup b
+// runs on XCD b % 8: with 8 or more queries all groups of query q run on XCD
+// q % 8, with fewer they spread over every XCD.
 constexpr int WALK_THREADS = 512;
+constexpr int WALK_WAVES = WALK_THREADS / 64;
+constexpr int WALK_LONG = 4;        // expected entries per range above which a list belongs to a wave
+constexpr int WALK_LONG_SLOTS = 4;  // lists per wave
+constexpr int WALK_MAX_LONG = WALK_LONG_SLOTS * WALK_WAVES;  // beyond that, lists stay with threads
+constexpr int WALK_MAX_LISTS = 4 * WALK_THREADS;              // Tq * nprobe
+constexpr int WALK_SHORT_ENTRIES = 4096;                      // short-list windows in all
+constexpr int WALK_BUCKET = WALK_SHORT_ENTRIES + WALK_MAX_LONG * 64;
+constexpr int WALK_DOC_BITS = 13;   // a bucket entry: list index << 13 | document in the range
 
+// Window of a thread's short list: WIN = 8, 4 or 2 entries as a thread owns
+// 1, 2 or 4 lists (WALK_SHORT_ENTRIES in all).
+template <int LPT>
+constexpr int walk_win() {
+  return WALK_SHORT_ENTRIES / (LPT * WALK_THREADS);
+}
 
+// Documents per range: 8192 with 32-bit token masks and fewer than 512
+// lists, else 4096; 2048 with 64-bit masks.
+static inline int walk_range_docs(int TQP, int nprobe, int Tq) {
+  return TQP == 32 ? (nprobe * Tq < 512 ? 8192 : 4096) : 2048;
+}
 
-// Walk state of one probed list (rank r, query token j): entries
-// ivf_doc[beg .. beg + len), cursor pos and the document at the cursor
-// (INT32_MAX past the end, or when another token's list stands for this one).
-// The query tokens whose rank-r centroid is the same form a group: the list
-// of the group's first token is walked once for all of them, with the
-// group's token mask and the sum of their scores S[j][c].
-// A group whose centroid has a dense list (see dense_lists) is not walked:
-// dslot is the centroid's bit in the documents' dense masks (-1 otherwise).
-template <typename MaskT>
-struct WalkList {
+// LDS cursor of a wave's list: entries ivf_doc[beg .. beg + len), pos the
+// first entry not yet credited; t its list index r * Tq + j.
+struct LongList {
   int64_t beg;
-  MaskT mask;
-  int32_t pos, len, next, gsum, dslot;
+  int32_t pos, len, t, rank, n, off;  // n, off: entries in the current range and their bucket offset
 };
 
+// Register state of a thread's short list: entries lp[0 .. len); e[i] holds
+// lp[pos0 + i] for i < avail; e[0 .. c) are credited.  rank < 0: no list.
+template <int WIN>
+struct ShortList {
+  const int32_t *lp;
+  int32_t len, pos0, avail, c, rank, t;
+  int32_t e[WIN];
+};
+
+// Credits the group (gmask, gsum) to document v of the range: the tokens of
+// the group not yet seen there add their scores.
+template <typename MaskT>
+__device__ __forceinline__ void credit(MaskT *smask, int32_t *sfp, int v, MaskT gmask, int32_t gsum,
+                                       const int32_t *keys) {
+  const MaskT fresh = gmask & ~atomicOr(&smask[v], gmask);
+  if (fresh == gmask) {
+    atomicAdd(&sfp[v], gsum);
+  } else if (fresh) {
+    int32_t add = 0;
+    for (MaskT m = fresh; m; m &= m - 1) add += keys[__builtin_ctzll((unsigned long long)m)];
+    atomicAdd(&sfp[v], add);
+  }
+}
+
 // One wave walks a list from pos up to the range's end d1, U blocks of 64
-// entries per step (entries past d1 are read but not applied; the next range
-// reads them again); leaves pos at the first entry >= d1 and next = its doc.
+// entries per step; leaves pos at the first entry >= d1.
 template <int U, typename MaskT>
 __device__ __forceinline__ void walk_list(const int32_t *__restrict__ list, int32_t len, int64_t d0, int64_t d1,
                                           MaskT gmask, int32_t gsum, const int32_t *keys, int lane, MaskT *smask,
-                                          int32_t *sfp, int32_t &pos, int32_t &next) {
+                                          int32_t *sfp, int32_t &pos) {
   bool done = false;
   while (!done) {
     int32_t doc[U];
@@ -87,22 +132,10 @@ __device__ __forceinline__ void walk_list(const int32_t *__restrict__ list, int3
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool in = doc[u] < d1;
-      if (in) {
-        const int v = (int)(doc[u] - d0);
-        const MaskT fresh = gmask & ~atomicOr(&smask[v], gmask);  // tokens for which this is the first hit
-        if (fresh == gmask) {
-          atomicAdd(&sfp[v], gsum);
-        } else if (fresh) {
-          int32_t add = 0;
-          for (MaskT m = fresh; m; m &= m - 1) add += keys[__builtin_ctzll((unsigned long long)m)];
-          atomicAdd(&sfp[v], add);
-        }
-      }
+      if (in && !done) credit(smask, sfp, (int)(doc[u] - d0), gmask, gsum, keys);
       const unsigned long long out = __ballot(!in);  // lanes at or past the range's end
       if (out && !done) {
-        const int first = __ffsll((long long)out) - 1;
-        next = __shfl(doc[u], first, 64);
-        pos += 64 * u + first;
+        pos += 64 * u + (__ffsll((long long)out) - 1);
         done = true;
       }
     }
@@ -110,24 +143,80 @@ __device__ __forceinline__ void walk_list(const int32_t *__restrict__ list, int3
   }
 }
 
-template <typename MaskT, int R>
+// Entries lp[pos .. pos + n) of a window, every load issued (indices past
+// the list read its last entry and are not used), so each range issues the
+// same loads.
+template <int N>
+__device__ __forceinline__ void load_window(const int32_t *lp, int32_t pos, int32_t len, int32_t (&e)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) e[i] = lp[min(pos + i, len - 1)];
+}
+
+// Byte offsets of the walk's LDS arrays (each 16-byte aligned).
+struct WalkLds {
+  size_t smask, sfp, bucket, ll, lmask, lsum, skey, scid, dset, dcount, bcnt, bbase, dgm, dgs, dlist, dls, nlong,
+      total;
+};
+__host__ __device__ inline WalkLds walk_lds_layout(int R, int mask_bytes, int nprobe, int Tq) {
+  const size_t nl = (size_t)nprobe * Tq;
+  WalkLds L;
+  size_t o = 0;
+  auto take = [&o](size_t bytes) {
+    const size_t at = o;
+    o += (bytes + 15) / 16 * 16;
+    return at;
+  };
+  L.smask = take((size_t)R * mask_bytes);
+  L.sfp = take((size_t)R * 4);
+  L.bucket = take((size_t)WALK_BUCKET * 4);
+  L.ll = take(WALK_MAX_LONG * sizeof(LongList));
+  L.lmask = take(nl * mask_bytes);
+  L.lsum = take(nl * 4);
+  L.skey = take(nl * 4);
+  L.scid = take(nl * 4);
+  L.dset = take((size_t)nprobe * 8);
+  L.dcount = take((size_t)nprobe * 4);
+  L.bcnt = take((size_t)nprobe * 4);
+  L.bbase = take((size_t)nprobe * 4);
+  L.dgm = take((size_t)kMaxDense * mask_bytes);
+  L.dgs = take((size_t)kMaxDense * 4);
+  L.dlist = take(nl);
+  L.dls = take(nl);
+  L.nlong = take(4);
+  L.total = o;
+  return L;
+}
+
+template <typename MaskT, int R, int LPT>
 __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, int64_t nq, int Tq, int TQP,
     int nprobe, const int64_t *__restrict__ ivf_off, const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
     int ndense, const int8_t *__restrict__ dense_slot, const uint64_t *__restrict__ doc_dense, int nranges, int G,
     int M, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
   constexpr int DPT = R / WALK_THREADS;  // documents of a range each thread owns in the dense phase
+  constexpr int WIN = walk_win<LPT>();
   static_assert(R * sizeof(MaskT) >= SEL_BINS * 4, "the histogram reuses the mask array");
+  static_assert(R <= (1 << WALK_DOC_BITS), "a bucket entry holds the document in 13 bits");
   extern __shared__ __align__(16) unsigned char walk_lds[];
-  MaskT *smask = (MaskT *)walk_lds;                        // [R]
-  int32_t *sfp = (int32_t *)(smask + R);                     // [R]
-  WalkList<MaskT> *L = (WalkList<MaskT> *)(sfp + R);         // [nprobe][Tq]
-  int32_t *skey = (int32_t *)(L + nprobe * Tq);              // [nprobe][Tq] S[j][c] keys
-  int32_t *scid = skey + nprobe * Tq;                        // [nprobe][Tq] centroid ids
-  uint64_t *dset = (uint64_t *)(scid + nprobe * Tq);         // [nprobe] dense slots probed at each rank
-  int32_t *dcount = (int32_t *)(dset + nprobe);              // [nprobe] dense groups per rank
-  int8_t *dtab = (int8_t *)(dcount + nprobe);                // [kMaxDense] slot -> first token, current rank
-  int8_t *dlist = dtab + kMaxDense;                          // [nprobe][Tq] first tokens of the dense groups
+  const int nl = nprobe * Tq;
+  const WalkLds lay = walk_lds_layout(R, (int)sizeof(MaskT), nprobe, Tq);
+  MaskT *smask = (MaskT *)(walk_lds + lay.smask);        // [R] tokens already credited, per document
+  int32_t *sfp = (int32_t *)(walk_lds + lay.sfp);        // [R] F' accumulators
+  uint32_t *bucket = (uint32_t *)(walk_lds + lay.bucket);  // [WALK_BUCKET] the range's entries, by rank
+  LongList *LL = (LongList *)(walk_lds + lay.ll);        // [WALK_MAX_LONG]
+  MaskT *lmask = (MaskT *)(walk_lds + lay.lmask);        // [nl] group token masks
+  int32_t *lsum = (int32_t *)(walk_lds + lay.lsum);      // [nl] group score sums
+  int32_t *skey = (int32_t *)(walk_lds + lay.skey);      // [nl] S[j][c] keys, index r * Tq + j
+  int32_t *scid = (int32_t *)(walk_lds + lay.scid);      // [nl] centroid ids
+  uint64_t *dset = (uint64_t *)(walk_lds + lay.dset);    // [nprobe] dense slots probed at each rank
+  int32_t *dcount = (int32_t *)(walk_lds + lay.dcount);  // [nprobe] dense groups per rank
+  int32_t *bcnt = (int32_t *)(walk_lds + lay.bcnt);      // [nprobe] bucket entries per rank
+  int32_t *bbase = (int32_t *)(walk_lds + lay.bbase);    // [nprobe] first bucket entry of each rank
+  MaskT *dgm = (MaskT *)(walk_lds + lay.dgm);            // [kMaxDense] slot -> group mask, current rank
+  int32_t *dgs = (int32_t *)(walk_lds + lay.dgs);        // [kMaxDense] slot -> group score sum, current rank
+  int8_t *dlist = (int8_t *)(walk_lds + lay.dlist);      // [nl] first tokens of the dense groups, per rank
+  int8_t *dls = (int8_t *)(walk_lds + lay.dls);          // [nl] their dense slots
+  int32_t *nlong = (int32_t *)(walk_lds + lay.nlong);    // wave-owned lists
   // workgroup b runs on XCD b % 8: with 8 or more queries, the groups of
   // query q run on XCD q % 8; fewer queries spread over every XCD
   const int b = blockIdx.x;
@@ -137,7 +226,7 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   const int rg0 = g * M, rg1 = min(nranges, rg0 + M);
   if (rg0 >= rg1) return;  // uniform, before any barrier
   const int64_t dstart = (int64_t)rg0 * R;
-  const int nl = nprobe * Tq;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int t = threadIdx.x; t < nl; t += WALK_THREADS) {
     const int r = t / Tq, j = t - r * Tq;
     const int64_t e = (q * TQP + j) * nprobe + r;
@@ -148,50 +237,93 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     dcount[r] = 0;
     dset[r] = 0;
   }
+  if (threadIdx.x == 0) *nlong = 0;
   __syncthreads();
-  for (int t = threadIdx.x; t < nl; t += WALK_THREADS) {
+  // classify list t = threadIdx.x + WALK_THREADS * i: group head or not,
+  // dense, long or short; a short list stays with this thread (slot i)
+  ShortList<WIN> S[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int t = threadIdx.x + WALK_THREADS * i;
+    S[i].rank = -1;
+    S[i].avail = 0;
+    S[i].lp = ivf_doc;  // a readable entry for slots without a list
+    S[i].len = 1;
+    S[i].pos0 = 0;
+    S[i].c = 0;
+    if (t >= nl) continue;
     const int r = t / Tq, j = t - r * Tq;
     const int32_t c = scid[t];
-    WalkList<MaskT> w;
-    w.beg = 0;
-    w.pos = 0;
-    w.len = 0;
-    w.mask = 0;
-    w.gsum = 0;
-    w.dslot = -1;
     // one pass over the rank's centroids: is j the group's first token, and
     // the group's mask and score sum
     bool head = (uint32_t)c < (uint32_t)ncent;
     MaskT gm = 0;
     int32_t gs = 0;
-    for (int i = 0; i < Tq; ++i) {
-      const bool same = scid[r * Tq + i] == c;
-      head = head && !(same && i < j);
-      gm |= same ? (MaskT)1 << i : (MaskT)0;
-      gs += same ? skey[r * Tq + i] : 0;
+    for (int u = 0; u < Tq; ++u) {
+      const bool same = scid[r * Tq + u] == c;
+      head = head && !(same && u < j);
+      gm |= same ? (MaskT)1 << u : (MaskT)0;
+      gs += same ? skey[r * Tq + u] : 0;
     }
-    if (head && ndense > 0 && dense_slot[c] >= 0) {
+    lmask[t] = gm;
+    lsum[t] = gs;
+    if (!head) continue;
+    if (ndense > 0 && dense_slot[c] >= 0) {
       // a dense list: applied from the documents' masks, never walked
-      dlist[r * Tq + atomicAdd(&dcount[r], 1)] = (int8_t)j;
+      const int k = atomicAdd(&dcount[r], 1);
+      dlist[r * Tq + k] = (int8_t)j;
+      dls[r * Tq + k] = dense_slot[c];
       atomicOr((unsigned long long *)&dset[r], 1ull << dense_slot[c]);
-      w.mask = gm;
-      w.gsum = gs;
-      w.dslot = dense_slot[c];
-      head = false;
+      continue;
     }
-    if (head) {
-      w.mask = gm;
-      w.gsum = gs;
-      const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
-      const int64_t p = dstart > 0 ? lower_bound_i32(ivf_doc, beg, end, dstart) : beg;
-      w.beg = beg;
-      w.len = (int32_t)(end - beg);
-      w.pos = (int32_t)(p - beg);
+    const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
+    const int64_t p = dstart > 0 ? lower_bound_i32(ivf_doc, beg, end, dstart) : beg;
+    const int32_t len = (int32_t)(end - beg), pos = (int32_t)(p - beg);
+    if (pos >= len) continue;  // nothing left in the group's documents
+    if ((int64_t)(len - pos) * R > (int64_t)WALK_LONG * (ndocs - dstart)) {
+      const int k = atomicAdd(nlong, 1);
+      if (k < WALK_MAX_LONG) {
+        LongList w;
+        w.beg = beg;
+        w.pos = pos;
+        w.len = len;
+        w.t = t;
+        w.rank = r;
+        LL[k] = w;
+        continue;
+      }
     }
-    w.next = w.pos < w.len ? ivf_doc[w.beg + w.pos] : INT32_MAX;
-    L[t] = w;
+    S[i].lp = ivf_doc + beg;
+    S[i].len = len;
+    S[i].pos0 = pos;
+    S[i].c = 0;
+    S[i].rank = r;
+    S[i].t = t;
+    S[i].avail = min(WIN, len - pos);
+    load_window(S[i].lp, pos, len, S[i].e);
   }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = WALK_THREADS / 64;
+  __syncthreads();
+  // the wave's lists and their windows: slot i is list wave + WALK_WAVES * i
+  const int nlw = min(*nlong, WALK_MAX_LONG);
+  // (lane l holds entry pos + l, loaded as is: lanes past the list's end hold
+  // its last entry and are masked where the window is read)
+  int32_t lw[WALK_LONG_SLOTS];
+#pragma unroll
+  for (int i = 0; i < WALK_LONG_SLOTS; ++i) {
+    const int k = wave + WALK_WAVES * i;
+    if (k < nlw) {
+      const LongList w = LL[k];
+      lw[i] = ivf_doc[w.beg + min(w.pos + lane, w.len - 1)];
+    }
+  }
+  // dense-list masks of the documents this thread owns (tid + WALK_THREADS * i),
+  // loaded at the end of the previous range
+  uint64_t dm[DPT];
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) {
+    const int64_t v = dstart + threadIdx.x + WALK_THREADS * i;
+    dm[i] = ndense > 0 && v < ndocs ? doc_dense[v] : 0;
+  }
   for (int rg = rg0; rg < rg1; ++rg) {
     const int64_t d0 = (int64_t)rg * R;
     const int64_t d1 = min(ndocs, d0 + R);
@@ -200,69 +332,174 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
       smask[v] = 0;
       sfp[v] = 0;
     }
-    // dense-list masks of the documents this thread owns: tid + WALK_THREADS * i
-    uint64_t dm[DPT];
+    for (int r = threadIdx.x; r < nprobe; r += WALK_THREADS) bcnt[r] = 0;
+    __syncthreads();  // the range is cleared; the previous range's reads are done
+
+    // the windows' entries inside the range: count them per rank and reserve
+    // their places in the rank's bucket
+    int snew[LPT], soff[LPT];
+    bool sovf[LPT];
 #pragma unroll
-    for (int i = 0; i < DPT; ++i) {
-      const int v = threadIdx.x + WALK_THREADS * i;
-      dm[i] = ndense > 0 && v < nd ? doc_dense[d0 + v] : 0;
+    for (int i = 0; i < LPT; ++i) {
+      snew[i] = 0;
+      soff[i] = 0;
+      sovf[i] = false;
+      if (S[i].avail == 0) continue;
+      int mt = 0;
+#pragma unroll
+      for (int u = 0; u < WIN; ++u) mt += (u < S[i].avail && S[i].e[u] < d1) ? 1 : 0;
+      snew[i] = mt - S[i].c;
+      sovf[i] = mt == S[i].avail && S[i].pos0 + S[i].avail < S[i].len;
+      if (snew[i] > 0) soff[i] = atomicAdd(&bcnt[S[i].rank], snew[i]);
     }
-    __syncthreads();  // the lists are set up; the previous range's reads are done
+#pragma unroll
+    for (int i = 0; i < WALK_LONG_SLOTS; ++i) {
+      const int k = wave + WALK_WAVES * i;
+      if (k >= nlw) continue;  // wave-uniform
+      const LongList w = LL[k];
+      const int n = __popcll(__ballot(w.pos + lane < w.len && lw[i] < d1));
+      if (lane == 0) {
+        LL[k].n = n;
+        if (n > 0) LL[k].off = atomicAdd(&bcnt[LL[k].rank], n);
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {  // bucket base of each rank: exclusive prefix sum (nprobe <= 64)
+      const int x = lane < nprobe ? bcnt[lane] : 0;
+      int incl = x;
+#pragma unroll
+      for (int dd = 1; dd < 64; dd <<= 1) {
+        const int y = __shfl_up(incl, dd, 64);
+        if (lane >= dd) incl += y;
+      }
+      if (lane < nprobe) bbase[lane] = incl - x;
+    }
+    __syncthreads();
+    // copy the entries into the buckets, then move every window forward;
+    // the refills are needed a range later
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      if (S[i].avail == 0) continue;
+      if (snew[i] > 0) {
+        uint32_t *bk = bucket + bbase[S[i].rank] + soff[i] - S[i].c;
+#pragma unroll
+        for (int u = 0; u < WIN; ++u)
+          if (u >= S[i].c && u < S[i].c + snew[i])
+            bk[u] = (uint32_t)S[i].t << WALK_DOC_BITS | (uint32_t)(S[i].e[u] - d0);
+      }
+      S[i].c += snew[i];
+    }
+#pragma unroll
+    for (int i = 0; i < WALK_LONG_SLOTS; ++i) {
+      const int k = wave + WALK_WAVES * i;
+      if (k >= nlw) continue;  // wave-uniform
+      const LongList w = LL[k];
+      const int n = w.n;
+      if (n == 0) continue;
+      if (lane < n) bucket[bbase[w.rank] + w.off + lane] = (uint32_t)w.t << WALK_DOC_BITS | (uint32_t)(lw[i] - d0);
+      if (n < 64 && lane == 0) LL[k].pos = w.pos + n;  // a full window goes on through memory at its rank
+    }
+    __syncthreads();  // the buckets are complete
 
     for (int r = 0; r < nprobe; ++r) {
       const int ndg = dcount[r];
       if (threadIdx.x < ndg) {  // slot table of rank r; read after the barrier below
-        const int j = dlist[r * Tq + threadIdx.x];
-        dtab[L[r * Tq + j].dslot] = (int8_t)j;
+        const int gi = r * Tq + dlist[r * Tq + threadIdx.x], sl = dls[r * Tq + threadIdx.x];
+        dgm[sl] = lmask[gi];
+        dgs[sl] = lsum[gi];
       }
-      // list j of rank r is always walked by wave j % nwaves
-      for (int j = wave; j < Tq; j += nwaves) {
-        WalkList<MaskT> *w = &L[r * Tq + j];
-        if (w->next >= d1) continue;  // wave-uniform: nothing of this list in the range
-        const MaskT gmask = w->mask;
-        const int32_t gsum = w->gsum, len = w->len;
-        const int32_t *list = ivf_doc + w->beg;
-        int32_t pos = w->pos, next = INT32_MAX;
-        // lists expected to hold more than 64 entries per range keep 8 blocks
-        // of 64 entries in flight per step, others one
-        if ((int64_t)len * R > 64 * ndocs)
-          walk_list<8>(list, len, d0, d1, gmask, gsum, skey + r * Tq, lane, smask, sfp, pos, next);
-        else
-          walk_list<1>(list, len, d0, d1, gmask, gsum, skey + r * Tq, lane, smask, sfp, pos, next);
-        if (lane == 0) {
-          w->pos = pos;
-          w->next = next;
+      const int32_t *keys = skey + r * Tq;
+      // the rank's bucket, spread over every thread
+      const int e1 = bbase[r] + bcnt[r];
+      for (int e = bbase[r] + threadIdx.x; e < e1; e += WALK_THREADS) {
+        const uint32_t x = bucket[e];
+        const int t = (int)(x >> WALK_DOC_BITS);
+        credit(smask, sfp, (int)(x & ((1u << WALK_DOC_BITS) - 1)), lmask[t], lsum[t], keys);
+      }
+      // lists with more entries in the range than their window held
+#pragma unroll
+      for (int i = 0; i < LPT; ++i) {
+        if (!sovf[i] || S[i].rank != r) continue;
+        int32_t p = S[i].pos0 + S[i].avail;
+        const MaskT gm = lmask[S[i].t];
+        const int32_t gs = lsum[S[i].t];
+        while (p < S[i].len) {
+          const int32_t d = S[i].lp[p];
+          if (d >= d1) break;
+          credit(smask, sfp, (int)(d - d0), gm, gs, keys);
+          ++p;
         }
+        S[i].pos0 = p;
+        S[i].c = 0;
+      }
+#pragma unroll
+      for (int i = 0; i < WALK_LONG_SLOTS; ++i) {
+        const int k = wave + WALK_WAVES * i;
+        if (k >= nlw) continue;  // wave-uniform
+        const LongList w = LL[k];
+        if (w.rank != r || w.n != 64) continue;
+        int32_t pos = w.pos + 64;
+        walk_list<8>(ivf_doc + w.beg, w.len, d0, d1, lmask[w.t], lsum[w.t], keys, lane, smask, sfp, pos);
+        if (lane == 0) LL[k].pos = pos;
       }
       if (ndg > 0) {  // uniform
         // dense lists of rank r: each thread applies them to the documents it
-        // owns from their masks, without atomics (the sparse lists are done)
+        // owns from their masks, without atomics (the other lists are done)
         __syncthreads();
-        const uint64_t S = dset[r];
+        // the groups of one rank hold disjoint tokens, so a document's hits
+        // add up to one token mask and one score sum
+        const uint64_t Sd = dset[r];
 #pragma unroll
         for (int i = 0; i < DPT; ++i) {
-          uint64_t hits = dm[i] & S;
+          uint64_t hits = dm[i] & Sd;
           if (!hits) continue;
-          const int v = threadIdx.x + WALK_THREADS * i;
-          MaskT cur = smask[v];
-          int32_t add = 0;
+          MaskT nb = 0;
+          int32_t sall = 0;
           do {
-            const WalkList<MaskT> &g = L[r * Tq + dtab[__builtin_ctzll(hits)]];
+            const int sl = __builtin_ctzll(hits);
             hits &= hits - 1;
-            const MaskT gmask = g.mask;
-            const MaskT fresh = gmask & ~cur;
-            cur |= fresh;
-            if (fresh == gmask) {
-              add += g.gsum;
-            } else {
-              for (MaskT m = fresh; m; m &= m - 1) add += skey[r * Tq + __builtin_ctzll((unsigned long long)m)];
-            }
+            nb |= dgm[sl];
+            sall += dgs[sl];
           } while (hits);
-          smask[v] = cur;
+          const int v = threadIdx.x + WALK_THREADS * i;
+          const MaskT cur = smask[v];
+          const MaskT fresh = nb & ~cur;
+          if (!fresh) continue;
+          smask[v] = cur | fresh;
+          int32_t add = sall;
+          if (fresh != nb) {
+            add = 0;
+            for (MaskT m = fresh; m; m &= m - 1) add += keys[__builtin_ctzll((unsigned long long)m)];
+          }
           sfp[v] += add;
         }
       }
       __syncthreads();  // rank r's LDS updates complete before rank r+1's
+    }
+    // the next range's inputs, loaded now and first read a range from now:
+    // every window at its list's new position (its lines are cached), and
+    // the dense masks
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      S[i].pos0 += S[i].c;
+      S[i].c = 0;
+      S[i].avail = S[i].rank < 0 ? 0 : min(WIN, S[i].len - S[i].pos0);
+      load_window(S[i].lp, S[i].pos0, S[i].len, S[i].e);
+    }
+#pragma unroll
+    for (int i = 0; i < WALK_LONG_SLOTS; ++i) {
+      const int k = wave + WALK_WAVES * i;
+      if (k < nlw) {  // wave-uniform
+        const LongList w = LL[k];
+        lw[i] = ivf_doc[w.beg + min(w.pos + lane, w.len - 1)];
+      }
+    }
+    if (rg + 1 < rg1) {
+#pragma unroll
+      for (int i = 0; i < DPT; ++i) {
+        const int64_t v = d1 + threadIdx.x + WALK_THREADS * i;
+        dm[i] = ndense > 0 && v < ndocs ? doc_dense[v] : 0;
+      }
     }
     for (int v = threadIdx.x; v < nd; v += WALK_THREADS)
       if (smask[v] == 0) sfp[v] = NO_HIT;
@@ -284,20 +521,12 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   }
 }
 
-// Documents per range: 8192 with 32-bit token masks, except when a query
-// walks 512 lists or more; then, as with 64-bit masks, 4096, which lets two
-// workgroups share a compute unit and hide each other's waits (measured: the
-// list setup and the per-rank barriers weigh more with many lists, the
-// per-range work with few).
-static int walk_range_docs(int TQP, int nprobe, int Tq) { return TQP == 32 && nprobe * Tq < 512 ? 8192 : 4096; }
-
 size_t walk_lds_bytes(int TQP, int nprobe, int Tq) {
-  const size_t mask = TQP == 32 ? 4 : 8, R = (size_t)walk_range_docs(TQP, nprobe, Tq);
-  const size_t list = TQP == 32 ? sizeof(WalkList<uint32_t>) : sizeof(WalkList<unsigned long long>);
-  return R * (mask + 4) + (size_t)nprobe * Tq * (list + 9) + (size_t)nprobe * 12 + kMaxDense;
+  if ((size_t)nprobe * Tq > (size_t)WALK_MAX_LISTS) return SIZE_MAX;
+  return walk_lds_layout(walk_range_docs(TQP, nprobe, Tq), TQP == 32 ? 4 : 8, nprobe, Tq).total;
 }
 
-template <typename MaskT, int R>
+template <typename MaskT, int R, int LPT>
 static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                           const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
                           const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
@@ -311,28 +540,46 @@ static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int
   if (blocks == 0 || nranges == 0) return;
   const size_t lds = walk_lds_bytes(TQP, nprobe, Tq);
   static bool attr = [] {
-    return hipFuncSetAttribute((const void *)k_cand_walk<MaskT, R>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    return hipFuncSetAttribute((const void *)k_cand_walk<MaskT, R, LPT>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                160 * 1024) == hipSuccess;
   }();
   (void)attr;
-  hipLaunchKernelGGL((k_cand_walk<MaskT, R>), dim3((unsigned)blocks), dim3(WALK_THREADS), lds, s, cent_ids, cent_keys,
-                     nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense, dense_slot, doc_dense, nranges,
-                     G, M, fp, hist);
+  hipLaunchKernelGGL((k_cand_walk<MaskT, R, LPT>), dim3((unsigned)blocks), dim3(WALK_THREADS), lds, s, cent_ids,
+                     cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense, dense_slot, doc_dense,
+                     nranges, G, M, fp, hist);
+}
+
+template <typename MaskT, int R>
+static void launch_walk_r(int lpt, const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP,
+                          int nprobe, const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent,
+                          int ndense, const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp,
+                          uint32_t *hist, hipStream_t s) {
+  if (lpt <= 1)
+    launch_walk_t<MaskT, R, 1>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
+                               dense_slot, doc_dense, fp, hist, s);
+  else if (lpt <= 2)
+    launch_walk_t<MaskT, R, 2>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
+                               dense_slot, doc_dense, fp, hist, s);
+  else
+    launch_walk_t<MaskT, R, 4>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
+                               dense_slot, doc_dense, fp, hist, s);
 }
 
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
                       const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
                       hipStream_t s) {
-  if (TQP == 32 && walk_range_docs(TQP, nprobe, Tq) == 8192)
-    launch_walk_t<uint32_t, 8192>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                                  dense_slot, doc_dense, fp, hist, s);
+  const int lpt = (nprobe * Tq + WALK_THREADS - 1) / WALK_THREADS;  // at most 4 (walk_lds_bytes)
+  const int R = walk_range_docs(TQP, nprobe, Tq);
+  if (TQP == 32 && R == 8192)
+    launch_walk_r<uint32_t, 8192>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
+                                  ndense, dense_slot, doc_dense, fp, hist, s);
   else if (TQP == 32)
-    launch_walk_t<uint32_t, 4096>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                                  dense_slot, doc_dense, fp, hist, s);
+    launch_walk_r<uint32_t, 4096>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
+                                  ndense, dense_slot, doc_dense, fp, hist, s);
   else
-    launch_walk_t<unsigned long long, 4096>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
-                                            ndense, dense_slot, doc_dense, fp, hist, s);
+    launch_walk_r<unsigned long long, 2048>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs,
+                                            ncent, ndense, dense_slot, doc_dense, fp, hist, s);
 }
 
 // ------------------------------------------------------- block helpers
