@@ -803,6 +803,11 @@ struct SelState {
 };
 constexpr int SPLIT_THREADS = 256;
 
+// Documents per chunk of the split select: a multiple of 16, so that chunks
+// start 16-byte aligned within an F' row.
+__host__ __device__ inline int64_t sel_chunk_docs(int64_t ndocs, int P) { return ((ndocs + P - 1) / P + 15) / 16 * 16; }
+
+
 // Per query: bin of bits 31..20 from the walk's histogram; clears the
 // histograms of the next passes.
 __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_first(const uint32_t *__restrict__ hist1, int ncand,
@@ -842,7 +847,7 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_hist(const int32_t *__res
   const uint32_t prefix = st[q].prefix;
   for (int i = threadIdx.x; i < (1 << BITS); i += SPLIT_THREADS) h[i] = 0;
   __syncthreads();
-  const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
+  const int64_t per = sel_chunk_docs(ndocs, P), v0 = min(ndocs, c * per), v1 = min(ndocs, v0 + per);
   const int32_t *f = fp + q * ndocs;
   for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += SPLIT_THREADS * SEL_UNROLL) {
     int32_t x[SEL_UNROLL];
@@ -899,7 +904,7 @@ constexpr int SEL_LAST_ITEMS = 16;  // contiguous F' entries per thread and step
 constexpr uint32_t SEL_NO_LIST = 0xFFFFFFFFu;
 
 __host__ __device__ inline int sel_list_cap(int64_t ndocs, int P, int ncand) {
-  const int64_t per = (ndocs + P - 1) / P;
+  const int64_t per = sel_chunk_docs(ndocs, P);
   return (int)std::min<int64_t>(per, 4 * ((int64_t)ncand / P) + 1024);
 }
 
@@ -920,17 +925,31 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__res
   for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) h[i] = 0;
   if (threadIdx.x == 0) s_above = 0;
   __syncthreads();
-  const int64_t per = (ndocs + P - 1) / P, v0 = c * per, v1 = min(ndocs, v0 + per);
+  const int64_t per = sel_chunk_docs(ndocs, P), v0 = min(ndocs, c * per), v1 = min(ndocs, v0 + per);
   const int32_t *f = fp + q * ndocs;
   int2 *L = clist + ((int64_t)q * P + c) * cap;
   uint32_t above = 0;
   long long nlist = 0;  // uniform
   const int64_t step = (int64_t)SPLIT_THREADS * SEL_LAST_ITEMS;
+  // 16-byte loads where the row allows it (every F' row starts 16-byte
+  // aligned when ndocs is a multiple of 4, and chunks start at multiples of 16)
+  const bool vec = ((uintptr_t)f & 15) == 0 && (v0 & 3) == 0;
   for (int64_t vb = v0; vb < v1; vb += step) {
     const int64_t vt = vb + (int64_t)threadIdx.x * SEL_LAST_ITEMS;
     int32_t x[SEL_LAST_ITEMS];
+    if (vec && vt + SEL_LAST_ITEMS <= v1) {
 #pragma unroll
-    for (int i = 0; i < SEL_LAST_ITEMS; ++i) x[i] = vt + i < v1 ? f[vt + i] : NO_HIT;
+      for (int i = 0; i < SEL_LAST_ITEMS; i += 4) {
+        const int4 y = *(const int4 *)(f + vt + i);
+        x[i] = y.x;
+        x[i + 1] = y.y;
+        x[i + 2] = y.z;
+        x[i + 3] = y.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < SEL_LAST_ITEMS; ++i) x[i] = vt + i < v1 ? f[vt + i] : NO_HIT;
+    }
     int flags = 0;
 #pragma unroll
     for (int i = 0; i < SEL_LAST_ITEMS; ++i) {
@@ -1050,7 +1069,7 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__re
   const uint32_t nl = clen[q * P + c];
   const bool from_list = nl != SEL_NO_LIST;  // uniform
   const int2 *L = clist + (q * P + c) * (int64_t)cap;
-  const int64_t per = (ndocs + P - 1) / P, vb = c * per, ve = min(ndocs, vb + per);
+  const int64_t per = sel_chunk_docs(ndocs, P), vb = min(ndocs, c * per), ve = min(ndocs, vb + per);
   const int64_t b0 = from_list ? 0 : vb, b1 = from_list ? (int64_t)nl : ve;
   const int32_t *f = fp + q * ndocs;
   const int64_t step = (int64_t)SPLIT_THREADS * SEL_ITEMS;
