@@ -359,7 +359,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     stage_mark(idx, s, mark);
     launch_round_queries(Qb, q_dtype, nb, Tq, TQP, Qs, s);
     stage_mark(idx, s, mark);
-    launch_probe(Qs, rows, TQP, idx->d_cent, idx->ncent, plan, part, ST, s);
+    launch_probe(Qs, rows, TQP, idx->d_cent, idx->ncent, plan, nprobe, part, ST, s);
     launch_probe_merge(part, nb, Tq, TQP, plan, nprobe, ci, ck, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PROBE) {

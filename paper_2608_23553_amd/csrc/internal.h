@@ -78,11 +78,12 @@ void launch_check_queries(const void *Q, int q_dtype, int64_t ntokens, double li
 // part: [nsplit][rows][pmax] u64 partial lists.  ST (optional): [nq][ncent][TQP] f32.
 struct ProbePlan {
   int pmax = 0, nsplit = 0, tiles_per_split = 0;
+  int sample = 0, s_nsplit = 0, s_tiles_per_split = 0;  // centroid sample for the row bounds (0: none)
 };
 ProbePlan plan_probe(int64_t rows, int ncent, int nprobe);
 size_t probe_part_bytes(const ProbePlan &p, int64_t rows);
 void launch_probe(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent,
-                  const ProbePlan &p, uint64_t *part, float *ST, hipStream_t s);
+                  const ProbePlan &p, int nprobe, uint64_t *part, float *ST, hipStream_t s);
 // Merge partial lists into cent_ids/cent_keys [nq][TQP][nprobe] (rows j < Tq).
 void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const ProbePlan &p, int nprobe,
                         int32_t *cent_ids, int32_t *cent_keys, hipStream_t s);

@@ -156,11 +156,15 @@ __device__ __forceinline__ void fold_tile(uint64_t (&L)[P], uint64_t (&K)[16]) {
 // in at once through sorting networks (lists of 4 to 16); lists of 4 or 8
 // switch, once a lane has seen 128 * PMAX keys and entries have become rare,
 // to inserting keys one by one where they beat the list's last, as lists of
-// 32 and 64 do throughout.
-template <int PMAX, int TQP, bool WRITE_ST>
+// 32 and 64 do throughout.  With TAU, tau[row] is a lower bound on the row's
+// nprobe-th best key (from a sample of the centroids): keys below it can
+// never be selected and are dropped before they reach a list, so keys are
+// inserted one by one, and rarely.
+template <int PMAX, int TQP, bool WRITE_ST, bool TAU>
 __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, const uint16_t *__restrict__ cent,
                                                int ncent, int tiles_per_split, int64_t rows,
-                                               uint64_t *__restrict__ part, float *__restrict__ ST) {
+                                               uint64_t *__restrict__ part, float *__restrict__ ST,
+                                               const uint64_t *__restrict__ tau) {
   __shared__ uint64_t lds[3][32][PMAX];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 31, h = lane >> 5;
@@ -176,6 +180,7 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
   uint64_t L[PMAX];
 #pragma unroll
   for (int i = 0; i < PMAX; ++i) L[i] = 0;  // every real key is > 0
+  const uint64_t tr = TAU ? tau[qrow] : 0;
 
   const int ntiles = (ncent + 31) >> 5;
   const int t0 = split * tiles_per_split;
@@ -215,7 +220,7 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
       }
     }
     // wave-uniform; lists of 16 stay on the networks throughout (measured faster)
-    const bool network = PMAX == 16 || (PMAX <= 8 && 16 * ((t - t0 - wave) / 4 + 1) <= 128 * PMAX);
+    const bool network = !TAU && (PMAX == 16 || (PMAX <= 8 && 16 * ((t - t0 - wave) / 4 + 1) <= 128 * PMAX));
     if constexpr (PMAX <= 16) {
       if (network) {
         uint64_t K[16];
@@ -235,7 +240,7 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
         const int c = cbase + 8 * (v >> 2) + (v & 3);
         if (c < ncent) {
           const uint64_t K = pack_key(to_key(acc[v]), (uint32_t)c);
-          if (K > L[PMAX - 1]) insert_desc<PMAX>(L, K);
+          if (K >= tr && K > L[PMAX - 1]) insert_desc<PMAX>(L, K);
         }
       }
     }
@@ -264,52 +269,116 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
   }
 }
 
-ProbePlan plan_probe(int64_t rows, int ncent, int nprobe) {
-  ProbePlan p;
-  p.pmax = nprobe <= 4 ? 4 : nprobe <= 8 ? 8 : nprobe <= 16 ? 16 : nprobe <= 32 ? 32 : 64;
+// Splits of the centroid tiles: ~2048 workgroups, at least 4 tiles (one per
+// wave) per split, at most 512 splits (the merge folds every split's list).
+static void plan_splits(int64_t rows, int ncent, int &nsplit, int &tiles_per_split) {
   const int ntiles = (ncent + 31) / 32;
   const int64_t ncb = rows / 32;
-  // aim at ~2048 workgroups, at least 4 tiles (one per wave) per split, and
-  // at most 512 splits (the merge folds every split's list)
   int64_t want = std::min<int64_t>(512, (2048 + ncb - 1) / ncb);
   int64_t maxsplit = (ntiles + 3) / 4;
   int64_t ns = want < 1 ? 1 : want;
   if (ns > maxsplit) ns = maxsplit;
   if (ns > 65535) ns = 65535;
-  p.tiles_per_split = (int)((ntiles + ns - 1) / ns);
-  p.nsplit = (ntiles + p.tiles_per_split - 1) / p.tiles_per_split;
+  tiles_per_split = (int)((ntiles + ns - 1) / ns);
+  nsplit = (ntiles + tiles_per_split - 1) / tiles_per_split;
+}
+
+ProbePlan plan_probe(int64_t rows, int ncent, int nprobe) {
+  ProbePlan p;
+  p.pmax = nprobe <= 4 ? 4 : nprobe <= 8 ? 8 : nprobe <= 16 ? 16 : nprobe <= 32 ? 32 : 64;
+  plan_splits(rows, ncent, p.nsplit, p.tiles_per_split);
+  // with many centroids, the first 1/16 of them first give every row a lower
+  // bound on its nprobe-th best key
+  p.sample = ncent >= 65536 ? (ncent / 16 + 31) / 32 * 32 : 0;
+  if (p.sample) plan_splits(rows, p.sample, p.s_nsplit, p.s_tiles_per_split);
   return p;
 }
 
-size_t probe_part_bytes(const ProbePlan &p, int64_t rows) { return (size_t)p.nsplit * rows * p.pmax * 8; }
+size_t probe_part_bytes(const ProbePlan &p, int64_t rows) {
+  const int64_t ns = std::max(p.nsplit, p.sample ? p.s_nsplit : 0);
+  return (size_t)ns * rows * p.pmax * 8 + (p.sample ? (size_t)rows * 8 : 0);
+}
+
+// Per row (one wave each): the nprobe-th best key over the partial lists of
+// nsplit splits, folded as k_probe_merge folds them.
+template <int PMAX>
+__global__ __launch_bounds__(256) void k_probe_tau(const uint64_t *__restrict__ part, int64_t rows, int nsplit,
+                                                   int nprobe, uint64_t *__restrict__ tau) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  uint64_t L[PMAX];
+#pragma unroll
+  for (int i = 0; i < PMAX; ++i) L[i] = 0;
+  for (int sp = lane; sp < nsplit; sp += 64) {
+    const uint64_t *src = part + ((int64_t)sp * rows + row) * PMAX;
+    for (int i = 0; i < PMAX; ++i) {
+      const uint64_t K = src[i];
+      if (K <= L[PMAX - 1]) break;
+      insert_desc<PMAX>(L, K);
+    }
+  }
+  uint64_t best = 0;
+  for (int r = 0; r < nprobe; ++r) {
+    best = L[0];
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const uint64_t o = shfl_xor_u64(best, m);
+      best = o > best ? o : best;
+    }
+    if (L[0] == best) {  // keys are unique: one lane owns the winner
+#pragma unroll
+      for (int i = 0; i < PMAX - 1; ++i) L[i] = L[i + 1];
+      L[PMAX - 1] = 0;
+    }
+  }
+  if (lane == 0) tau[row] = best;
+}
 
 template <int P, int TQP>
 static void launch_probe_t(const uint16_t *Qs, int64_t rows, const uint16_t *cent, int ncent, const ProbePlan &p,
-                           uint64_t *part, float *ST, hipStream_t s) {
+                           int nprobe, uint64_t *part, float *ST, hipStream_t s) {
+  uint64_t *tau = nullptr;
+  if (p.sample) {
+    // the sample's lists, then each row's bound
+    const int64_t ns = std::max(p.nsplit, p.s_nsplit);
+    tau = part + (size_t)ns * rows * P;
+    hipLaunchKernelGGL((k_probe<P, TQP, false, false>), dim3((unsigned)(rows / 32), (unsigned)p.s_nsplit), dim3(256),
+                       0, s, Qs, cent, p.sample, p.s_tiles_per_split, rows, part, (float *)nullptr,
+                       (const uint64_t *)nullptr);
+    hipLaunchKernelGGL((k_probe_tau<P>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, part, rows, p.s_nsplit,
+                       nprobe, tau);
+  }
   dim3 grid((unsigned)(rows / 32), (unsigned)p.nsplit);
-  if (ST)
-    hipLaunchKernelGGL((k_probe<P, TQP, true>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows, part,
-                       ST);
+  if (ST && tau)
+    hipLaunchKernelGGL((k_probe<P, TQP, true, true>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows,
+                       part, ST, (const uint64_t *)tau);
+  else if (ST)
+    hipLaunchKernelGGL((k_probe<P, TQP, true, false>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows,
+                       part, ST, (const uint64_t *)nullptr);
+  else if (tau)
+    hipLaunchKernelGGL((k_probe<P, TQP, false, true>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows,
+                       part, ST, (const uint64_t *)tau);
   else
-    hipLaunchKernelGGL((k_probe<P, TQP, false>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split, rows, part,
-                       ST);
+    hipLaunchKernelGGL((k_probe<P, TQP, false, false>), grid, dim3(256), 0, s, Qs, cent, ncent, p.tiles_per_split,
+                       rows, part, ST, (const uint64_t *)nullptr);
 }
 
 template <int P>
 static void launch_probe_p(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent,
-                           const ProbePlan &p, uint64_t *part, float *ST, hipStream_t s) {
-  if (TQP == 32) launch_probe_t<P, 32>(Qs, rows, cent, ncent, p, part, ST, s);
-  else launch_probe_t<P, 64>(Qs, rows, cent, ncent, p, part, ST, s);
+                           const ProbePlan &p, int nprobe, uint64_t *part, float *ST, hipStream_t s) {
+  if (TQP == 32) launch_probe_t<P, 32>(Qs, rows, cent, ncent, p, nprobe, part, ST, s);
+  else launch_probe_t<P, 64>(Qs, rows, cent, ncent, p, nprobe, part, ST, s);
 }
 
 void launch_probe(const uint16_t *Qs, int64_t rows, int TQP, const uint16_t *cent, int ncent, const ProbePlan &p,
-                  uint64_t *part, float *ST, hipStream_t s) {
+                  int nprobe, uint64_t *part, float *ST, hipStream_t s) {
   switch (p.pmax) {
-    case 4: launch_probe_p<4>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    case 8: launch_probe_p<8>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    case 16: launch_probe_p<16>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    case 32: launch_probe_p<32>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
-    default: launch_probe_p<64>(Qs, rows, TQP, cent, ncent, p, part, ST, s); break;
+    case 4: launch_probe_p<4>(Qs, rows, TQP, cent, ncent, p, nprobe, part, ST, s); break;
+    case 8: launch_probe_p<8>(Qs, rows, TQP, cent, ncent, p, nprobe, part, ST, s); break;
+    case 16: launch_probe_p<16>(Qs, rows, TQP, cent, ncent, p, nprobe, part, ST, s); break;
+    case 32: launch_probe_p<32>(Qs, rows, TQP, cent, ncent, p, nprobe, part, ST, s); break;
+    default: launch_probe_p<64>(Qs, rows, TQP, cent, ncent, p, nprobe, part, ST, s); break;
   }
 }
 
