@@ -154,8 +154,7 @@ __device__ __forceinline__ void load_window(const int32_t *lp, int32_t pos, int3
 
 // Byte offsets of the walk's LDS arrays (each 16-byte aligned).
 struct WalkLds {
-  size_t smask, sfp, bucket, ll, lmask, lsum, skey, scid, dset, dcount, bcnt, bbase, dgm, dgs, dlist, dls, nlong,
-      total;
+  size_t smask, sfp, bucket, ll, lmask, lsum, skey, scid, dcount, bcnt, bbase, dgm, dgs, dls, nlong, total;
 };
 __host__ __device__ inline WalkLds walk_lds_layout(int R, int mask_bytes, int nprobe, int Tq) {
   const size_t nl = (size_t)nprobe * Tq;
@@ -174,13 +173,11 @@ __host__ __device__ inline WalkLds walk_lds_layout(int R, int mask_bytes, int np
   L.lsum = take(nl * 4);
   L.skey = take(nl * 4);
   L.scid = take(nl * 4);
-  L.dset = take((size_t)nprobe * 8);
   L.dcount = take((size_t)nprobe * 4);
   L.bcnt = take((size_t)nprobe * 4);
   L.bbase = take((size_t)nprobe * 4);
-  L.dgm = take((size_t)kMaxDense * mask_bytes);
-  L.dgs = take((size_t)kMaxDense * 4);
-  L.dlist = take(nl);
+  L.dgm = take(nl * mask_bytes);
+  L.dgs = take(nl * 4);
   L.dls = take(nl);
   L.nlong = take(4);
   L.total = o;
@@ -208,14 +205,13 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
   int32_t *lsum = (int32_t *)(walk_lds + lay.lsum);      // [nl] group score sums
   int32_t *skey = (int32_t *)(walk_lds + lay.skey);      // [nl] S[j][c] keys, index r * Tq + j
   int32_t *scid = (int32_t *)(walk_lds + lay.scid);      // [nl] centroid ids
-  uint64_t *dset = (uint64_t *)(walk_lds + lay.dset);    // [nprobe] dense slots probed at each rank
   int32_t *dcount = (int32_t *)(walk_lds + lay.dcount);  // [nprobe] dense groups per rank
   int32_t *bcnt = (int32_t *)(walk_lds + lay.bcnt);      // [nprobe] bucket entries per rank
   int32_t *bbase = (int32_t *)(walk_lds + lay.bbase);    // [nprobe] first bucket entry of each rank
-  MaskT *dgm = (MaskT *)(walk_lds + lay.dgm);            // [kMaxDense] slot -> group mask, current rank
-  int32_t *dgs = (int32_t *)(walk_lds + lay.dgs);        // [kMaxDense] slot -> group score sum, current rank
-  int8_t *dlist = (int8_t *)(walk_lds + lay.dlist);      // [nl] first tokens of the dense groups, per rank
-  int8_t *dls = (int8_t *)(walk_lds + lay.dls);          // [nl] their dense slots
+  // the dense groups of rank r: k < dcount[r] at r * Tq + k
+  MaskT *dgm = (MaskT *)(walk_lds + lay.dgm);            // [nl] token masks
+  int32_t *dgs = (int32_t *)(walk_lds + lay.dgs);        // [nl] score sums
+  int8_t *dls = (int8_t *)(walk_lds + lay.dls);          // [nl] dense slots
   int32_t *nlong = (int32_t *)(walk_lds + lay.nlong);    // wave-owned lists
   // workgroup b runs on XCD b % 8: with 8 or more queries, the groups of
   // query q run on XCD q % 8; fewer queries spread over every XCD
@@ -233,10 +229,7 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     scid[t] = cent_ids[e];
     skey[t] = cent_keys[e];
   }
-  for (int r = threadIdx.x; r < nprobe; r += WALK_THREADS) {
-    dcount[r] = 0;
-    dset[r] = 0;
-  }
+  for (int r = threadIdx.x; r < nprobe; r += WALK_THREADS) dcount[r] = 0;
   if (threadIdx.x == 0) *nlong = 0;
   __syncthreads();
   // classify list t = threadIdx.x + WALK_THREADS * i: group head or not,
@@ -271,9 +264,9 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     if (ndense > 0 && dense_slot[c] >= 0) {
       // a dense list: applied from the documents' masks, never walked
       const int k = atomicAdd(&dcount[r], 1);
-      dlist[r * Tq + k] = (int8_t)j;
       dls[r * Tq + k] = dense_slot[c];
-      atomicOr((unsigned long long *)&dset[r], 1ull << dense_slot[c]);
+      dgm[r * Tq + k] = gm;
+      dgs[r * Tq + k] = gs;
       continue;
     }
     const int64_t beg = ivf_off[c], end = ivf_off[c + 1];
@@ -403,11 +396,6 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
 
     for (int r = 0; r < nprobe; ++r) {
       const int ndg = dcount[r];
-      if (threadIdx.x < ndg) {  // slot table of rank r; read after the barrier below
-        const int gi = r * Tq + dlist[r * Tq + threadIdx.x], sl = dls[r * Tq + threadIdx.x];
-        dgm[sl] = lmask[gi];
-        dgs[sl] = lsum[gi];
-      }
       const int32_t *keys = skey + r * Tq;
       // the rank's bucket, spread over every thread
       const int e1 = bbase[r] + bcnt[r];
@@ -444,30 +432,39 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
       }
       if (ndg > 0) {  // uniform
         // dense lists of rank r: each thread applies them to the documents it
-        // owns from their masks, without atomics (the other lists are done)
-        __syncthreads();
-        // the groups of one rank hold disjoint tokens, so a document's hits
-        // add up to one token mask and one score sum
-        const uint64_t Sd = dset[r];
+        // owns from their masks, without atomics, once the other lists are
+        // done.  The groups of one rank hold disjoint tokens, so a document's
+        // hits add up to one token mask and one score sum; the groups are
+        // visited in the same order by every lane.
+        MaskT nb[DPT];
+        int32_t sall[DPT];
 #pragma unroll
         for (int i = 0; i < DPT; ++i) {
-          uint64_t hits = dm[i] & Sd;
-          if (!hits) continue;
-          MaskT nb = 0;
-          int32_t sall = 0;
-          do {
-            const int sl = __builtin_ctzll(hits);
-            hits &= hits - 1;
-            nb |= dgm[sl];
-            sall += dgs[sl];
-          } while (hits);
+          nb[i] = 0;
+          sall[i] = 0;
+        }
+        for (int k = 0; k < ndg; ++k) {
+          const int sl = dls[r * Tq + k];
+          const MaskT gm = dgm[r * Tq + k];
+          const int32_t gs = dgs[r * Tq + k];
+#pragma unroll
+          for (int i = 0; i < DPT; ++i) {
+            const bool hit = (dm[i] >> sl) & 1;
+            nb[i] |= hit ? gm : (MaskT)0;
+            sall[i] += hit ? gs : 0;
+          }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < DPT; ++i) {
+          if (!nb[i]) continue;
           const int v = threadIdx.x + WALK_THREADS * i;
           const MaskT cur = smask[v];
-          const MaskT fresh = nb & ~cur;
+          const MaskT fresh = nb[i] & ~cur;
           if (!fresh) continue;
           smask[v] = cur | fresh;
-          int32_t add = sall;
-          if (fresh != nb) {
+          int32_t add = sall[i];
+          if (fresh != nb[i]) {
             add = 0;
             for (MaskT m = fresh; m; m &= m - 1) add += keys[__builtin_ctzll((unsigned long long)m)];
           }
@@ -571,9 +568,9 @@ void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t
                       hipStream_t s) {
   const int lpt = (nprobe * Tq + WALK_THREADS - 1) / WALK_THREADS;  // at most 4 (walk_lds_bytes)
   const int R = walk_range_docs(TQP, nprobe, Tq);
-  if (TQP == 32 && R == 8192)
-    launch_walk_r<uint32_t, 8192>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
-                                  ndense, dense_slot, doc_dense, fp, hist, s);
+  if (TQP == 32 && R == 8192)  // fewer than 512 lists: one per thread
+    launch_walk_t<uint32_t, 8192, 1>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
+                                     dense_slot, doc_dense, fp, hist, s);
   else if (TQP == 32)
     launch_walk_r<uint32_t, 4096>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
                                   ndense, dense_slot, doc_dense, fp, hist, s);
