@@ -313,6 +313,33 @@ def search_streamed(oi, q_k, nprobe: int, ncand: int, k: int, docs_tokens):
     return dict(cent_ids=ci, cent_keys=ck, cand=r, cand_keys=rk, ids=ids, keys=keys, scores=keys_to_scores(keys))
 
 
+def search_deleted(oi, q_k, nprobe: int, ncand: int, k: int, deleted, refine: bool = False):
+    """The search with a deletion bitmap (Sec. 3.3, handling updates): the
+    stages composed as orc_search composes them, with the deleted documents
+    (deleted: bool [ndocs]) dropped from S_Q before the top-ncand.  q_k
+    [nq, Tq, dim]; ids padded with -1 and keys with INT64_MIN past the hits."""
+    q_k = _c(q_k, np.int16)
+    deleted = np.asarray(deleted, dtype=bool)
+    nq = q_k.shape[0]
+    ids = np.full((nq, k), -1, np.int32)
+    keys = np.full((nq, k), np.iinfo(np.int64).min, np.int64)
+    lens = np.diff(oi.doc_off)
+    rf, off, tok, tdoc = oi._refine_args(refine)
+    for qi in range(nq):
+        S = centroid_scores(q_k[qi], oi.cent_k)
+        ci, _ = probe(S, nprobe)
+        if rf:
+            docs, fp = partial_scores_res(S, ci, q_k[qi], oi.w_k, off, tok, tdoc, oi.codes, oi.ndocs)
+        else:
+            docs, fp = partial_scores(S, ci, oi.ivf_off, oi.ivf_doc, oi.ndocs)
+        keep = ~deleted[docs]
+        r, _ = topk(docs[keep], fp[keep], ncand)
+        fh = doc_scores(S, q_k[qi], oi.w_k, oi.doc_off[r], lens[r].astype(np.int32), oi.cid, oi.codes)
+        i, kk = topk(r, fh, k)
+        ids[qi, :len(i)], keys[qi, :len(i)] = i, kk
+    return dict(ids=ids, keys=keys, scores=keys_to_scores(keys))
+
+
 # ------------------------------------------------------- oracle index
 class OracleIndex:
     """The oracle's own view of a corpus: assignment given by the corpus,
