@@ -102,6 +102,7 @@ typedef struct {
   int32_t device;        /* HIP device ordinal */
   double q_norm_limit;   /* query tokens of smaller L2 norm get exact scores
                             (see "Value grid"); 0 for a builder */
+  int64_t ndeleted;      /* documents deleted (chimera_index_delete); 0 for a builder */
 } chimera_index_info;
 
 /* Last error message of the calling thread; never NULL. */
@@ -178,6 +179,28 @@ void chimera_builder_free(chimera_builder *b); /* NULL-safe */
 int chimera_index_load(const char *path, int hip_device, chimera_index **out);
 void chimera_index_free(chimera_index *idx); /* NULL-safe; waits for pending work */
 int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out);
+
+/* Deletion (Sec. 3.3, handling updates: a deletion bitmap over document ids
+ * that retrieval skips, with periodic compaction).
+ *
+ * chimera_index_delete sets the bits of doc_ids [n] (host memory; repeats
+ * and ids deleted before are allowed) in the index's bitmap.  From then on
+ * every search treats those documents as outside S_Q: they get no F', are
+ * never candidates, and never appear in any result; every other document's
+ * F', scores and order are unchanged.  E_INVAL (nothing changes) if an id is
+ * outside [0, ndocs) or n < 0.  It waits for all work on the index's device
+ * to finish before it updates the device copy of the bitmap, so it must not
+ * overlap a search of this index on another thread.
+ *
+ * chimera_index_compact rebuilds the device index without the deleted
+ * documents' tokens and posting-list entries, so retrieval no longer walks
+ * them.  Document ids do not change: a deleted document keeps its id and has
+ * no tokens.  Every search returns the same as before the call.  A store
+ * attached with chimera_fullbit_attach is compacted with it.  The old and the
+ * new device arrays are held at once while it runs; on failure (E_NOMEM,
+ * E_DEVICE) the index is left as it was. */
+int chimera_index_delete(chimera_index *idx, const int64_t *doc_ids, int64_t n);
+int chimera_index_compact(chimera_index *idx);
 
 /* ===================================================================== *
  * Search (Alg. 1 without the CPU full-bit stage).

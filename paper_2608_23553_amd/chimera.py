@@ -34,7 +34,7 @@ class _Info(ctypes.Structure):
     _fields_ = [("ndocs", ctypes.c_int64), ("ntokens", ctypes.c_int64), ("nnz", ctypes.c_int64),
                 ("ncent", ctypes.c_int32), ("dim", ctypes.c_int32), ("nbits", ctypes.c_int32),
                 ("max_doc_len", ctypes.c_int32), ("device_bytes", ctypes.c_int64), ("device", ctypes.c_int32),
-                ("q_norm_limit", ctypes.c_double)]
+                ("q_norm_limit", ctypes.c_double), ("ndeleted", ctypes.c_int64)]
 
 
 def lib():
@@ -62,6 +62,8 @@ def lib():
         "chimera_index_load": ([ctypes.c_char_p, INT, P], INT),
         "chimera_index_free": ([P], None),
         "chimera_index_info_get": ([P, P], INT),
+        "chimera_index_delete": ([P, P, I64], INT),
+        "chimera_index_compact": ([P], INT),
         "chimera_search": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_search_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_search_noalloc": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
@@ -248,6 +250,18 @@ class Index:
         st = _Info()
         _check(lib().chimera_index_info_get(self._h, ctypes.byref(st)))
         return _info(st)
+
+    def delete(self, doc_ids):
+        """chimera_index_delete: later searches skip these documents."""
+        ids = np.ascontiguousarray(np.asarray(doc_ids, dtype=np.int64).ravel())
+        _check(lib().chimera_index_delete(self._h, _np(ids), ids.size))
+        self._info = self.info()
+
+    def compact(self):
+        """chimera_index_compact: drops the deleted documents' tokens and
+        posting entries from the device index (ids unchanged)."""
+        _check(lib().chimera_index_compact(self._h))
+        self._info = self.info()
 
     def _q(self, Q):
         """Q as the library takes it, on the index's own GPU (the library

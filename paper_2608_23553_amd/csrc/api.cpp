@@ -376,10 +376,12 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     launch_fill_zero(hist, (size_t)nb * 4096 * 4, s);
     if (refine == CHIMERA_REFINE_TOKEN)
       launch_refine_walk(ci, ck, Qs, nb, Tq, TQP, nprobe, idx->d_tok_off, idx->d_ivf_tok, idx->d_tok_doc,
-                         idx->d_doc_off, idx->d_codes, idx->nbits, idx->h_weights, idx->ndocs, fp, hist, s);
+                         idx->d_doc_off, idx->d_codes, idx->nbits, idx->h_weights, idx->ndocs,
+                         idx->ndeleted ? idx->d_deleted : nullptr, fp, hist, s);
     else
       launch_cand_walk(ci, ck, nb, Tq, TQP, nprobe, idx->d_ivf_off, idx->d_ivf_doc, idx->ndocs, idx->ncent,
-                       idx->ndense, idx->d_dense_slot, idx->d_doc_dense, fp, hist, s);
+                       idx->ndense, idx->d_dense_slot, idx->d_doc_dense, idx->ndeleted ? idx->d_deleted : nullptr, fp,
+                       hist, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_CANDIDATES) {
       int64_t *cnt = cv.take<int64_t>((size_t)nb + 1);
@@ -466,7 +468,7 @@ void chimera_index_free(chimera_index *idx) {
   (void)hipDeviceSynchronize();
   void *ptrs[] = {idx->d_cent,    idx->d_doc_off,    idx->d_cid,       idx->d_codes,     idx->d_ivf_off,
                   idx->d_ivf_doc, idx->d_dense_slot, idx->d_doc_dense, idx->d_tok_off,   idx->d_ivf_tok,
-                  idx->d_tok_doc, idx->scratch,      idx->d_check};
+                  idx->d_tok_doc, idx->scratch,      idx->d_check,     idx->d_deleted};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   collab_free(idx);
@@ -481,7 +483,118 @@ int chimera_index_info_get(const chimera_index *idx, chimera_index_info *out) {
   out->dim = idx->dim; out->nbits = idx->nbits; out->max_doc_len = idx->max_doc_len;
   out->device_bytes = idx->device_bytes; out->device = idx->device;
   out->q_norm_limit = idx->q_norm_limit;
+  out->ndeleted = idx->ndeleted;
   return CHIMERA_OK;
+}
+
+int chimera_index_delete(chimera_index *idx, const int64_t *doc_ids, int64_t n) {
+  if (!idx || n < 0 || (n > 0 && !doc_ids)) return fail(CHIMERA_E_INVAL, "null index, null ids or n < 0");
+  for (int64_t i = 0; i < n; ++i)
+    if (doc_ids[i] < 0 || doc_ids[i] >= idx->ndocs)
+      return fail(CHIMERA_E_INVAL, "document id %lld (entry %lld) outside [0, %lld)", (long long)doc_ids[i],
+                  (long long)i, (long long)idx->ndocs);
+  if (n == 0) return CHIMERA_OK;
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  return guarded([&]() -> int {
+    const size_t words = (size_t)(idx->ndocs + 63) / 64;
+    std::vector<uint64_t> bits = idx->h_deleted;
+    bits.resize(words, 0);
+    int64_t added = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      uint64_t &w = bits[(size_t)doc_ids[i] >> 6];
+      const uint64_t b = 1ull << (doc_ids[i] & 63);
+      added += (w & b) ? 0 : 1;
+      w |= b;
+    }
+    if (!idx->d_deleted) CHIMERA_HIP(hipMalloc(&idx->d_deleted, words * 8));
+    // searches already queued read the bitmap as it was
+    CHIMERA_HIP(hipDeviceSynchronize());
+    CHIMERA_HIP(hipMemcpy(idx->d_deleted, bits.data(), words * 8, hipMemcpyHostToDevice));
+    idx->h_deleted.swap(bits);
+    idx->ndeleted += added;
+    return CHIMERA_OK;
+  });
+}
+
+int chimera_index_compact(chimera_index *idx) {
+  if (!idx) return fail(CHIMERA_E_INVAL, "null index");
+  BusyGuard bg(idx);
+  if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  DeviceGuard dg(idx->device);
+  if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
+  if (idx->ndeleted == 0) return CHIMERA_OK;
+  return guarded([&]() -> int {
+    CHIMERA_HIP(hipDeviceSynchronize());
+    // the index as the host builder holds it, without the deleted
+    // documents' tokens: the same centroids and quantiser, lists rebuilt
+    HostIndex h;
+    h.ncent = idx->ncent;
+    h.dim = idx->dim;
+    h.nbits = idx->nbits;
+    h.ndocs = idx->ndocs;
+    const int64_t cb = (int64_t)idx->dim * idx->nbits / 8;
+    h.cent.resize((size_t)idx->ncent * idx->dim);
+    CHIMERA_HIP(hipMemcpy(h.cent.data(), idx->d_cent, h.cent.size() * 2, hipMemcpyDeviceToHost));
+    h.cut_k.assign(idx->h_cut, idx->h_cut + (1 << idx->nbits) - 1);
+    h.weights.assign(idx->h_weights, idx->h_weights + (1 << idx->nbits));
+    std::vector<int32_t> cid((size_t)idx->ntok);
+    std::vector<uint8_t> codes((size_t)(idx->ntok * cb));
+    CHIMERA_HIP(hipMemcpy(cid.data(), idx->d_cid, cid.size() * 4, hipMemcpyDeviceToHost));
+    CHIMERA_HIP(hipMemcpy(codes.data(), idx->d_codes, codes.size(), hipMemcpyDeviceToHost));
+    const std::vector<int64_t> &off = idx->h_doc_off;
+    auto gone = [&](int64_t v) { return (idx->h_deleted[(size_t)v >> 6] >> (v & 63)) & 1; };
+    h.doc_off.assign((size_t)idx->ndocs + 1, 0);
+    for (int64_t v = 0; v < idx->ndocs; ++v) {
+      const int64_t len = gone(v) ? 0 : off[v + 1] - off[v];
+      h.doc_off[v + 1] = h.doc_off[v] + len;
+      h.max_doc_len = std::max<int32_t>(h.max_doc_len, (int32_t)len);
+    }
+    h.ntok = h.doc_off[idx->ndocs];
+    h.cid.resize((size_t)h.ntok);
+    h.codes.resize((size_t)(h.ntok * cb));
+    std::vector<int16_t> fullbit;
+    if (!idx->fullbit.empty()) fullbit.resize((size_t)h.ntok * idx->dim);
+    for (int64_t v = 0; v < idx->ndocs; ++v) {
+      const int64_t len = h.doc_off[v + 1] - h.doc_off[v];
+      if (!len) continue;
+      std::memcpy(&h.cid[h.doc_off[v]], &cid[off[v]], len * 4);
+      std::memcpy(&h.codes[h.doc_off[v] * cb], &codes[off[v] * cb], len * cb);
+      if (!fullbit.empty())
+        std::memcpy(&fullbit[h.doc_off[v] * idx->dim], &idx->fullbit[off[v] * idx->dim], len * idx->dim * 2);
+    }
+    std::vector<int32_t>().swap(cid);
+    std::vector<uint8_t>().swap(codes);
+    ivf_lists(h);
+    chimera_index *fresh = nullptr;
+    if (int rc = upload(h, idx->device, &fresh)) return rc;
+    // the new arrays replace the old ones; the handle, its scratch, events,
+    // bitmap and host state stay
+    void **mine[] = {(void **)&idx->d_cent,      (void **)&idx->d_doc_off,    (void **)&idx->d_cid,
+                     (void **)&idx->d_codes,     (void **)&idx->d_ivf_off,    (void **)&idx->d_ivf_doc,
+                     (void **)&idx->d_dense_slot, (void **)&idx->d_doc_dense, (void **)&idx->d_tok_off,
+                     (void **)&idx->d_ivf_tok,   (void **)&idx->d_tok_doc};
+    void **theirs[] = {(void **)&fresh->d_cent,      (void **)&fresh->d_doc_off,    (void **)&fresh->d_cid,
+                       (void **)&fresh->d_codes,     (void **)&fresh->d_ivf_off,    (void **)&fresh->d_ivf_doc,
+                       (void **)&fresh->d_dense_slot, (void **)&fresh->d_doc_dense, (void **)&fresh->d_tok_off,
+                       (void **)&fresh->d_ivf_tok,   (void **)&fresh->d_tok_doc};
+    for (size_t i = 0; i < sizeof(mine) / sizeof(mine[0]); ++i) {
+      (void)hipFree(*mine[i]);
+      *mine[i] = *theirs[i];
+      *theirs[i] = nullptr;
+    }
+    idx->ntok = fresh->ntok;
+    idx->nnz = fresh->nnz;
+    idx->max_doc_len = fresh->max_doc_len;
+    idx->ndense = fresh->ndense;
+    idx->device_bytes = fresh->device_bytes;
+    idx->h_doc_off.swap(fresh->h_doc_off);
+    idx->fullbit.swap(fullbit);
+    chimera_index_free(fresh);
+    return CHIMERA_OK;
+  });
 }
 
 int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,

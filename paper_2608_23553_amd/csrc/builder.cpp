@@ -353,9 +353,7 @@ static int32_t quantile_k(const std::vector<int64_t> &hist, int64_t n, int64_t n
   return 4096;
 }
 
-static void build_lists(chimera_builder *b) {
-  if (b->lists_built) return;
-  HostIndex &h = b->h;
+void chimera::ivf_lists(HostIndex &h) {
   std::vector<int64_t> last(h.ncent, -1), cnt(h.ncent + 1, 0);
   for (int64_t v = 0; v < h.ndocs; ++v)
     for (int64_t t = h.doc_off[v]; t < h.doc_off[v + 1]; ++t) {
@@ -372,6 +370,11 @@ static void build_lists(chimera_builder *b) {
       int32_t c = h.cid[t];
       if (last[c] != v) { last[c] = v; h.ivf_doc[cnt[c]++] = (int32_t)v; }
     }
+}
+
+static void build_lists(chimera_builder *b) {
+  if (b->lists_built) return;
+  chimera::ivf_lists(b->h);
   b->lists_built = true;
 }
 
@@ -548,7 +551,7 @@ int chimera_builder_info(const chimera_builder *b, chimera_index_info *out) {
   build_lists(const_cast<chimera_builder *>(b));
   const HostIndex &h = b->h;
   out->ndocs = h.ndocs; out->ntokens = h.ntok; out->nnz = h.nnz; out->ncent = h.ncent; out->dim = h.dim;
-  out->nbits = h.nbits; out->max_doc_len = h.max_doc_len; out->device = -1; out->q_norm_limit = 0.0;
+  out->nbits = h.nbits; out->max_doc_len = h.max_doc_len; out->device = -1; out->q_norm_limit = 0.0; out->ndeleted = 0;
   out->device_bytes = (int64_t)(h.cent.size() * 2 + h.doc_off.size() * 8 + h.cid.size() * 4 + h.codes.size() +
                                 h.ivf_off.size() * 8 + h.ivf_doc.size() * 4);
   return CHIMERA_OK;

@@ -59,6 +59,10 @@ void token_lists(const HostIndex &h, std::vector<int64_t> &tok_off, std::vector<
 const HostIndex *builder_host(const chimera_builder *b);  // builds the lists on first use
 int load_index(const char *path, HostIndex &h);
 
+// Posting lists ivf_off, ivf_doc and nnz from doc_off and cid (each list
+// ascending, one entry per document).
+void ivf_lists(HostIndex &h);
+
 // Zeroed tokens appended to the device copies of cid and codes.
 constexpr int kTokenPad = 64;
 
@@ -89,7 +93,8 @@ void launch_probe_merge(const uint64_t *part, int64_t nq, int Tq, int TQP, const
                         int32_t *cent_ids, int32_t *cent_keys, hipStream_t s);
 
 // Candidate walk: fp [nq][ndocs] i32 receives F' of every document, or
-// INT32_MIN for documents outside S_Q (every entry is written); hist
+// INT32_MIN for documents outside S_Q and for documents whose bit is set in
+// deleted [ceil(ndocs / 64)] (optional; every entry is written); hist
 // [nq][4096] u32, zero on entry, receives the histogram of the top 12 bits of
 // F' ^ 0x80000000 over S_Q.
 void launch_fill_zero(void *p, size_t bytes, hipStream_t s);
@@ -99,8 +104,8 @@ size_t walk_lds_bytes(int TQP, int nprobe, int Tq);
 constexpr size_t kWalkMaxLds = 160 * 1024;
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
-                      const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
-                      hipStream_t s);
+                      const int8_t *dense_slot, const uint64_t *doc_dense, const uint64_t *deleted, int32_t *fp,
+                      uint32_t *hist, hipStream_t s);
 
 // Refinement select: per query, the ncand best of S_Q by (F' desc, V asc),
 // written in ascending V order; n_valid [nq].  scratch holds
@@ -122,7 +127,7 @@ size_t refine_lds_bytes(int TQP, int nprobe, int Tq);
 void launch_refine_walk(const int32_t *cent_ids, const int32_t *cent_keys, const uint16_t *Qs, int64_t nq, int Tq,
                         int TQP, int nprobe, const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
                         const int64_t *doc_off, const uint8_t *codes, int nbits, const uint16_t *weights_host,
-                        int64_t ndocs, int32_t *fp, uint32_t *hist, hipStream_t s);
+                        int64_t ndocs, const uint64_t *deleted, int32_t *fp, uint32_t *hist, hipStream_t s);
 
 // Residual scoring of candidates lo .. hi-1 of each query (those below
 // n_valid): fhat [nq][ncand] i32 keys; ST is [nq][ncent + 1][TQP] (row ncent
@@ -181,6 +186,11 @@ struct chimera_index {
   int64_t *d_tok_off = nullptr;     // token-level lists (see token_lists)
   int32_t *d_ivf_tok = nullptr;
   int32_t *d_tok_doc = nullptr;
+  // deletion bitmap over document ids (bit v of word v / 64), host copy and
+  // device copy (allocated on the first deletion)
+  std::vector<uint64_t> h_deleted;
+  uint64_t *d_deleted = nullptr;
+  int64_t ndeleted = 0;
   uint16_t h_weights[16] = {0};
   int32_t h_cut[15] = {0};
   // exact scores need every query token's L2 norm below this (see upload)

@@ -188,8 +188,9 @@ template <typename MaskT, int R, int LPT>
 __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
     const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, int64_t nq, int Tq, int TQP,
     int nprobe, const int64_t *__restrict__ ivf_off, const int32_t *__restrict__ ivf_doc, int64_t ndocs, int ncent,
-    int ndense, const int8_t *__restrict__ dense_slot, const uint64_t *__restrict__ doc_dense, int nranges, int G,
-    int M, int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
+    int ndense, const int8_t *__restrict__ dense_slot, const uint64_t *__restrict__ doc_dense,
+    const uint64_t *__restrict__ deleted, int nranges, int G, int M, int32_t *__restrict__ fp,
+    uint32_t *__restrict__ hist) {
   constexpr int DPT = R / WALK_THREADS;  // documents of a range each thread owns in the dense phase
   constexpr int WIN = walk_win<LPT>();
   static_assert(R * sizeof(MaskT) >= SEL_BINS * 4, "the histogram reuses the mask array");
@@ -498,8 +499,9 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
         dm[i] = ndense > 0 && v < ndocs ? doc_dense[v] : 0;
       }
     }
+    // documents outside S_Q, and deleted ones, get NO_HIT
     for (int v = threadIdx.x; v < nd; v += WALK_THREADS)
-      if (smask[v] == 0) sfp[v] = NO_HIT;
+      if (smask[v] == 0 || (deleted && ((deleted[(d0 + v) >> 6] >> ((d0 + v) & 63)) & 1))) sfp[v] = NO_HIT;
     __syncthreads();
     uint32_t *sh = (uint32_t *)smask;  // the masks are no longer needed
     for (int i = threadIdx.x; i < SEL_BINS; i += WALK_THREADS) sh[i] = 0;
@@ -526,7 +528,7 @@ size_t walk_lds_bytes(int TQP, int nprobe, int Tq) {
 template <typename MaskT, int R, int LPT>
 static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                           const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
-                          const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
+                          const int8_t *dense_slot, const uint64_t *doc_dense, const uint64_t *deleted, int32_t *fp, uint32_t *hist,
                           hipStream_t s) {
   const int nranges = (int)((ndocs + R - 1) / R);
   // ranges per workgroup: enough groups per query for about 4096 workgroups
@@ -543,40 +545,40 @@ static void launch_walk_t(const int32_t *cent_ids, const int32_t *cent_keys, int
   (void)attr;
   hipLaunchKernelGGL((k_cand_walk<MaskT, R, LPT>), dim3((unsigned)blocks), dim3(WALK_THREADS), lds, s, cent_ids,
                      cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense, dense_slot, doc_dense,
-                     nranges, G, M, fp, hist);
+                     deleted, nranges, G, M, fp, hist);
 }
 
 template <typename MaskT, int R>
 static void launch_walk_r(int lpt, const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP,
                           int nprobe, const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent,
-                          int ndense, const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp,
+                          int ndense, const int8_t *dense_slot, const uint64_t *doc_dense, const uint64_t *deleted, int32_t *fp,
                           uint32_t *hist, hipStream_t s) {
   if (lpt <= 1)
     launch_walk_t<MaskT, R, 1>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                               dense_slot, doc_dense, fp, hist, s);
+                               dense_slot, doc_dense, deleted, fp, hist, s);
   else if (lpt <= 2)
     launch_walk_t<MaskT, R, 2>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                               dense_slot, doc_dense, fp, hist, s);
+                               dense_slot, doc_dense, deleted, fp, hist, s);
   else
     launch_walk_t<MaskT, R, 4>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                               dense_slot, doc_dense, fp, hist, s);
+                               dense_slot, doc_dense, deleted, fp, hist, s);
 }
 
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
-                      const int8_t *dense_slot, const uint64_t *doc_dense, int32_t *fp, uint32_t *hist,
+                      const int8_t *dense_slot, const uint64_t *doc_dense, const uint64_t *deleted, int32_t *fp, uint32_t *hist,
                       hipStream_t s) {
   const int lpt = (nprobe * Tq + WALK_THREADS - 1) / WALK_THREADS;  // at most 4 (walk_lds_bytes)
   const int R = walk_range_docs(TQP, nprobe, Tq);
   if (TQP == 32 && R == 8192)  // fewer than 512 lists: one per thread
     launch_walk_t<uint32_t, 8192, 1>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                                     dense_slot, doc_dense, fp, hist, s);
+                                     dense_slot, doc_dense, deleted, fp, hist, s);
   else if (TQP == 32)
     launch_walk_r<uint32_t, 4096>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
-                                  ndense, dense_slot, doc_dense, fp, hist, s);
+                                  ndense, dense_slot, doc_dense, deleted, fp, hist, s);
   else
     launch_walk_r<unsigned long long, 2048>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs,
-                                            ncent, ndense, dense_slot, doc_dense, fp, hist, s);
+                                            ncent, ndense, dense_slot, doc_dense, deleted, fp, hist, s);
 }
 
 // ------------------------------------------------------- block helpers

@@ -120,8 +120,8 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     const int32_t *__restrict__ cent_ids, const int32_t *__restrict__ cent_keys, const uint16_t *__restrict__ Qs,
     int64_t nq, int Tq, int nprobe, const int64_t *__restrict__ tok_off, const int32_t *__restrict__ ivf_tok,
     const int32_t *__restrict__ tok_doc, const int64_t *__restrict__ doc_off, const uint8_t *__restrict__ codes,
-    uint4 w_lo, uint4 w_hi, int64_t ndocs, int nranges, int G, int M, int32_t *__restrict__ fp,
-    uint32_t *__restrict__ hist) {
+    uint4 w_lo, uint4 w_hi, int64_t ndocs, const uint64_t *__restrict__ deleted, int nranges, int G, int M,
+    int32_t *__restrict__ fp, uint32_t *__restrict__ hist) {
   constexpr int RR = ref_range_docs<TQP>();
   static_assert((RR & (RR - 1)) == 0 && RR % 32 == 0, "ranges of a power of two documents");
   extern __shared__ __align__(16) unsigned char ref_lds[];
@@ -315,7 +315,9 @@ __global__ __launch_bounds__(REF_THREADS) void k_refine_walk(
     __syncthreads();
     int32_t *f = fp + q * ndocs + d0;
     for (int v = threadIdx.x; v < nd; v += REF_THREADS) {
-      const bool hit = (hitw[v >> 5] >> (v & 31)) & 1u;
+      // deleted documents get NO_HIT
+      const bool hit = ((hitw[v >> 5] >> (v & 31)) & 1u) &&
+                       !(deleted && ((deleted[(d0 + v) >> 6] >> ((d0 + v) & 63)) & 1));
       const int32_t x = hit ? sfp[v] : NO_HIT;
       f[v] = x;
       sfp[v] = 0;
@@ -341,7 +343,7 @@ template <int NBITS, int TQP>
 static void launch_refine_t(const int32_t *cent_ids, const int32_t *cent_keys, const uint16_t *Qs, int64_t nq, int Tq,
                             int nprobe, const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
                             const int64_t *doc_off, const uint8_t *codes, uint4 w_lo, uint4 w_hi, int64_t ndocs,
-                            int32_t *fp, uint32_t *hist, hipStream_t s) {
+                            const uint64_t *deleted, int32_t *fp, uint32_t *hist, hipStream_t s) {
   constexpr int RR = ref_range_docs<TQP>();
   const int nranges = (int)((ndocs + RR - 1) / RR);
   // ranges per workgroup: enough groups per query for about 4096 workgroups
@@ -358,20 +360,20 @@ static void launch_refine_t(const int32_t *cent_ids, const int32_t *cent_keys, c
   (void)attr;
   hipLaunchKernelGGL((k_refine_walk<NBITS, TQP>), dim3((unsigned)blocks), dim3(REF_THREADS), lds, s, cent_ids,
                      cent_keys, Qs, nq, Tq, nprobe, tok_off, ivf_tok, tok_doc, doc_off, codes, w_lo, w_hi, ndocs,
-                     nranges, G, M, fp, hist);
+                     deleted, nranges, G, M, fp, hist);
 }
 
 void launch_refine_walk(const int32_t *cent_ids, const int32_t *cent_keys, const uint16_t *Qs, int64_t nq, int Tq,
                         int TQP, int nprobe, const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc,
                         const int64_t *doc_off, const uint8_t *codes, int nbits, const uint16_t *weights_host,
-                        int64_t ndocs, int32_t *fp, uint32_t *hist, hipStream_t s) {
+                        int64_t ndocs, const uint64_t *deleted, int32_t *fp, uint32_t *hist, hipStream_t s) {
   uint32_t w[8] = {0};
   const int B = 1 << nbits;
   for (int u = 0; u < B; ++u) w[u >> 1] |= (uint32_t)weights_host[u] << (16 * (u & 1));
   const uint4 w_lo = make_uint4(w[0], w[1], w[2], w[3]), w_hi = make_uint4(w[4], w[5], w[6], w[7]);
 #define CHIMERA_RF(NB, TP)                                                                                       \
   launch_refine_t<NB, TP>(cent_ids, cent_keys, Qs, nq, Tq, nprobe, tok_off, ivf_tok, tok_doc, doc_off, codes, \
-                          w_lo, w_hi, ndocs, fp, hist, s)
+                          w_lo, w_hi, ndocs, deleted, fp, hist, s)
   if (nbits == 2 && TQP == 32) CHIMERA_RF(2, 32);
   else if (nbits == 2) CHIMERA_RF(2, 64);
   else if (TQP == 32) CHIMERA_RF(4, 32);
