@@ -54,6 +54,12 @@ def _load():
                         P, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, ctypes.c_int], ctypes.c_int),
         "orc_prune_batch": ([P, I32, I32, I64, P, P, P, I64, I32, I32, I32, P, P, P, P, P, P,
                              ctypes.c_int, P, P, P, P, P, ctypes.c_int], ctypes.c_int),
+        "orc_rabitq_rotate": ([P, I64, I32, P, P], None),
+        "orc_rabitq_quantize": ([P, I64, I32, ctypes.c_int, P, P], None),
+        "orc_rabitq_encode": ([P, I64, I32, P, ctypes.c_int, P, P, P], None),
+        "orc_rabitq_pack1": ([P, I64, I32, ctypes.c_int, P], None),
+        "orc_lut_ip": ([P, P, I32], I64),
+        "orc_rabitq_doc_scores": ([P, I32, I32, P, ctypes.c_int, ctypes.c_int, I64, P, P, P, P, P], None),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -335,6 +341,83 @@ def search_deleted(oi, q_k, nprobe: int, ncand: int, k: int, deleted, refine: bo
         keep = ~deleted[docs]
         r, _ = topk(docs[keep], fp[keep], ncand)
         fh = doc_scores(S, q_k[qi], oi.w_k, oi.doc_off[r], lens[r].astype(np.int32), oi.cid, oi.codes)
+        i, kk = topk(r, fh, k)
+        ids[qi, :len(i)], keys[qi, :len(i)] = i, kk
+    return dict(ids=ids, keys=keys, scores=keys_to_scores(keys))
+
+
+# ------------------------------------------------------- RaBitQ (Sec. 2.2, 3.1, 4.1)
+def rabitq_rotate(x_k, signs) -> np.ndarray:
+    """xp = H diag(s) x per row (orc_rabitq_rotate), int64."""
+    x_k, signs = _c(np.atleast_2d(x_k), np.int16), _c(signs, np.int8)
+    n, D = x_k.shape
+    out = np.empty((n, D), np.int64)
+    _load().orc_rabitq_rotate(_p(x_k), n, D, _p(signs), _p(out))
+    return out
+
+
+def rabitq_quantize(xp, B: int):
+    """Nearest codewords of the rows of xp: (codes uint8 [n, D], az int64 [n])."""
+    xp = _c(np.atleast_2d(xp), np.int64)
+    n, D = xp.shape
+    codes = np.empty((n, D), np.uint8)
+    az = np.empty(max(n, 1), np.int64)
+    _load().orc_rabitq_quantize(_p(xp), n, D, B, _p(codes), _p(az))
+    return codes, az[:n]
+
+
+def rabitq_encode(x_k, signs, B: int):
+    """(codes uint8 [n, D], gB float32 [n], g1 float32 [n]) of grid tokens."""
+    x_k, signs = _c(np.atleast_2d(x_k), np.int16), _c(signs, np.int8)
+    n, D = x_k.shape
+    codes = np.empty((n, D), np.uint8)
+    gB = np.empty(max(n, 1), np.float32)
+    g1 = np.empty(max(n, 1), np.float32)
+    _load().orc_rabitq_encode(_p(x_k), n, D, _p(signs), B, _p(codes), _p(gB), _p(g1))
+    return codes, gB[:n], g1[:n]
+
+
+def rabitq_pack1(codes, B: int) -> np.ndarray:
+    codes = _c(np.atleast_2d(codes), np.uint8)
+    n, D = codes.shape
+    out = np.empty((n, D // 8), np.uint8)
+    _load().orc_rabitq_pack1(_p(codes), n, D, B, _p(out))
+    return out
+
+
+def lut_ip(xq, bits) -> int:
+    xq, bits = _c(xq, np.int64), _c(bits, np.uint8)
+    return int(_load().orc_lut_ip(_p(xq), _p(bits), xq.shape[0]))
+
+
+def rabitq_doc_scores(q_k, signs, B: int, bits: int, tok_begin, tok_len, codes, g) -> np.ndarray:
+    q_k, signs = _c(q_k, np.int16), _c(signs, np.int8)
+    tok_begin, tok_len = _c(tok_begin, np.int64), _c(tok_len, np.int32)
+    codes, g = _c(codes, np.uint8), _c(g, np.float32)
+    Tq, D = q_k.shape
+    n = tok_begin.shape[0]
+    out = np.empty(max(n, 1), np.int64)
+    _load().orc_rabitq_doc_scores(_p(q_k), Tq, D, _p(signs), B, bits, n, _p(tok_begin), _p(tok_len), _p(codes),
+                                  _p(g), _p(out))
+    return out[:n].copy()
+
+
+def search_rabitq(oi, q_k, nprobe: int, ncand: int, k: int, signs, B: int, codes, g1):
+    """The search with the document scores of the 1-bit RaBitQ part (Sec.
+    3.2 document scoring on the GPU): probe, candidates, F' and top-ncand as
+    orc_search, then F^ from rabitq_doc_scores (bits 1) and the top-k.  codes
+    [ntok, D] are the B-bit codes of every token, g1 their 1-bit factors."""
+    q_k = _c(q_k, np.int16)
+    nq = q_k.shape[0]
+    ids = np.full((nq, k), -1, np.int32)
+    keys = np.full((nq, k), np.iinfo(np.int64).min, np.int64)
+    lens = np.diff(oi.doc_off)
+    for qi in range(nq):
+        S = centroid_scores(q_k[qi], oi.cent_k)
+        ci, _ = probe(S, nprobe)
+        docs, fp = partial_scores(S, ci, oi.ivf_off, oi.ivf_doc, oi.ndocs)
+        r, _ = topk(docs, fp, ncand)
+        fh = rabitq_doc_scores(q_k[qi], signs, B, 1, oi.doc_off[r], lens[r].astype(np.int32), codes, g1)
         i, kk = topk(r, fh, k)
         ids[qi, :len(i)], keys[qi, :len(i)] = i, kk
     return dict(ids=ids, keys=keys, scores=keys_to_scores(keys))

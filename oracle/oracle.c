@@ -448,3 +448,170 @@ int orc_search(const int16_t *cent_k, int32_t ncent, int32_t dim, const int64_t 
   }
   return 0;
 }
+
+/* ------------------------------------------------------------- RaBitQ */
+
+void orc_rabitq_rotate(const int16_t *x_k, int64_t n, int32_t D, const int8_t *signs, int64_t *xp) {
+  for (int64_t r = 0; r < n; ++r)
+    for (int32_t i = 0; i < D; ++i) {
+      int64_t s = 0;
+      for (int32_t j = 0; j < D; ++j) {
+        const int64_t h = (__builtin_popcount((unsigned)(i & j)) & 1) ? -1 : 1;
+        s += h * (int64_t)signs[j] * (int64_t)x_k[r * D + j];
+      }
+      xp[r * D + i] = s;
+    }
+}
+
+/* t = num / den at which coordinate i of the rounding path steps up */
+typedef struct {
+  int64_t num, den;
+  int32_t i;
+} rq_event;
+
+static int rq_event_cmp(const void *pa, const void *pb) {
+  const rq_event *a = (const rq_event *)pa, *b = (const rq_event *)pb;
+  const int64_t l = a->num * b->den, r = b->num * a->den;
+  if (l != r) return l < r ? -1 : 1;
+  return a->i < b->i ? -1 : (a->i > b->i ? 1 : 0);
+}
+
+/* The nearest codeword of one vector.  As t grows, rounding t * xp to the
+ * nearest point of the half-integer grid (clamped to |y| <= (2^B-1)/2) visits
+ * a sequence of codewords; the codeword of largest cosine lies on it (it is a
+ * nearest grid point of some t * xp, and of the points tied at a step of
+ * several coordinates at once the cosine is largest at the two ends, since
+ * every stepping coordinate adds the same ratio of <xp, 2y> to |2y|^2).  So
+ * the candidates are the codewords between consecutive distinct step values
+ * of t, compared exactly: A / sqrt(N) with A = <xp, 2y>, N = |2y|^2. */
+static void rq_quantize_one(const int64_t *xp, int32_t D, int B, uint8_t *code, int64_t *az, rq_event *ev,
+                            int32_t *level, int32_t *best) {
+  const int32_t half = 1 << (B - 1);
+  int64_t A = 0, N = D;
+  int64_t ne = 0;
+  for (int32_t i = 0; i < D; ++i) {
+    level[i] = 0;
+    best[i] = 0;
+    const int64_t a = xp[i] < 0 ? -xp[i] : xp[i];
+    A += a;
+    if (a == 0) continue;
+    for (int32_t m = 1; m < half; ++m) {
+      ev[ne].num = m;
+      ev[ne].den = a;
+      ev[ne].i = i;
+      ++ne;
+    }
+  }
+  qsort(ev, (size_t)ne, sizeof(rq_event), rq_event_cmp);
+  int64_t bestA = A, bestN = N;
+  for (int64_t e = 0; e < ne;) {
+    int64_t f = e;
+    while (f < ne && ev[f].num * ev[e].den == ev[e].num * ev[f].den) {
+      const int32_t i = ev[f].i;
+      const int64_t a = xp[i] < 0 ? -xp[i] : xp[i];
+      A += 2 * a;
+      N += 8 * (int64_t)level[i] + 8;
+      level[i] += 1;
+      ++f;
+    }
+    e = f;
+    /* A / sqrt(N) > bestA / sqrt(bestN), both A > 0 */
+    if ((__int128)A * A * bestN > (__int128)bestA * bestA * N) {
+      bestA = A;
+      bestN = N;
+      memcpy(best, level, sizeof(int32_t) * (size_t)D);
+    }
+  }
+  for (int32_t i = 0; i < D; ++i) code[i] = (uint8_t)(xp[i] < 0 ? half - 1 - best[i] : half + best[i]);
+  *az = bestA;
+}
+
+void orc_rabitq_quantize(const int64_t *xp, int64_t n, int32_t D, int B, uint8_t *codes, int64_t *az) {
+  rq_event *ev = (rq_event *)malloc(sizeof(rq_event) * (size_t)D * (size_t)(1 << (B - 1)));
+  int32_t *level = (int32_t *)malloc(sizeof(int32_t) * (size_t)D);
+  int32_t *best = (int32_t *)malloc(sizeof(int32_t) * (size_t)D);
+  for (int64_t r = 0; r < n; ++r) rq_quantize_one(xp + r * D, D, B, codes + r * D, az + r, ev, level, best);
+  free(ev);
+  free(level);
+  free(best);
+}
+
+static float rq_factor(int64_t k2, int64_t a) {
+  return a == 0 ? 0.0f : (float)((double)k2 / ((double)a * 1024.0));
+}
+
+void orc_rabitq_encode(const int16_t *x_k, int64_t n, int32_t D, const int8_t *signs, int B, uint8_t *codes,
+                       float *gB, float *g1) {
+  int64_t *xp = (int64_t *)malloc(sizeof(int64_t) * (size_t)D);
+  for (int64_t r = 0; r < n; ++r) {
+    orc_rabitq_rotate(x_k + r * D, 1, D, signs, xp);
+    int64_t az = 0;
+    orc_rabitq_quantize(xp, 1, D, B, codes + r * D, &az);
+    int64_t k2 = 0, a1 = 0;
+    for (int32_t i = 0; i < D; ++i) {
+      k2 += (int64_t)x_k[r * D + i] * x_k[r * D + i];
+      a1 += xp[i] < 0 ? -xp[i] : xp[i]; /* <xp, 2 y1> with y1 = msb - 1/2 */
+    }
+    gB[r] = rq_factor(k2, az);
+    g1[r] = rq_factor(k2, a1);
+  }
+  free(xp);
+}
+
+void orc_rabitq_pack1(const uint8_t *codes, int64_t n, int32_t D, int B, uint8_t *bits) {
+  memset(bits, 0, (size_t)(n * D / 8));
+  for (int64_t r = 0; r < n; ++r)
+    for (int32_t i = 0; i < D; ++i)
+      if (codes[r * D + i] >> (B - 1)) bits[r * (D / 8) + i / 8] |= (uint8_t)(1u << (i % 8));
+}
+
+int64_t orc_lut_ip(const int64_t *xq, const uint8_t *bits, int32_t D) {
+  int64_t s = 0;
+  for (int32_t j = 0; j < D / 4; ++j) {
+    int64_t T[16];
+    for (int u = 0; u < 16; ++u) {
+      T[u] = 0;
+      for (int t = 0; t < 4; ++t)
+        if ((u >> t) & 1) T[u] += xq[4 * j + t];
+    }
+    const int u = (bits[(4 * j) / 8] >> ((4 * j) % 8)) & 15;
+    s += T[u];
+  }
+  return s;
+}
+
+/* est = g * float(<xq, 2y> * 2^-12) */
+static float rq_est(const int64_t *xq, const uint8_t *code, int32_t D, int B, int bits, float g) {
+  int64_t ip = 0;
+  for (int32_t i = 0; i < D; ++i) {
+    const int64_t z = bits == 1 ? (code[i] >> (B - 1) ? 1 : -1) : 2 * (int64_t)code[i] - ((1 << B) - 1);
+    ip += xq[i] * z;
+  }
+  const float x = (float)ldexp((double)ip, -12);
+  return g * x;
+}
+
+void orc_rabitq_doc_scores(const int16_t *q_k, int32_t Tq, int32_t D, const int8_t *signs, int B, int bits,
+                           int64_t n, const int64_t *tok_begin, const int32_t *tok_len, const uint8_t *codes,
+                           const float *g, int64_t *out) {
+  int64_t *xq = (int64_t *)malloc(sizeof(int64_t) * (size_t)Tq * D);
+  orc_rabitq_rotate(q_k, Tq, D, signs, xq);
+  for (int64_t i = 0; i < n; ++i) {
+    if (tok_len[i] <= 0) {
+      out[i] = LLONG_MIN;
+      continue;
+    }
+    int64_t f = 0;
+    for (int32_t j = 0; j < Tq; ++j) {
+      float m = -INFINITY;
+      for (int32_t t = 0; t < tok_len[i]; ++t) {
+        const int64_t tok = tok_begin[i] + t;
+        const float e = rq_est(xq + (int64_t)j * D, codes + tok * D, D, B, bits, g[tok]);
+        if (e > m) m = e;
+      }
+      f += (int64_t)nearbyint((double)m * 4194304.0);
+    }
+    out[i] = f;
+  }
+  free(xq);
+}

@@ -149,6 +149,44 @@ int orc_prune_batch(const int16_t *cent_k, int32_t ncent, int32_t dim, int64_t n
                     int64_t *cand_keys, int64_t *n_cand, int refine, const int32_t *w_k, const uint8_t *codes,
                     const int64_t *tok_off, const int32_t *ivf_tok, const int32_t *tok_doc, int nthreads);
 
+/* ---- RaBitQ codes (Sec. 2.2, Eqs. 2-6, extended to B bits; Sec. 3.1, the
+ * 1-bit most significant part; Sec. 4.1, the LUT binary inner product).
+ *
+ * Readings.  The random orthonormal P is P = H diag(s) / sqrt(D): H the
+ * Sylvester Hadamard matrix of order D (H[i][j] = (-1)^popcount(i & j)), s
+ * random signs (an input).  Every quantity below is a ratio in which the
+ * factor 1/sqrt(D) and the norms of Eq. 2 cancel, so the oracle works with
+ * xp = H diag(s) x on grid integers, exactly.  The codeword of Eq. 4 is the
+ * y in {-(2^B-1)/2 + u}^D of largest cosine with xp, ties to the smallest
+ * |y| (a zero coordinate of xp takes y = +1/2).  The estimate of <q_r, o_r> (Eq. 5, with Eq. 2's norms and Eq. 6's
+ * code form) is |o_r|^2 <P q_r, y> / <P o_r, y>, carried as
+ *   est = g * float(<xq, 2y> * 2^-12),   g = float(K2 / (A * 1024.0)),
+ * xq = H diag(s) q_k, K2 = sum_d o_k[d]^2, A = <xp, 2y> (integers; the last
+ * multiply is one fp32 rounding).  The 1-bit part uses y1 = msb - 1/2 and its
+ * own factor g1. ---- */
+/* xp [n][D] = H diag(s) x for each of the n rows of x_k [n][D]. */
+void orc_rabitq_rotate(const int16_t *x_k, int64_t n, int32_t D, const int8_t *signs, int64_t *xp);
+/* codes [n][D] in 0..2^B-1 (B <= 8) of the nearest codewords of the rows of
+ * xp, and az [n] = <xp, 2y> of each. */
+void orc_rabitq_quantize(const int64_t *xp, int64_t n, int32_t D, int B, uint8_t *codes, int64_t *az);
+/* Rotation, quantisation and the factors gB (B-bit code) and g1 (its most
+ * significant bits) of n tokens; g = 0 for a zero token. */
+void orc_rabitq_encode(const int16_t *x_k, int64_t n, int32_t D, const int8_t *signs, int B, uint8_t *codes,
+                       float *gB, float *g1);
+/* The most significant bits of B-bit codes [n][D], packed: bit i of a token
+ * in byte i / 8, bit i % 8. */
+void orc_rabitq_pack1(const uint8_t *codes, int64_t n, int32_t D, int B, uint8_t *bits);
+/* <xq, b> of a packed 1-bit code through the table of Sec. 4.1:
+ * T[j][u] = sum_{t<4} u_t xq[4j+t], summed over the D/4 nibbles. */
+int64_t orc_lut_ip(const int64_t *xq, const uint8_t *bits, int32_t D);
+/* RaBitQ document scores: for doc i (tokens tok_begin[i] .. + tok_len[i] of
+ * codes [..][D] with factors g [..]) F^ = sum_{j<Tq} key(max_t est(q_j, t)),
+ * key(x) = rint(x * 2^22) (ties to even); est from the whole code (bits == B)
+ * or from its most significant bits (bits == 1).  INT64_MIN for an empty doc. */
+void orc_rabitq_doc_scores(const int16_t *q_k, int32_t Tq, int32_t D, const int8_t *signs, int B, int bits,
+                           int64_t n, const int64_t *tok_begin, const int32_t *tok_len, const uint8_t *codes,
+                           const float *g, int64_t *out);
+
 #ifdef __cplusplus
 }
 #endif
