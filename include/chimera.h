@@ -152,6 +152,22 @@ int chimera_builder_add_docs(chimera_builder *b, const uint16_t *tokens_bf16, co
  * tokens, so that add_docs never reallocates (a 2-bit index of 600M tokens
  * holds about 20 GB of codes).  E_NOMEM if the memory cannot be reserved. */
 int chimera_builder_reserve(chimera_builder *b, int64_t ndocs, int64_t ntok);
+/* Optional, before pass 2: also encode every document token with RaBitQ
+ * (Sec. 2.2, the extended-bits quantiser, with B = 4 as Sec. 3.1 uses),
+ * for chimera_search_rabitq.  The random orthonormal rotation is
+ * P = H diag(signs) / sqrt(dim), H the Sylvester Hadamard matrix of order dim
+ * (H[i][j] = (-1)^popcount(i & j)), signs host [dim] int8, each +1 or -1
+ * (drawn at random by the caller).  A token o (grid values) gets the code
+ * y in {-7.5, -6.5, .., 7.5}^dim of largest cosine with P o (ties to the
+ * smallest |y|; a zero coordinate takes +1/2), and the factors
+ *     g = |o|^2 / <P o, y>   (rounded once to float32)
+ * of its 4-bit code and of its most significant bits (y1 = msb - 1/2).  The
+ * most significant bits (16 bytes a token) and their factor go to the GPU
+ * with the index (Sec. 3.1: 1-bit codes on the GPU); the 4-bit codes stay
+ * in host memory.  E_INVAL if documents were already added or a sign is not
+ * +-1.  Index files do not hold these codes: chimera_builder_save then
+ * returns E_UNSUPPORTED. */
+int chimera_builder_rabitq(chimera_builder *b, const int8_t *signs);
 /* Quantiser as fixed by freeze: cut_k [2^b - 1] cutoffs in units of 2^-11,
  * weights_bf16 [2^b] bucket values.  Either pointer may be NULL. */
 int chimera_builder_quantizer(const chimera_builder *b, int32_t *cut_k, uint16_t *weights_bf16);
@@ -166,6 +182,14 @@ int chimera_builder_upload(const chimera_builder *b, int hip_device, chimera_ind
  * ivf_off [ncent+1] i64, ivf_doc [nnz] i32.  Any pointer may be NULL. */
 int chimera_builder_sections(const chimera_builder *b, int64_t *doc_off, int32_t *cid, uint8_t *codes,
                              int64_t *ivf_off, int32_t *ivf_doc);
+/* Host copies of the RaBitQ sections (chimera_builder_rabitq), per token:
+ * bits1 [ntok][dim / 8] the most significant bits (bit d in byte d / 8, bit
+ * d % 8), g1 [ntok] their factor, codes4 [ntok][dim / 2] the 4-bit codes
+ * (dimension 2i in the low nibble of byte i, 2i + 1 in the high nibble), g4
+ * [ntok] their factor.  Any pointer may be NULL; E_INVAL if the builder has
+ * no RaBitQ codes. */
+int chimera_builder_rabitq_sections(const chimera_builder *b, uint8_t *bits1, float *g1, uint8_t *codes4,
+                                    float *g4);
 int chimera_builder_info(const chimera_builder *b, chimera_index_info *out);
 void chimera_builder_free(chimera_builder *b); /* NULL-safe */
 
@@ -247,6 +271,21 @@ int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, i
 int chimera_search_refine(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
                           int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
                           void *hip_stream);
+
+/* chimera_search with step 4 scored from the RaBitQ 1-bit codes (index built
+ * with chimera_builder_rabitq, else E_UNSUPPORTED): Sec. 3.2 document
+ * scoring on the GPU, the complete 1-bit score over every token of each
+ * kept document,
+ *   F^(V) = sum_j key(max_{t in V} est_1(Q_j, t)),
+ *   est_1(q, t) = g1_t * <P' q, 2 y1_t> * 2^-12,   key(x) = rint(x * 2^22),
+ * with P' = H diag(signs) and y1_t = msb_t - 1/2 (Eq. 5 with Eq. 2's norms,
+ * through Eq. 6; <P' q, 2 y1> is the binary inner product of Sec. 4.1 less
+ * the sum of P' q, computed exactly); key rounds ties to even.  Scores are
+ * F^ * 2^-22 in float32.  Exact (equal to the reference formula) for query
+ * tokens of L2 norm below 2.8; F^ saturates at +-(2^31 - 1).  Steps 1-3 and
+ * 5 are chimera_search's; the probe writes no centroid-score table. */
+int chimera_search_rabitq(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream);
 
 /* chimera_search for callers that cannot allocate memory (code under HIP
  * graph capture, tight serving loops, harnesses that forbid allocation):

@@ -53,6 +53,8 @@ def lib():
         "chimera_builder_freeze_quantizer": ([P], INT),
         "chimera_builder_add_docs": ([P, P, P, P, I64], INT),
         "chimera_builder_reserve": ([P, I64, I64], INT),
+        "chimera_builder_rabitq": ([P, P], INT),
+        "chimera_builder_rabitq_sections": ([P, P, P, P, P], INT),
         "chimera_builder_quantizer": ([P, P, P], INT),
         "chimera_builder_save": ([P, ctypes.c_char_p], INT),
         "chimera_builder_upload": ([P, INT, P], INT),
@@ -67,6 +69,7 @@ def lib():
         "chimera_search": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_search_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_search_noalloc": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
+        "chimera_search_rabitq": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P], INT),
         "chimera_probe": ([P, P, INT, I64, I32, I32, I32, P, P, P], INT),
         "chimera_candidates": ([P, P, INT, I64, I32, I32, I32, P, P, I64, P], INT),
         "chimera_prune": ([P, P, INT, I64, I32, I32, I32, I32, P, P, P, P], INT),
@@ -155,6 +158,14 @@ class Builder:
     def reserve(self, ndocs: int, ntok: int):
         _check(lib().chimera_builder_reserve(self._h, ndocs, ntok))
 
+    def rabitq(self, signs: np.ndarray):
+        """chimera_builder_rabitq: also encode the tokens with RaBitQ under
+        the rotation H diag(signs) (signs int8 [dim] of +-1)."""
+        s = np.ascontiguousarray(signs, dtype=np.int8)
+        if s.shape != (self.dim,):
+            raise ValueError(f"signs must be [{self.dim}], got {list(s.shape)}")
+        _check(lib().chimera_builder_rabitq(self._h, _np(s)))
+
     def quantizer(self) -> Tuple[np.ndarray, np.ndarray]:
         B = 1 << self.nbits
         cut = np.empty(B - 1, np.int32)
@@ -166,6 +177,15 @@ class Builder:
         st = _Info()
         _check(lib().chimera_builder_info(self._h, ctypes.byref(st)))
         return _info(st)
+
+    def rabitq_sections(self) -> dict:
+        """Host copies of the RaBitQ sections (chimera_builder_rabitq_sections)."""
+        n = self.info()["ntokens"]
+        out = dict(bits1=np.empty((n, self.dim // 8), np.uint8), g1=np.empty(n, np.float32),
+                   codes4=np.empty((n, self.dim // 2), np.uint8), g4=np.empty(n, np.float32))
+        _check(lib().chimera_builder_rabitq_sections(self._h, _np(out["bits1"]), _np(out["g1"]), _np(out["codes4"]),
+                                                     _np(out["g4"])))
+        return out
 
     def sections(self, which=("doc_off", "cid", "codes", "ivf_off", "ivf_doc")) -> dict:
         """Host copies of the built sections named in `which`."""
@@ -188,11 +208,15 @@ class Builder:
 
 
 def build_index(centroids_bf16: np.ndarray, nbits: int,
-                chunks: Callable[[], Iterable[Tuple[np.ndarray, np.ndarray, np.ndarray]]]) -> Builder:
+                chunks: Callable[[], Iterable[Tuple[np.ndarray, np.ndarray, np.ndarray]]],
+                rabitq_signs: np.ndarray | None = None) -> Builder:
     """Two-pass streaming build.  ``chunks()`` must yield the same sequence of
     (tokens_bf16 [rows,dim], cids [rows], doc_lens [ndocs_chunk]) each time it
-    is called, covering every document in order."""
+    is called, covering every document in order.  rabitq_signs: also encode
+    RaBitQ codes (Builder.rabitq)."""
     b = Builder(centroids_bf16, nbits)
+    if rabitq_signs is not None:
+        b.rabitq(rabitq_signs)
     for tok, cid, _ in chunks():
         b.add_residuals(tok, cid)
     b.freeze()
@@ -299,6 +323,21 @@ class Index:
             _check(lib().chimera_search_refine(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand,
                                                k, refine, ctypes.c_void_p(ids.data_ptr()),
                                                ctypes.c_void_p(scores.data_ptr()), _stream_ptr(stream)))
+        return ids, scores
+
+    def search_rabitq(self, Q, nprobe: int, ncand: int, k: int, out=None, stream=None):
+        """chimera_search_rabitq: step 4 scored from the RaBitQ 1-bit codes."""
+        import torch
+        Q, dt = self._q(Q)
+        nq, Tq, d = Q.shape
+        if out is None:
+            ids = torch.empty((nq, k), dtype=torch.int32, device=Q.device)
+            scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
+        else:
+            ids, scores = out
+        _check(lib().chimera_search_rabitq(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, k,
+                                           ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(scores.data_ptr()),
+                                           _stream_ptr(stream)))
         return ids, scores
 
     def attach_fullbit(self, tokens_bf16):

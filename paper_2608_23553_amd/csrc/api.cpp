@@ -91,7 +91,8 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
   std::vector<int64_t> tok_off;
   std::vector<int32_t> ivf_tok, tok_doc;
   token_lists(h, tok_off, ivf_tok, tok_doc);
-  struct Sec { void **dst; const void *src; size_t bytes; } secs[] = {
+  struct Sec { void **dst; const void *src; size_t bytes; size_t pad; };
+  std::vector<Sec> secs = {
       {(void **)&idx->d_cent, h.cent.data(), h.cent.size() * 2},
       {(void **)&idx->d_doc_off, h.doc_off.data(), h.doc_off.size() * 8},
       {(void **)&idx->d_cid, h.cid.data(), h.cid.size() * 4},
@@ -104,6 +105,23 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
       {(void **)&idx->d_ivf_tok, ivf_tok.data(), ivf_tok.size() * 4},
       {(void **)&idx->d_tok_doc, tok_doc.data(), tok_doc.size() * 4},
   };
+  // Token arrays (cid, codes, RaBitQ bits and factors) are followed by
+  // kTokenPad zeroed tokens: the scorers read whole 16- or 32-token tiles
+  // and may run up to 31 tokens past the last document.  Every section gets
+  // at least 256 spare bytes.
+  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256, 256,
+                              256, 256, 256, 256};
+  static_assert(sizeof(pad_bytes) / sizeof(pad_bytes[0]) == 11, "one pad per section");
+  for (size_t i = 0; i < secs.size(); ++i) secs[i].pad = pad_bytes[i];
+  if (h.rq) {
+    idx->rq = true;
+    idx->rq_signs = h.rq_signs;
+    idx->rq_codes = h.rq_codes;
+    idx->rq_g4 = h.rq_g4;
+    secs.push_back({(void **)&idx->d_rq_bits, h.rq_bits.data(), h.rq_bits.size(), (size_t)kTokenPad * 16 + 256});
+    secs.push_back({(void **)&idx->d_rq_g1, h.rq_g1.data(), h.rq_g1.size() * 4, (size_t)kTokenPad * 4 + 256});
+    secs.push_back({(void **)&idx->d_rq_signs, h.rq_signs.data(), h.rq_signs.size(), 256});
+  }
   size_t need = 0;
   for (auto &s : secs) need += s.bytes;
   size_t free_b = 0, total_b = 0;
@@ -111,15 +129,8 @@ static int upload(const HostIndex &h, int device, chimera_index **out) {
     delete idx;
     return fail(CHIMERA_E_NOMEM, "index needs %zu bytes, %zu free on device %d", need, free_b, device);
   }
-  // Token arrays (cid, codes) are followed by kTokenPad zeroed tokens: the
-  // residual scorer reads whole 16-token tiles and may run up to 15 tokens
-  // past the last document.  Every section gets at least 256 spare bytes.
-  const size_t pad_bytes[] = {256, 256, kTokenPad * 4 + 256, (size_t)kTokenPad * h.code_bytes() + 256, 256, 256, 256,
-                              256, 256, 256, 256};
-  static_assert(sizeof(pad_bytes) / sizeof(pad_bytes[0]) == sizeof(secs) / sizeof(secs[0]), "one pad per section");
-  int si = 0;
   for (auto &s : secs) {
-    const size_t pad = pad_bytes[si++];
+    const size_t pad = s.pad;
     hipError_t e = hipMalloc(s.dst, s.bytes + pad);
     if (e == hipSuccess) e = hipMemset((char *)*s.dst + s.bytes, 0, pad);
     if (e == hipSuccess && s.bytes) e = hipMemcpy(*s.dst, s.src, s.bytes, hipMemcpyHostToDevice);
@@ -192,6 +203,7 @@ struct Outs {
   int32_t *cand_ids = nullptr, *cand_keys = nullptr, *n_valid = nullptr;         // prune tap
   int32_t *ids = nullptr; float *scores = nullptr;                               // search
   const CollabOut *collab = nullptr;                                             // collaborative scoring
+  bool rabitq = false;                                                           // score from RaBitQ bits
 };
 
 static size_t align_up(size_t x) { return (x + 255) / 256 * 256; }
@@ -208,14 +220,16 @@ struct Carve {
 };
 
 // Exact bytes the sub-batch loop below carves for nb queries.
-static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int nprobe, int ncand, Stop stop) {
+static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int nprobe, int ncand, Stop stop,
+                          bool rq) {
   const int64_t rows = nb * TQP;
   const ProbePlan plan = plan_probe(rows, idx->ncent, nprobe);
   size_t b = 0;
   b += align_up((size_t)rows * 128 * 2);                       // Qs
   b += align_up(probe_part_bytes(plan, rows));                 // partial lists
   b += 2 * align_up((size_t)rows * nprobe * 4);                // cent ids / keys
-  if (stop >= STOP_FULL) b += align_up((size_t)nb * (idx->ncent + 1) * TQP * 4);  // S^T + sentinel rows
+  if (stop >= STOP_FULL && !rq) b += align_up((size_t)nb * (idx->ncent + 1) * TQP * 4);  // S^T + sentinel rows
+  if (rq) b += 2 * align_up((size_t)rows * 128 * 2) + align_up((size_t)rows * 4);  // Qh, Ql, qsum
   if (stop >= STOP_CANDIDATES) {
     b += align_up((size_t)nb * idx->ndocs * 4);  // F'
     b += align_up((size_t)nb * 4096 * 4);        // select histogram
@@ -300,7 +314,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
   int64_t lo = 1, hi = std::min<int64_t>(nq, 65535);
   while (lo < hi) {
     const int64_t mid = lo + (hi - lo + 1) / 2;
-    if (carve_bytes(idx, mid, TQP, nprobe, ncand, stop) <= budget) lo = mid;
+    if (carve_bytes(idx, mid, TQP, nprobe, ncand, stop, o.rabitq) <= budget) lo = mid;
     else hi = mid - 1;
   }
   int64_t B = lo;
@@ -308,8 +322,8 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
   const int64_t npass = (nq + B - 1) / B;
   B = (nq + npass - 1) / npass;
   auto need_for = [&](int64_t b) {
-    size_t n = carve_bytes(idx, b, TQP, nprobe, ncand, stop);
-    if (nq % b) n = std::max(n, carve_bytes(idx, nq % b, TQP, nprobe, ncand, stop));
+    size_t n = carve_bytes(idx, b, TQP, nprobe, ncand, stop, o.rabitq);
+    if (nq % b) n = std::max(n, carve_bytes(idx, nq % b, TQP, nprobe, ncand, stop, o.rabitq));
     return n;
   };
   size_t need = need_for(B);
@@ -351,7 +365,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     uint64_t *part = cv.take<uint64_t>(probe_part_bytes(plan, rows) / 8);
     int32_t *ci = cv.take<int32_t>((size_t)rows * nprobe);
     int32_t *ck = cv.take<int32_t>((size_t)rows * nprobe);
-    float *ST = stop >= STOP_FULL ? cv.take<float>((size_t)nb * (idx->ncent + 1) * TQP) : nullptr;
+    float *ST = stop >= STOP_FULL && !o.rabitq ? cv.take<float>((size_t)nb * (idx->ncent + 1) * TQP) : nullptr;
     if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
     const size_t qbytes = (size_t)Tq * 128 * (q_dtype == CHIMERA_F32 ? 4 : 2);
     const void *Qb = (const char *)Q + (size_t)q0 * qbytes;
@@ -420,8 +434,17 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
       continue;
     }
     stage_mark(idx, s, mark);
-    launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
-                          idx->h_weights, cand, nval, ncand, 0, ncand, fhat, s);
+    if (o.rabitq) {
+      uint32_t *Qh = cv.take<uint32_t>((size_t)rows * 64), *Ql = cv.take<uint32_t>((size_t)rows * 64);
+      float *qsum = cv.take<float>((size_t)rows);
+      if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+      launch_rq_prep(Qs, rows, idx->d_rq_signs, Qh, Ql, qsum, s);
+      launch_rq_score(Qh, Ql, qsum, nb, TQP, idx->d_doc_off, idx->d_rq_bits, idx->d_rq_g1, cand, nval, ncand, 0,
+                      ncand, fhat, s);
+    } else {
+      launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
+                            idx->h_weights, cand, nval, ncand, 0, ncand, fhat, s);
+    }
     stage_mark(idx, s, mark);
     launch_topk(fhat, cand, nval, nb, ncand, k, o.ids + q0 * k, o.scores + q0 * k, s);
     stage_mark(idx, s, mark);
@@ -468,7 +491,8 @@ void chimera_index_free(chimera_index *idx) {
   (void)hipDeviceSynchronize();
   void *ptrs[] = {idx->d_cent,    idx->d_doc_off,    idx->d_cid,       idx->d_codes,     idx->d_ivf_off,
                   idx->d_ivf_doc, idx->d_dense_slot, idx->d_doc_dense, idx->d_tok_off,   idx->d_ivf_tok,
-                  idx->d_tok_doc, idx->scratch,      idx->d_check,     idx->d_deleted};
+                  idx->d_tok_doc, idx->scratch,      idx->d_check,     idx->d_deleted,   idx->d_rq_bits,
+                  idx->d_rq_g1,   idx->d_rq_signs};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   collab_free(idx);
@@ -557,13 +581,35 @@ int chimera_index_compact(chimera_index *idx) {
     h.codes.resize((size_t)(h.ntok * cb));
     std::vector<int16_t> fullbit;
     if (!idx->fullbit.empty()) fullbit.resize((size_t)h.ntok * idx->dim);
+    // RaBitQ codes: bits and factors from the device, 4-bit codes from host
+    const int64_t b1 = idx->dim / 8, b4 = idx->dim / 2;
+    std::vector<uint8_t> rq_bits;
+    std::vector<float> rq_g1;
+    if (idx->rq) {
+      rq_bits.resize((size_t)(idx->ntok * b1));
+      rq_g1.resize((size_t)idx->ntok);
+      CHIMERA_HIP(hipMemcpy(rq_bits.data(), idx->d_rq_bits, rq_bits.size(), hipMemcpyDeviceToHost));
+      CHIMERA_HIP(hipMemcpy(rq_g1.data(), idx->d_rq_g1, rq_g1.size() * 4, hipMemcpyDeviceToHost));
+      h.rq = true;
+      h.rq_signs = idx->rq_signs;
+      h.rq_bits.resize((size_t)(h.ntok * b1));
+      h.rq_g1.resize((size_t)h.ntok);
+      h.rq_codes.resize((size_t)(h.ntok * b4));
+      h.rq_g4.resize((size_t)h.ntok);
+    }
     for (int64_t v = 0; v < idx->ndocs; ++v) {
       const int64_t len = h.doc_off[v + 1] - h.doc_off[v];
       if (!len) continue;
-      std::memcpy(&h.cid[h.doc_off[v]], &cid[off[v]], len * 4);
-      std::memcpy(&h.codes[h.doc_off[v] * cb], &codes[off[v] * cb], len * cb);
-      if (!fullbit.empty())
-        std::memcpy(&fullbit[h.doc_off[v] * idx->dim], &idx->fullbit[off[v] * idx->dim], len * idx->dim * 2);
+      const int64_t to = h.doc_off[v], from = off[v];
+      std::memcpy(&h.cid[to], &cid[from], len * 4);
+      std::memcpy(&h.codes[to * cb], &codes[from * cb], len * cb);
+      if (!fullbit.empty()) std::memcpy(&fullbit[to * idx->dim], &idx->fullbit[from * idx->dim], len * idx->dim * 2);
+      if (idx->rq) {
+        std::memcpy(&h.rq_bits[to * b1], &rq_bits[from * b1], len * b1);
+        std::memcpy(&h.rq_g1[to], &rq_g1[from], len * 4);
+        std::memcpy(&h.rq_codes[to * b4], &idx->rq_codes[from * b4], len * b4);
+        std::memcpy(&h.rq_g4[to], &idx->rq_g4[from], len * 4);
+      }
     }
     std::vector<int32_t>().swap(cid);
     std::vector<uint8_t>().swap(codes);
@@ -575,13 +621,15 @@ int chimera_index_compact(chimera_index *idx) {
     void **mine[] = {(void **)&idx->d_cent,      (void **)&idx->d_doc_off,    (void **)&idx->d_cid,
                      (void **)&idx->d_codes,     (void **)&idx->d_ivf_off,    (void **)&idx->d_ivf_doc,
                      (void **)&idx->d_dense_slot, (void **)&idx->d_doc_dense, (void **)&idx->d_tok_off,
-                     (void **)&idx->d_ivf_tok,   (void **)&idx->d_tok_doc};
+                     (void **)&idx->d_ivf_tok,   (void **)&idx->d_tok_doc,    (void **)&idx->d_rq_bits,
+                     (void **)&idx->d_rq_g1,     (void **)&idx->d_rq_signs};
     void **theirs[] = {(void **)&fresh->d_cent,      (void **)&fresh->d_doc_off,    (void **)&fresh->d_cid,
                        (void **)&fresh->d_codes,     (void **)&fresh->d_ivf_off,    (void **)&fresh->d_ivf_doc,
                        (void **)&fresh->d_dense_slot, (void **)&fresh->d_doc_dense, (void **)&fresh->d_tok_off,
-                       (void **)&fresh->d_ivf_tok,   (void **)&fresh->d_tok_doc};
+                       (void **)&fresh->d_ivf_tok,   (void **)&fresh->d_tok_doc,    (void **)&fresh->d_rq_bits,
+                       (void **)&fresh->d_rq_g1,     (void **)&fresh->d_rq_signs};
     for (size_t i = 0; i < sizeof(mine) / sizeof(mine[0]); ++i) {
-      (void)hipFree(*mine[i]);
+      if (*mine[i]) (void)hipFree(*mine[i]);
       *mine[i] = *theirs[i];
       *theirs[i] = nullptr;
     }
@@ -592,6 +640,8 @@ int chimera_index_compact(chimera_index *idx) {
     idx->device_bytes = fresh->device_bytes;
     idx->h_doc_off.swap(fresh->h_doc_off);
     idx->fullbit.swap(fullbit);
+    idx->rq_codes.swap(fresh->rq_codes);
+    idx->rq_g4.swap(fresh->rq_g4);
     chimera_index_free(fresh);
     return CHIMERA_OK;
   });
@@ -607,7 +657,7 @@ int chimera_search(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, i
 // scratch (chimera_search_noalloc).
 static int search_common(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
                          int32_t nprobe, int32_t ncand, int32_t k, int32_t refine, int32_t *ids, float *scores,
-                         void *hip_stream, bool fixed) {
+                         void *hip_stream, bool fixed, bool rabitq = false) {
   int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe, refine);
   if (rc) return rc;
   if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
@@ -615,6 +665,7 @@ static int search_common(chimera_index *idx, const void *Q, int q_dtype, int64_t
   if (k > kMaxK) return fail(CHIMERA_E_UNSUPPORTED, "k %d > %d", k, kMaxK);
   if (ncand > CHIMERA_MAX_NCAND) return fail(CHIMERA_E_UNSUPPORTED, "ncand %d > %d", ncand, CHIMERA_MAX_NCAND);
   if (nq > 0 && (!ids || !scores)) return fail(CHIMERA_E_INVAL, "null output pointer");
+  if (rabitq && !idx->rq) return fail(CHIMERA_E_UNSUPPORTED, "the index holds no RaBitQ codes");
   if (nq == 0) return CHIMERA_OK;
   BusyGuard bg(idx);
   if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
@@ -631,6 +682,7 @@ static int search_common(chimera_index *idx, const void *Q, int q_dtype, int64_t
   Outs o;
   o.ids = ids;
   o.scores = scores;
+  o.rabitq = rabitq;
   return guarded([&] {
     return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, k, STOP_FULL, o, (hipStream_t)hip_stream, refine, fs);
   });
@@ -646,6 +698,12 @@ int chimera_search_noalloc(chimera_index *idx, const void *Q, int q_dtype, int64
                            int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream) {
   return search_common(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, k, CHIMERA_REFINE_CENTROID, ids, scores,
                        hip_stream, true);
+}
+
+int chimera_search_rabitq(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t k, int32_t *ids, float *scores, void *hip_stream) {
+  return search_common(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, k, CHIMERA_REFINE_CENTROID, ids, scores,
+                       hip_stream, false, true);
 }
 
 int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,

@@ -475,11 +475,23 @@ int chimera_builder_add_docs(chimera_builder *b, const uint16_t *tokens_bf16, co
     h.cid.resize(t0);
     h.codes.resize(t0 * cb);
     h.doc_off.resize(ndoc_off);
+    if (h.rq) {
+      h.rq_bits.resize(t0 * (dim / 8));
+      h.rq_codes.resize(t0 * (dim / 2));
+      h.rq_g1.resize(t0);
+      h.rq_g4.resize(t0);
+    }
   };
   try {
     h.cid.resize(t0 + rows);
     h.codes.resize((t0 + rows) * cb);
     h.doc_off.reserve(ndoc_off + ndocs);
+    if (h.rq) {
+      h.rq_bits.resize((t0 + rows) * (dim / 8));
+      h.rq_codes.resize((t0 + rows) * (dim / 2));
+      h.rq_g1.resize(t0 + rows);
+      h.rq_g4.resize(t0 + rows);
+    }
   } catch (...) {
     roll_back();
     return fail(CHIMERA_E_NOMEM, "host allocation for %lld tokens", (long long)rows);
@@ -496,12 +508,30 @@ int chimera_builder_add_docs(chimera_builder *b, const uint16_t *tokens_bf16, co
     roll_back();
     return fail(CHIMERA_E_INVAL, "token components must lie in [-1, 1]");
   }
+  if (h.rq) {  // the tokens are valid: their RaBitQ codes
+    parallel_for(rows, [&](int64_t a, int64_t e) {
+      std::vector<int16_t> kk((size_t)(e - a) * dim);
+      grid_rows(tokens_bf16 + a * dim, (e - a) * dim, kk.data());
+      rabitq_encode_rows(kk.data(), e - a, dim, h.rq_signs.data(), h.rq_bits.data() + (t0 + a) * (dim / 8),
+                         h.rq_g1.data() + t0 + a, h.rq_codes.data() + (t0 + a) * (dim / 2), h.rq_g4.data() + t0 + a);
+    });
+  }
   std::memcpy(h.cid.data() + t0, cids, rows * 4);
   for (int64_t i = 0; i < ndocs; ++i) h.doc_off.push_back(h.doc_off.back() + doc_lens[i]);
   h.max_doc_len = std::max(h.max_doc_len, longest);
   h.ntok = t0 + rows;
   h.ndocs += ndocs;
   b->lists_built = false;
+  return CHIMERA_OK;
+}
+
+int chimera_builder_rabitq(chimera_builder *b, const int8_t *signs) {
+  if (!b || !signs) return fail(CHIMERA_E_INVAL, "null argument");
+  if (b->h.ntok > 0) return fail(CHIMERA_E_INVAL, "enable RaBitQ codes before adding documents");
+  for (int d = 0; d < b->h.dim; ++d)
+    if (signs[d] != 1 && signs[d] != -1) return fail(CHIMERA_E_INVAL, "sign %d is %d, not +1 or -1", d, signs[d]);
+  b->h.rq = true;
+  b->h.rq_signs.assign(signs, signs + b->h.dim);
   return CHIMERA_OK;
 }
 
@@ -529,6 +559,7 @@ int chimera_builder_quantizer(const chimera_builder *b, int32_t *cut_k, uint16_t
 int chimera_builder_save(const chimera_builder *b, const char *path) {
   if (!b || !path) return fail(CHIMERA_E_INVAL, "null argument");
   if (!b->frozen) return fail(CHIMERA_E_INVAL, "quantiser not frozen");
+  if (b->h.rq) return fail(CHIMERA_E_UNSUPPORTED, "index files do not hold RaBitQ codes");
   build_lists(const_cast<chimera_builder *>(b));
   return save_index(b->h, path);
 }
@@ -543,6 +574,18 @@ int chimera_builder_sections(const chimera_builder *b, int64_t *doc_off, int32_t
   if (codes) std::memcpy(codes, h.codes.data(), h.codes.size());
   if (ivf_off) std::memcpy(ivf_off, h.ivf_off.data(), h.ivf_off.size() * 8);
   if (ivf_doc) std::memcpy(ivf_doc, h.ivf_doc.data(), h.ivf_doc.size() * 4);
+  return CHIMERA_OK;
+}
+
+int chimera_builder_rabitq_sections(const chimera_builder *b, uint8_t *bits1, float *g1, uint8_t *codes4,
+                                    float *g4) {
+  if (!b) return fail(CHIMERA_E_INVAL, "null builder");
+  const HostIndex &h = b->h;
+  if (!h.rq) return fail(CHIMERA_E_INVAL, "the builder has no RaBitQ codes");
+  if (bits1) std::memcpy(bits1, h.rq_bits.data(), h.rq_bits.size());
+  if (g1) std::memcpy(g1, h.rq_g1.data(), h.rq_g1.size() * 4);
+  if (codes4) std::memcpy(codes4, h.rq_codes.data(), h.rq_codes.size());
+  if (g4) std::memcpy(g4, h.rq_g4.data(), h.rq_g4.size() * 4);
   return CHIMERA_OK;
 }
 

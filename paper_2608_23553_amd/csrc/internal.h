@@ -40,8 +40,23 @@ struct HostIndex {
   std::vector<uint16_t> weights;  // bf16 [2^nbits]
   std::vector<int64_t> ivf_off;   // [ncent+1]
   std::vector<int32_t> ivf_doc;   // [nnz]
+  // RaBitQ codes (optional, see rabitq_encode_rows): the signs of the
+  // rotation [dim], per token the packed most significant bits [dim / 8]
+  // and their factor, the packed 4-bit codes [dim / 2] and their factor
+  bool rq = false;
+  std::vector<int8_t> rq_signs;
+  std::vector<uint8_t> rq_bits, rq_codes;
+  std::vector<float> rq_g1, rq_g4;
   int64_t code_bytes() const { return (int64_t)dim * nbits / 8; }
 };
+
+// RaBitQ codes with B = 4 of n tokens (grid integers k [n][dim]) under the
+// rotation H diag(signs): bits1 [n][dim / 8] the most significant bits (bit d
+// of a token in byte d / 8, bit d % 8) and g1 [n] their factor; codes4
+// [n][dim / 2] the 4-bit codes (dim 2i in the low nibble of byte i, 2i + 1 in
+// the high nibble) and g4 [n] their factor.  rabitq.cpp states the reading.
+void rabitq_encode_rows(const int16_t *k, int64_t n, int dim, const int8_t *signs, uint8_t *bits1, float *g1,
+                        uint8_t *codes4, float *g4);
 
 int save_index(const HostIndex &h, const char *path);
 // Dense posting lists: up to kMaxDense centroids whose doc-level list holds
@@ -137,6 +152,18 @@ void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, cons
                            const uint16_t *weights_host, const int32_t *cand_ids, const int32_t *n_valid,
                            int ncand, int lo, int hi, int32_t *fhat, hipStream_t s);
 
+// RaBitQ document scoring (k_rabitq.hip).  Query preparation: for each of
+// the rows rounded query rows Qs [rows][128], x = H diag(signs) q as bf16
+// hi and lo parts Qh, Ql [rows][64] (two bf16 per word) and qsum [rows] =
+// sum(x).  Scoring: fhat [nq][ncand] i32 keys of candidates lo .. hi-1 of
+// each query (those below n_valid) from the 1-bit codes bits [ntok][16] and
+// factors g1 [ntok] (both padded by kTokenPad tokens).
+void launch_rq_prep(const uint16_t *Qs, int64_t rows, const int8_t *signs, uint32_t *Qh, uint32_t *Ql, float *qsum,
+                    hipStream_t s);
+void launch_rq_score(const uint32_t *Qh, const uint32_t *Ql, const float *qsum, int64_t nq, int TQP,
+                     const int64_t *doc_off, const uint8_t *bits, const float *g1, const int32_t *cand_ids,
+                     const int32_t *n_valid, int ncand, int lo, int hi, int32_t *fhat, hipStream_t s);
+
 // Collaborative scoring of one sub-batch (collab.cpp): ids, scores, n_full
 // are host arrays for the whole batch, written at query q0 onwards.
 struct CollabOut {
@@ -183,6 +210,17 @@ struct chimera_index {
   int ndense = 0;                  // dense posting lists (see dense_lists)
   int8_t *d_dense_slot = nullptr;  // [ncent]
   uint64_t *d_doc_dense = nullptr;  // [ndocs] dense-list masks (see dense_lists)
+  // RaBitQ codes (chimera_builder_rabitq): on the device the most
+  // significant bits [ntok][16] and their factors [ntok] (both padded by
+  // kTokenPad tokens) and the rotation's signs [dim]; in host memory the
+  // 4-bit codes [ntok][dim / 2] and their factors
+  bool rq = false;
+  uint8_t *d_rq_bits = nullptr;
+  float *d_rq_g1 = nullptr;
+  int8_t *d_rq_signs = nullptr;
+  std::vector<int8_t> rq_signs;
+  std::vector<uint8_t> rq_codes;
+  std::vector<float> rq_g4;
   int64_t *d_tok_off = nullptr;     // token-level lists (see token_lists)
   int32_t *d_ivf_tok = nullptr;
   int32_t *d_tok_doc = nullptr;

@@ -194,6 +194,11 @@ def k_to_bf16_bits(k: np.ndarray) -> np.ndarray:
     return (bits >> 16).astype(np.uint16)
 
 
+def rotation_signs(seed: int, dim: int = 128) -> np.ndarray:
+    """Random signs (int8 +-1 [dim]) of a RaBitQ rotation, seeded."""
+    return np.where(np.random.default_rng(seed).random(dim) < 0.5, -1, 1).astype(np.int8)
+
+
 def splitmix64_at(state: int, n: int) -> int:
     return int(_load().synth_splitmix64_at(state, n))
 

@@ -18,5 +18,6 @@ def chunk_factory(corpus, docs_per_chunk=20_000):
     return gen
 
 
-def product_builder(corpus, nbits, docs_per_chunk=20_000):
-    return build_index(synth.k_to_bf16_bits(corpus.centroids_k), nbits, chunk_factory(corpus, docs_per_chunk))
+def product_builder(corpus, nbits, docs_per_chunk=20_000, rabitq_signs=None):
+    return build_index(synth.k_to_bf16_bits(corpus.centroids_k), nbits, chunk_factory(corpus, docs_per_chunk),
+                       rabitq_signs=rabitq_signs)
