@@ -423,6 +423,33 @@ def search_rabitq(oi, q_k, nprobe: int, ncand: int, k: int, signs, B: int, codes
     return dict(ids=ids, keys=keys, scores=keys_to_scores(keys))
 
 
+def search_collab_rabitq(oi, q_k, nprobe: int, ncand: int, kfb: int, chunks: int, k: int, signs, B: int,
+                         codes, g1, gB):
+    """Alg. 3 with the paper's code split (Sec. 3.1): steps 1-3 as orc_search,
+    the GPU-side score of each kept document from the 1-bit part of its
+    RaBitQ codes and the CPU-side score from the whole B-bit codes
+    (rabitq_doc_scores with bits 1 and bits B), through
+    collaborative_scoring."""
+    q_k = _c(q_k, np.int16)
+    nq = q_k.shape[0]
+    nc = min(ncand, oi.ndocs)
+    pr = oi.prune(q_k, nprobe, nc)
+    out = dict(ids=np.empty((nq, k), np.int32), keys=np.empty((nq, k), np.int64), n_full=np.empty(nq, np.int64))
+    lens = np.diff(oi.doc_off)
+    for qi in range(nq):
+        r = np.sort(pr["cand"][qi, :pr["n_cand"][qi]]).astype(np.int32)
+        fh = rabitq_doc_scores(q_k[qi], signs, B, 1, oi.doc_off[r], lens[r].astype(np.int32), codes, g1)
+
+        def full(d, q=q_k[qi]):
+            return rabitq_doc_scores(q, signs, B, B, oi.doc_off[d:d + 1], lens[d:d + 1].astype(np.int32), codes,
+                                     gB)[0]
+
+        ids, keys, nf = collaborative_scoring(r, fh, full, nc, kfb, chunks, k)
+        out["ids"][qi], out["keys"][qi], out["n_full"][qi] = ids, keys, nf
+    out["scores"] = keys_to_scores(out["keys"])
+    return out
+
+
 # ------------------------------------------------------- oracle index
 class OracleIndex:
     """The oracle's own view of a corpus: assignment given by the corpus,

@@ -142,3 +142,25 @@ def test_fine_codes_approach_the_exact_chamfer_score():
             ex = oracle.exact_chamfer(q[qi], k, c.doc_off)[docs]
             errs.append(np.abs(f - ex) * 2.0 ** -22 / w.Tq)
         assert np.mean(errs) < tol, (B, bits, np.mean(errs))
+
+
+def test_collab_with_full_budget_is_the_top_k_of_4bit_scores():
+    """kfb = ncand with one chunk scores every kept document from its 4-bit
+    codes, so Alg. 3 returns the top-k of those scores; the 1-bit scores only
+    order the work."""
+    w, c, k, cl = corpus("tiny")
+    from util_corpus import oracle_index
+    oi = oracle_index("tiny")
+    s = _signs(np.random.default_rng(6), 128)
+    codes, g4, g1 = oracle.rabitq_encode(k, s, 4)
+    q, _ = c.queries(4, w.Tq)
+    nc = 40
+    out = oracle.search_collab_rabitq(oi, q, w.nprobe, nc, nc, 1, w.k, s, 4, codes, g1, g4)
+    pr = oi.prune(q, w.nprobe, nc)
+    lens = np.diff(c.doc_off)
+    for qi in range(len(q)):
+        r = np.sort(pr["cand"][qi, :pr["n_cand"][qi]]).astype(np.int32)
+        f4 = oracle.rabitq_doc_scores(q[qi], s, 4, 4, c.doc_off[r], lens[r].astype(np.int32), codes, g4)
+        ids, keys = oracle.topk(r, f4, w.k)
+        assert np.array_equal(out["ids"][qi, :len(ids)], ids) and np.array_equal(out["keys"][qi, :len(ids)], keys)
+        assert out["n_full"][qi] == len(r)
