@@ -364,6 +364,18 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
                           int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
                           float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream);
 
+/* chimera_search_collab with the paper's code split (Sec. 3.1): the GPU
+ * scores each chunk from the RaBitQ 1-bit codes (the F^ of
+ * chimera_search_rabitq) and the host's score of a document is its score
+ * from the 4-bit RaBitQ codes held in host memory,
+ *   F(V) = sum_j key(max_{t in V} g4_t * <P' Q_j, 2 y_t> * 2^-12),
+ * (y_t the token's 4-bit codeword, key as in chimera_search_rabitq),
+ * instead of the full-precision score; no store needs attaching.
+ * E_UNSUPPORTED without RaBitQ codes (chimera_builder_rabitq). */
+int chimera_search_collab_rabitq(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                                 int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
+                                 float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream);
+
 /* Stage taps: the same inputs as chimera_search, stopping after a stage.
  * They exist so that each stage can be compared with an independent
  * reference; they cost as much as the stages they run. */

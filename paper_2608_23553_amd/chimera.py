@@ -77,6 +77,8 @@ def lib():
         "chimera_stage_times": ([P, P], INT),
         "chimera_fullbit_attach": ([P, P, I64], INT),
         "chimera_search_collab": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, I32, P, P, P, I32, P], INT),
+        "chimera_search_collab_rabitq": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, I32, P, P, P, I32, P],
+                                         INT),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -365,6 +367,20 @@ class Index:
         _check(lib().chimera_search_collab(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe, ncand, kfb,
                                            chunks, k, _np(ids), _np(scores), _np(n_full), nthreads,
                                            _stream_ptr(stream)))
+        return ids, scores, n_full
+
+    def search_collab_rabitq(self, Q, nprobe: int, ncand: int, kfb: int, chunks: int, k: int, nthreads: int = 0,
+                             stream=None):
+        """chimera_search_collab_rabitq: GPU 1-bit RaBitQ scores, host 4-bit
+        RaBitQ scores (host numpy ids, scores, n_full)."""
+        Q, dt = self._q(Q)
+        nq, Tq, d = Q.shape
+        ids = np.empty((nq, k), dtype=np.int32)
+        scores = np.empty((nq, k), dtype=np.float32)
+        n_full = np.empty(nq, dtype=np.int32)
+        _check(lib().chimera_search_collab_rabitq(self._h, ctypes.c_void_p(Q.data_ptr()), dt, nq, Tq, d, nprobe,
+                                                  ncand, kfb, chunks, k, _np(ids), _np(scores), _np(n_full),
+                                                  nthreads, _stream_ptr(stream)))
         return ids, scores, n_full
 
     def search_raw(self, q_ptr: int, q_dtype: int, nq: int, Tq: int, d: int, nprobe: int, ncand: int, k: int,

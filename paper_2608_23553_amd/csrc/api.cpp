@@ -428,19 +428,25 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     launch_select(fp, hist, nb, idx->ndocs, ncand, selw, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
+    // RaBitQ scoring: the rotated queries as bf16 hi and lo parts
+    RqQuery rq;
+    if (o.rabitq) {
+      rq.Qh = cv.take<uint32_t>((size_t)rows * 64);
+      rq.Ql = cv.take<uint32_t>((size_t)rows * 64);
+      rq.qsum = cv.take<float>((size_t)rows);
+      if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
+      launch_rq_prep(Qs, rows, idx->d_rq_signs, rq.Qh, rq.Ql, rq.qsum, s);
+    }
     if (stop == STOP_COLLAB) {
-      rc = collab_subbatch(idx, s, Qs, nb, q0, Tq, TQP, ST, cand, nval, ncand, fhat, *o.collab);
+      rc = collab_subbatch(idx, s, Qs, nb, q0, Tq, TQP, ST, o.rabitq ? &rq : nullptr, cand, nval, ncand, fhat,
+                           *o.collab);
       if (rc) return rc;
       continue;
     }
     stage_mark(idx, s, mark);
     if (o.rabitq) {
-      uint32_t *Qh = cv.take<uint32_t>((size_t)rows * 64), *Ql = cv.take<uint32_t>((size_t)rows * 64);
-      float *qsum = cv.take<float>((size_t)rows);
-      if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
-      launch_rq_prep(Qs, rows, idx->d_rq_signs, Qh, Ql, qsum, s);
-      launch_rq_score(Qh, Ql, qsum, nb, TQP, idx->d_doc_off, idx->d_rq_bits, idx->d_rq_g1, cand, nval, ncand, 0,
-                      ncand, fhat, s);
+      launch_rq_score(rq.Qh, rq.Ql, rq.qsum, nb, TQP, idx->d_doc_off, idx->d_rq_bits, idx->d_rq_g1, cand, nval,
+                      ncand, 0, ncand, fhat, s);
     } else {
       launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
                             idx->h_weights, cand, nval, ncand, 0, ncand, fhat, s);
@@ -706,9 +712,9 @@ int chimera_search_rabitq(chimera_index *idx, const void *Q, int q_dtype, int64_
                        hip_stream, false, true);
 }
 
-int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
-                          int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
-                          float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream) {
+static int collab_common(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                         int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
+                         float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream, bool rabitq) {
   int rc = check_query_args(idx, Q, q_dtype, nq, Tq, d, nprobe);
   if (rc) return rc;
   if (k < 1) return fail(CHIMERA_E_INVAL, "k must be >= 1");
@@ -722,7 +728,9 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
   BusyGuard bg(idx);
   if (!bg.ok) return fail(CHIMERA_E_BUSY, "index in use by another thread");
   // read under the guard: attach swaps the store while it holds it
-  if (idx->fullbit.empty()) return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
+  if (rabitq && !idx->rq) return fail(CHIMERA_E_UNSUPPORTED, "the index holds no RaBitQ codes");
+  if (!rabitq && idx->fullbit.empty())
+    return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
   DeviceGuard dg(idx->device);
   if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
   int nc = (int)std::min<int64_t>(ncand, idx->ndocs);
@@ -735,13 +743,29 @@ int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_
   co.ids = ids;
   co.scores = scores;
   co.n_full = n_full;
+  co.rabitq = rabitq;
   Outs o;
   o.collab = &co;
+  o.rabitq = rabitq;
   hipStream_t s = (hipStream_t)hip_stream;
   rc = guarded([&] { return run(idx, Q, q_dtype, nq, Tq, nprobe, nc, 1, STOP_COLLAB, o, s); });
   if (rc) return rc;
   CHIMERA_HIP(hipStreamSynchronize(s));
   return CHIMERA_OK;
+}
+
+int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                          int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
+                          float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream) {
+  return collab_common(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, kfb, chunks, k, ids, scores, n_full, nthreads,
+                       hip_stream, false);
+}
+
+int chimera_search_collab_rabitq(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
+                                 int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
+                                 float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream) {
+  return collab_common(idx, Q, q_dtype, nq, Tq, d, nprobe, ncand, kfb, chunks, k, ids, scores, n_full, nthreads,
+                       hip_stream, true);
 }
 
 int chimera_probe(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d, int32_t nprobe,

@@ -129,6 +129,7 @@ struct Collab {
   std::vector<std::vector<uint8_t>> done;                 // candidate has a full-precision score
   std::vector<std::vector<std::pair<int64_t, int32_t>>> full;  // (F, doc id)
   std::vector<int16_t> qk;                                // [nb][dim/2][TqP][2] query grid integers
+  std::vector<int32_t> xq;                                // [nb][Tq][dim] rotated queries (RaBitQ re-rank)
 };
 
 static void free_pinned(void *&p) {
@@ -338,6 +339,47 @@ static int64_t full_score(const HostKernels &K, const int16_t *qp, int Tq, int T
   return F;
 }
 
+// The host score of a document from its RaBitQ 4-bit codes (codes [L][64],
+// factors g4 [L]) for the rotated query tokens xq [Tq][128] (grid units):
+// sum_j key(max_t g4_t * float(<xq_j, 2y_t> * 2^-12)), 2y = 2 code - 15, key
+// = rint(x * 2^22); <xq_j, 2y_t> is exact in 32 bits for |Q_j| < 2^9.
+static int64_t rq_full_score(const int32_t *xq, int Tq, const uint8_t *codes, const float *g4, int64_t L) {
+  if (L <= 0) return INT64_MIN;
+  float best[CHIMERA_MAX_TQ];
+  for (int j = 0; j < Tq; ++j) best[j] = -INFINITY;
+  int32_t z[CHIMERA_DIM];
+  for (int64_t t = 0; t < L; ++t) {
+    for (int i = 0; i < CHIMERA_DIM / 2; ++i) {
+      const int c = codes[t * (CHIMERA_DIM / 2) + i];
+      z[2 * i] = 2 * (c & 15) - 15;
+      z[2 * i + 1] = 2 * (c >> 4) - 15;
+    }
+    for (int j = 0; j < Tq; ++j) {
+      const int32_t *x = xq + (size_t)j * CHIMERA_DIM;
+      int32_t ip = 0;
+      for (int d = 0; d < CHIMERA_DIM; ++d) ip += x[d] * z[d];
+      const float e = g4[t] * (float)std::ldexp((double)ip, -12);
+      if (e > best[j]) best[j] = e;
+    }
+  }
+  int64_t F = 0;
+  for (int j = 0; j < Tq; ++j) F += (int64_t)std::nearbyint((double)best[j] * 4194304.0);
+  return F;
+}
+
+// x <- H diag(signs) x for one query token (grid units; H the Sylvester
+// Hadamard matrix, by the fast transform)
+static void rq_rotate(const int16_t *row, const int8_t *signs, int32_t *x) {
+  for (int d = 0; d < CHIMERA_DIM; ++d) x[d] = signs[d] * row[d];
+  for (int h = 1; h < CHIMERA_DIM; h <<= 1)
+    for (int i = 0; i < CHIMERA_DIM; i += 2 * h)
+      for (int j = i; j < i + h; ++j) {
+        const int32_t a = x[j], b = x[j + h];
+        x[j] = a + b;
+        x[j + h] = a - b;
+      }
+}
+
 // A host task failed (an allocation): drain the stream, whose copies still
 // target the pinned buffers, then report.
 static int host_failed(hipStream_t s) {
@@ -346,8 +388,8 @@ static int host_failed(hipStream_t s) {
 }
 
 int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64_t nb, int64_t q0, int Tq, int TQP,
-                    const float *ST, const int32_t *cand, const int32_t *nval, int ncand, int32_t *fhat,
-                    const CollabOut &o) {
+                    const float *ST, const RqQuery *rq, const int32_t *cand, const int32_t *nval, int ncand,
+                    int32_t *fhat, const CollabOut &o) {
   if (!idx->collab) idx->collab = new Collab();
   Collab &C = *idx->collab;
   const int nthreads = o.nthreads > 0 ? o.nthreads : (int)std::max(1u, std::thread::hardware_concurrency());
@@ -377,8 +419,12 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
   for (int i = 0; i < c; ++i) {
     const int lo = (int)((int64_t)i * ncand / c), hi = (int)((int64_t)(i + 1) * ncand / c);
     if (hi > lo) {
-      launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,
-                            idx->h_weights, cand, nval, ncand, lo, hi, fhat, s);
+      if (o.rabitq)
+        launch_rq_score(rq->Qh, rq->Ql, rq->qsum, nb, TQP, idx->d_doc_off, idx->d_rq_bits, idx->d_rq_g1, cand, nval,
+                        ncand, lo, hi, fhat, s);
+      else
+        launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes,
+                              idx->nbits, idx->h_weights, cand, nval, ncand, lo, hi, fhat, s);
       CHIMERA_HIP(hipGetLastError());
       CHIMERA_HIP(hipMemcpy2DAsync(C.h_fhat + lo, (size_t)ncand * 4, fhat + lo, (size_t)ncand * 4,
                                    (size_t)(hi - lo) * 4, nb, hipMemcpyDeviceToHost, s));
@@ -403,6 +449,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
   C.full.resize(nb);
   const int TqP = (Tq + kQBlock - 1) / kQBlock * kQBlock;
   C.qk.assign((size_t)nb * TqP * dim, 0);
+  if (o.rabitq) C.xq.assign((size_t)nb * Tq * dim, 0);
   std::atomic<int64_t> bad_query{INT64_MAX};
   if (!C.pool->run(nb, [&](int64_t q) {
     C.ranked[q].clear();
@@ -414,6 +461,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
       K.to_grid(C.h_qs + ((size_t)q * TQP + j) * dim, dim, row);
       for (int d = 0; d < dim; ++d) qp[((size_t)(d >> 1) * TqP + j) * 2 + (d & 1)] = row[d];
       if (!query_in_range(row, dim)) atomic_min(bad_query, q0 + q);
+      if (o.rabitq) rq_rotate(row, idx->rq_signs.data(), C.xq.data() + ((size_t)q * Tq + j) * dim);
     }
   }))
     return host_failed(s);
@@ -446,8 +494,10 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
         if (C.done[q][u]) continue;
         C.done[q][u] = 1;
         const int32_t V = cq[u];
-        const int64_t F = full_score(K, C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V],
-                                     doc_off[V + 1]);
+        const int64_t F =
+            o.rabitq ? rq_full_score(C.xq.data() + (size_t)q * Tq * dim, Tq, idx->rq_codes.data() + doc_off[V] * 64,
+                                     idx->rq_g4.data() + doc_off[V], doc_off[V + 1] - doc_off[V])
+                     : full_score(K, C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V], doc_off[V + 1]);
         C.full[q].emplace_back(F, V);
       }
     }))

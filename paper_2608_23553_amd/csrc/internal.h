@@ -168,13 +168,19 @@ void launch_rq_score(const uint32_t *Qh, const uint32_t *Ql, const float *qsum, 
 // are host arrays for the whole batch, written at query q0 onwards.
 struct CollabOut {
   int kfb = 0, chunks = 1, k = 1, nthreads = 0;
+  bool rabitq = false;  // GPU scores from the RaBitQ bits, host scores from the 4-bit codes
   int32_t *ids = nullptr;
   float *scores = nullptr;
   int32_t *n_full = nullptr;
 };
+// The rotated queries of a sub-batch for RaBitQ scoring (launch_rq_prep).
+struct RqQuery {
+  uint32_t *Qh = nullptr, *Ql = nullptr;
+  float *qsum = nullptr;
+};
 int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64_t nb, int64_t q0, int Tq, int TQP,
-                    const float *ST, const int32_t *cand, const int32_t *nval, int ncand, int32_t *fhat,
-                    const CollabOut &o);
+                    const float *ST, const RqQuery *rq, const int32_t *cand, const int32_t *nval, int ncand,
+                    int32_t *fhat, const CollabOut &o);
 void collab_free(chimera_index *idx);
 
 // The fixed scratch of chimera_search_noalloc (noalloc.hip): its device

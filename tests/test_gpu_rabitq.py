@@ -17,11 +17,13 @@ from util_gpu import q_tensor, say, setup
 pytestmark = pytest.mark.gpu
 
 
-def _rq_index(name, ndocs=None, seed=17):
+def _rq_index(name, ndocs=None, seed=17, with_g4=False):
     w, c, k, cl, oi, _ = setup(name, ndocs)
     signs = synth.rotation_signs(seed)
     idx = product_builder(c, w.nbits, rabitq_signs=signs).upload(0)
     codes, g4, g1 = oracle.rabitq_encode(k, signs, 4)
+    if with_g4:
+        return w, c, k, oi, idx, signs, codes, g1, g4
     return w, c, k, oi, idx, signs, codes, g1
 
 
@@ -93,3 +95,19 @@ def test_rabitq_search_needs_rabitq_codes():
     with pytest.raises(ChimeraError) as e:
         idx.search_rabitq(q_tensor(q, "bf16"), w.nprobe, w.ncand, w.k)
     assert e.value.code == chimera.E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("kfb_mult,chunks", [(2, 1), (3, 4)])
+def test_rabitq_collab_search(kfb_mult, chunks):
+    """Alg. 3 with the code split: GPU 1-bit scores chunk by chunk, host
+    scores from the 4-bit codes."""
+    w, c, k, oi, idx, signs, codes, g1, g4 = _rq_index("tiny", with_g4=True)
+    q, src = c.queries(8, w.Tq, query_seed=21)
+    say("rabitq collab", kfb_mult, chunks)
+    gi, gs, gn = idx.search_collab_rabitq(q_tensor(q, "bf16"), w.nprobe, w.ncand, kfb_mult * w.k, chunks, w.k)
+    ref = oracle.search_collab_rabitq(oi, q, w.nprobe, w.ncand, kfb_mult * w.k, chunks, w.k, signs, 4, codes, g1, g4)
+    assert np.array_equal(gi, ref["ids"])
+    assert np.array_equal(gs, ref["scores"])
+    assert np.array_equal(gn, ref["n_full"])
+    assert np.mean(gi[:, 0] == src) >= 0.8
+    idx.close()
