@@ -117,6 +117,12 @@ void launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 // workgroup can use at most kWalkMaxLds.
 size_t walk_lds_bytes(int TQP, int nprobe, int Tq);
 constexpr size_t kWalkMaxLds = 160 * 1024;
+// The walk for an index without dense lists (k_walk_lists.hip; the same
+// outputs); launch_cand_walk picks it when ndense == 0.
+size_t list_walk_lds_bytes(int TQP, int nprobe, int Tq);
+void launch_list_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
+                      const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent,
+                      const uint64_t *deleted, int32_t *fp, uint32_t *hist, hipStream_t s);
 void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t nq, int Tq, int TQP, int nprobe,
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
                       const int8_t *dense_slot, const uint64_t *doc_dense, const uint64_t *deleted, int32_t *fp,

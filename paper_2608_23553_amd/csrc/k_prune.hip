@@ -78,11 +78,9 @@ constexpr int walk_win() {
   return WALK_SHORT_ENTRIES / (LPT * WALK_THREADS);
 }
 
-// Documents per range: 8192 with 32-bit token masks and fewer than 512
-// lists, else 4096; 2048 with 64-bit masks.
-static inline int walk_range_docs(int TQP, int nprobe, int Tq) {
-  return TQP == 32 ? (nprobe * Tq < 512 ? 8192 : 4096) : 2048;
-}
+// Documents per range: 4096 with 32-bit token masks, 2048 with 64-bit masks
+// (two workgroups per compute unit; 8192 needs one, measured 4x slower).
+static inline int walk_range_docs(int TQP, int, int) { return TQP == 32 ? 4096 : 2048; }
 
 // LDS cursor of a wave's list: entries ivf_doc[beg .. beg + len), pos the
 // first entry not yet credited; t its list index r * Tq + j.
@@ -522,7 +520,9 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
 
 size_t walk_lds_bytes(int TQP, int nprobe, int Tq) {
   if ((size_t)nprobe * Tq > (size_t)WALK_MAX_LISTS) return SIZE_MAX;
-  return walk_lds_layout(walk_range_docs(TQP, nprobe, Tq), TQP == 32 ? 4 : 8, nprobe, Tq).total;
+  // either walk may run (k_walk_lists.hip takes indexes without dense lists)
+  return std::max(walk_lds_layout(walk_range_docs(TQP, nprobe, Tq), TQP == 32 ? 4 : 8, nprobe, Tq).total,
+                  list_walk_lds_bytes(TQP, nprobe, Tq));
 }
 
 template <typename MaskT, int R, int LPT>
@@ -568,12 +568,15 @@ void launch_cand_walk(const int32_t *cent_ids, const int32_t *cent_keys, int64_t
                       const int64_t *ivf_off, const int32_t *ivf_doc, int64_t ndocs, int ncent, int ndense,
                       const int8_t *dense_slot, const uint64_t *doc_dense, const uint64_t *deleted, int32_t *fp, uint32_t *hist,
                       hipStream_t s) {
+  // without dense lists the centroids are used about evenly: each probed list
+  // is walked from memory at its rank (k_walk_lists.hip); measured 2x faster
+  // there than the bucketed walk, which wins on skewed (Zipf) lists
+  if (ndense == 0) {
+    launch_list_walk(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, deleted, fp, hist, s);
+    return;
+  }
   const int lpt = (nprobe * Tq + WALK_THREADS - 1) / WALK_THREADS;  // at most 4 (walk_lds_bytes)
-  const int R = walk_range_docs(TQP, nprobe, Tq);
-  if (TQP == 32 && R == 8192)  // fewer than 512 lists: one per thread
-    launch_walk_t<uint32_t, 8192, 1>(cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent, ndense,
-                                     dense_slot, doc_dense, deleted, fp, hist, s);
-  else if (TQP == 32)
+  if (TQP == 32)
     launch_walk_r<uint32_t, 4096>(lpt, cent_ids, cent_keys, nq, Tq, TQP, nprobe, ivf_off, ivf_doc, ndocs, ncent,
                                   ndense, dense_slot, doc_dense, deleted, fp, hist, s);
   else
@@ -785,7 +788,9 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const int32_t *__restric
 // key u = fp_key(F') finds the ncand-th largest key T and how many documents
 // with key T to keep (the lowest ids): bits 31..20 come from the walk's
 // histogram, bits 19..8 and 7..0 from two histogram passes over the chunks
-// (global atomics, only documents whose higher bits match count).  The last
+// (global atomics, only documents whose higher bits match count).  The middle
+// pass reads F' and lists each chunk's documents at or above the 12-bit
+// prefix, which the last pass reads instead of F'.  The last
 // pass also records, per chunk, how many keys lie above the 24-bit prefix and
 // the chunk's own histogram of the low 8 bits, so that once T is known every
 // chunk's kept and tied counts follow without another pass; the counts are
@@ -833,40 +838,6 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_first(const uint32_t *__r
   if (threadIdx.x == 0) st[q] = SelState{ncand - s_above, (uint32_t)s_bin, 1, 0, 0};
 }
 
-// Histogram pass over one chunk: keys whose top (32 - SHIFT - BITS) bits are
-// the state's prefix, binned by their next BITS bits.
-template <int SHIFT, int BITS>
-__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_hist(const int32_t *__restrict__ fp, int64_t ndocs, int P,
-                                                            const SelState *__restrict__ st,
-                                                            uint32_t *__restrict__ hout) {
-  __shared__ uint32_t h[1 << BITS];
-  const int64_t q = blockIdx.x / P;
-  const int c = blockIdx.x % P;
-  if (st[q].T == 0) return;  // uniform: every hit is kept
-  const uint32_t prefix = st[q].prefix;
-  for (int i = threadIdx.x; i < (1 << BITS); i += SPLIT_THREADS) h[i] = 0;
-  __syncthreads();
-  const int64_t per = sel_chunk_docs(ndocs, P), v0 = min(ndocs, c * per), v1 = min(ndocs, v0 + per);
-  const int32_t *f = fp + q * ndocs;
-  for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += SPLIT_THREADS * SEL_UNROLL) {
-    int32_t x[SEL_UNROLL];
-#pragma unroll
-    for (int i = 0; i < SEL_UNROLL; ++i) {
-      const int64_t v = vb + (int64_t)i * SPLIT_THREADS;
-      x[i] = v < v1 ? f[v] : NO_HIT;
-    }
-#pragma unroll
-    for (int i = 0; i < SEL_UNROLL; ++i) {
-      const uint32_t u = fp_key(x[i]);
-      if (x[i] != NO_HIT && (u >> (SHIFT + BITS)) == prefix) atomicAdd(&h[(u >> SHIFT) & ((1u << BITS) - 1)], 1u);
-    }
-  }
-  __syncthreads();
-  uint32_t *o = hout + q * (1 << BITS);
-  for (int i = threadIdx.x; i < (1 << BITS); i += SPLIT_THREADS)
-    if (h[i]) atomicAdd(&o[i], h[i]);
-}
-
 // Per query: the next bin from a pass's histogram; after the last pass, the
 // threshold key T and the ties to keep.
 template <int BITS, bool LAST>
@@ -890,8 +861,9 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_next(const uint32_t *__re
   }
 }
 
-// Last histogram pass over one chunk (bits 7..0 under the 24-bit prefix), as
-// k_sel_hist, plus the chunk's own record: chunk_hist [256] of those keys and
+// Last histogram pass over one chunk (bits 7..0 under the 24-bit prefix),
+// over the middle pass's list of the chunk (or its F' when that list was not
+// kept), plus the chunk's own record: chunk_hist [256] of those keys and
 // chunk_above, the number of keys above the prefix (every hit when all are
 // kept).
 // The last histogram pass also lists, per chunk and in document order, the
@@ -907,31 +879,30 @@ __host__ __device__ inline int sel_list_cap(int64_t ndocs, int P, int ncand) {
   return (int)std::min<int64_t>(per, 4 * ((int64_t)ncand / P) + 1024);
 }
 
-__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__restrict__ fp, int64_t ndocs, int P,
-                                                            const SelState *__restrict__ st,
-                                                            uint32_t *__restrict__ hout,
-                                                            uint32_t *__restrict__ chunk_hist,
-                                                            uint32_t *__restrict__ chunk_above, int cap,
-                                                            int2 *__restrict__ clist, uint32_t *__restrict__ clen) {
-  __shared__ uint32_t h[256];
-  __shared__ uint32_t s_above;
+// The middle histogram pass over one chunk (bits 19..8 under the 12-bit
+// prefix), which also lists, in document order, the chunk's documents whose
+// top 12 key bits reach the prefix (those above the prefix's bin and those in
+// it: every document the select can keep), so that the last pass reads these
+// lists instead of F'.  A list longer than cap is not kept (clen = SEL_NO_LIST;
+// the last pass then reads the chunk's F').
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_mid(const int32_t *__restrict__ fp, int64_t ndocs, int P,
+                                                           const SelState *__restrict__ st,
+                                                           uint32_t *__restrict__ hout, int cap,
+                                                           int2 *__restrict__ clist, uint32_t *__restrict__ clen) {
+  __shared__ uint32_t h[SEL_BINS];
   __shared__ long long wsum[SPLIT_THREADS / 64];
   __shared__ long long s_tot;
   const int64_t q = blockIdx.x / P;
   const int c = blockIdx.x % P;
-  const bool all = st[q].T == 0;  // uniform: every hit is kept (no list: the write pass reads F')
+  if (st[q].T == 0) return;  // uniform: every hit is kept
   const uint32_t prefix = st[q].prefix;
-  for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) h[i] = 0;
-  if (threadIdx.x == 0) s_above = 0;
+  for (int i = threadIdx.x; i < SEL_BINS; i += SPLIT_THREADS) h[i] = 0;
   __syncthreads();
   const int64_t per = sel_chunk_docs(ndocs, P), v0 = min(ndocs, c * per), v1 = min(ndocs, v0 + per);
   const int32_t *f = fp + q * ndocs;
   int2 *L = clist + ((int64_t)q * P + c) * cap;
-  uint32_t above = 0;
   long long nlist = 0;  // uniform
   const int64_t step = (int64_t)SPLIT_THREADS * SEL_LAST_ITEMS;
-  // 16-byte loads where the row allows it (every F' row starts 16-byte
-  // aligned when ndocs is a multiple of 4, and chunks start at multiples of 16)
   const bool vec = ((uintptr_t)f & 15) == 0 && (v0 & 3) == 0;
   for (int64_t vb = v0; vb < v1; vb += step) {
     const int64_t vt = vb + (int64_t)threadIdx.x * SEL_LAST_ITEMS;
@@ -954,6 +925,96 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__res
     for (int i = 0; i < SEL_LAST_ITEMS; ++i) {
       if (x[i] == NO_HIT) continue;
       const uint32_t u = fp_key(x[i]);
+      if ((u >> 20) > prefix) {
+        flags |= 1 << i;
+      } else if ((u >> 20) == prefix) {
+        atomicAdd(&h[(u >> 8) & (SEL_BINS - 1)], 1u);
+        flags |= 1 << i;
+      }
+    }
+    long long pos = block_exclusive_scan(__popc(flags), wsum, &s_tot);
+    const long long tot = s_tot;
+#pragma unroll
+    for (int i = 0; i < SEL_LAST_ITEMS; ++i)
+      if (flags & (1 << i)) {
+        if (nlist + pos < cap) L[nlist + pos] = make_int2((int)(vt + i), x[i]);
+        ++pos;
+      }
+    nlist += tot;
+  }
+  __syncthreads();
+  uint32_t *o = hout + q * SEL_BINS;
+  for (int i = threadIdx.x; i < SEL_BINS; i += SPLIT_THREADS)
+    if (h[i]) atomicAdd(&o[i], h[i]);
+  if (threadIdx.x == 0) clen[(int64_t)q * P + c] = nlist <= cap ? (uint32_t)nlist : SEL_NO_LIST;
+}
+
+__global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__restrict__ fp, int64_t ndocs, int P,
+                                                            const SelState *__restrict__ st,
+                                                            uint32_t *__restrict__ hout,
+                                                            uint32_t *__restrict__ chunk_hist,
+                                                            uint32_t *__restrict__ chunk_above, int cap,
+                                                            const int2 *__restrict__ mlist,
+                                                            const uint32_t *__restrict__ mlen,
+                                                            int2 *__restrict__ clist, uint32_t *__restrict__ clen) {
+  __shared__ uint32_t h[256];
+  __shared__ uint32_t s_above;
+  __shared__ long long wsum[SPLIT_THREADS / 64];
+  __shared__ long long s_tot;
+  const int64_t q = blockIdx.x / P;
+  const int c = blockIdx.x % P;
+  const bool all = st[q].T == 0;  // uniform: every hit is kept (no list: the write pass reads F')
+  const uint32_t prefix = st[q].prefix;
+  for (int i = threadIdx.x; i < 256; i += SPLIT_THREADS) h[i] = 0;
+  if (threadIdx.x == 0) s_above = 0;
+  __syncthreads();
+  const int64_t per = sel_chunk_docs(ndocs, P), v0 = min(ndocs, c * per), v1 = min(ndocs, v0 + per);
+  const int32_t *f = fp + q * ndocs;
+  int2 *L = clist + ((int64_t)q * P + c) * cap;
+  uint32_t above = 0;
+  long long nlist = 0;  // uniform
+  const int64_t step = (int64_t)SPLIT_THREADS * SEL_LAST_ITEMS;
+  // the middle pass's list of the chunk (documents with the 12-bit prefix or
+  // above, with their F'), when it kept one; else F' itself
+  const uint32_t ml = all ? SEL_NO_LIST : mlen[(int64_t)q * P + c];
+  const bool from_list = ml != SEL_NO_LIST;  // uniform
+  const int2 *M = mlist + ((int64_t)q * P + c) * cap;
+  const int64_t b0 = from_list ? 0 : v0, b1 = from_list ? (int64_t)ml : v1;
+  // 16-byte loads where the row allows it (every F' row starts 16-byte
+  // aligned when ndocs is a multiple of 4, and chunks start at multiples of 16)
+  const bool vec = !from_list && ((uintptr_t)f & 15) == 0 && (v0 & 3) == 0;
+  for (int64_t vb = b0; vb < b1; vb += step) {
+    const int64_t vt = vb + (int64_t)threadIdx.x * SEL_LAST_ITEMS;
+    int32_t x[SEL_LAST_ITEMS], d[SEL_LAST_ITEMS];
+    if (from_list) {
+#pragma unroll
+      for (int i = 0; i < SEL_LAST_ITEMS; ++i) {
+        const int2 e = vt + i < b1 ? M[vt + i] : make_int2(0, NO_HIT);
+        d[i] = e.x;
+        x[i] = e.y;
+      }
+    } else if (vec && vt + SEL_LAST_ITEMS <= v1) {
+#pragma unroll
+      for (int i = 0; i < SEL_LAST_ITEMS; i += 4) {
+        const int4 y = *(const int4 *)(f + vt + i);
+        x[i] = y.x;
+        x[i + 1] = y.y;
+        x[i + 2] = y.z;
+        x[i + 3] = y.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < SEL_LAST_ITEMS; ++i) x[i] = vt + i < v1 ? f[vt + i] : NO_HIT;
+    }
+    if (!from_list) {
+#pragma unroll
+      for (int i = 0; i < SEL_LAST_ITEMS; ++i) d[i] = (int)(vt + i);
+    }
+    int flags = 0;
+#pragma unroll
+    for (int i = 0; i < SEL_LAST_ITEMS; ++i) {
+      if (x[i] == NO_HIT) continue;
+      const uint32_t u = fp_key(x[i]);
       if (all || (u >> 8) > prefix) {
         ++above;
         flags |= 1 << i;
@@ -968,7 +1029,7 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_last(const int32_t *__res
 #pragma unroll
       for (int i = 0; i < SEL_LAST_ITEMS; ++i)
         if (flags & (1 << i)) {
-          if (nlist + pos < cap) L[nlist + pos] = make_int2((int)(vt + i), x[i]);
+          if (nlist + pos < cap) L[nlist + pos] = make_int2(d[i], x[i]);
           ++pos;
         }
       nlist += tot;
@@ -1127,7 +1188,7 @@ size_t select_scratch_bytes(int64_t nq, int64_t ndocs, int ncand) {
   const int P = select_chunks(nq, ndocs);
   const size_t cap = (size_t)sel_list_cap(ndocs, P, ncand);
   return (size_t)nq * (sizeof(SelState) + (SEL_BINS + 256) * 4 + (size_t)P * (24 + 256 * 4 + 4 + 4 + cap * 8)) +
-         512;
+         (size_t)nq * P * (4 + cap * 8) + 1024;
 }
 
 void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t ndocs, int ncand, void *scratch,
@@ -1151,11 +1212,14 @@ void launch_select(const int32_t *fp, const uint32_t *hist, int64_t nq, int64_t 
   uint32_t *clen = chunk_above + (size_t)nq * P;
   const int cap = sel_list_cap(ndocs, P, ncand);
   int2 *clist = (int2 *)(((uintptr_t)(clen + (size_t)nq * P) + 15) & ~(uintptr_t)15);
+  uint32_t *mlen = (uint32_t *)(clist + (size_t)nq * P * cap);
+  int2 *mlist = (int2 *)(((uintptr_t)(mlen + (size_t)nq * P) + 15) & ~(uintptr_t)15);
   const dim3 gq((unsigned)nq), gc((unsigned)(nq * P)), tb(SPLIT_THREADS);
   hipLaunchKernelGGL(k_sel_first, gq, tb, 0, s, hist, ncand, hist2, hist3, st);
-  hipLaunchKernelGGL((k_sel_hist<8, 12>), gc, tb, 0, s, fp, ndocs, P, st, hist2);
+  hipLaunchKernelGGL(k_sel_mid, gc, tb, 0, s, fp, ndocs, P, st, hist2, cap, mlist, mlen);
   hipLaunchKernelGGL((k_sel_next<12, false>), gq, tb, 0, s, hist2, st);
-  hipLaunchKernelGGL(k_sel_last, gc, tb, 0, s, fp, ndocs, P, st, hist3, chunk_hist, chunk_above, cap, clist, clen);
+  hipLaunchKernelGGL(k_sel_last, gc, tb, 0, s, fp, ndocs, P, st, hist3, chunk_hist, chunk_above, cap, mlist, mlen,
+                     clist, clen);
   hipLaunchKernelGGL((k_sel_next<8, true>), gq, tb, 0, s, hist3, st);
   hipLaunchKernelGGL(k_sel_scan, gq, tb, 0, s, P, ncand, st, chunk_hist, chunk_above, counts, cand_ids, cand_keys,
                      n_valid);
