@@ -46,6 +46,28 @@ SOURCE_OF_STAGE = {"probe": "k_probe.hip", "walk": "k_prune.hip", "select": "k_p
                    "score": "k_score.hip", "topk": "k_score.hip", "round": "k_probe.hip"}
 
 
+def host_memory_fits(nbytes: int, cap: float = 240 * 2**30):
+    """Whether a host allocation of nbytes fits beside this process: under
+    the available memory with 16 GiB to spare, and under cap in total."""
+    rss = avail = 0
+    try:
+        with open("/proc/self/status") as f:
+            for line in f:
+                if line.startswith("VmRSS:"):
+                    rss = int(line.split()[1]) * 1024
+        with open("/proc/meminfo") as f:
+            for line in f:
+                if line.startswith("MemAvailable:"):
+                    avail = int(line.split()[1]) * 1024
+    except OSError:
+        return False, "host memory unknown"
+    log(f"host memory: {rss / 2**30:.1f} GiB in use, {avail / 2**30:.0f} GiB available, {nbytes / 2**30:.1f} GiB wanted")
+    if nbytes + 16 * 2**30 > avail or nbytes + rss > cap:
+        return False, (f"the full-precision host store would take {nbytes / 2**30:.0f} GiB beside "
+                       f"{rss / 2**30:.0f} GiB in use ({avail / 2**30:.0f} GiB available)")
+    return True, ""
+
+
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
@@ -228,6 +250,9 @@ def measured_traffic(stage, workload):
     return d.get("hbm_bytes_per_launch")
 
 
+CHIMERA_MAX_NCAND = 1 << 20
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -248,6 +273,8 @@ def main():
                                                          "(default 4 k)")
     ap.add_argument("--chunks", type=int, default=4, help="chunks of the collaborative scoring")
     ap.add_argument("--no-collab", action="store_true", help="skip the collaborative-scoring measurement")
+    ap.add_argument("--no-recall-sweep", action="store_true",
+                    help="skip the QPS / recall sweep over larger nprobe and ncand")
     ap.add_argument("--docs-per-chunk", type=int, default=100_000, help="documents per generated chunk")
     ap.add_argument("--profile", action="store_true",
                     help="warmup + timed steps only (for rocprofv3): no reference, oracle or extra legs")
@@ -453,16 +480,57 @@ def main():
     src_first = float(np.mean(got[:, 0] == q_src[:nr]))
     del ref
 
+    # ---- QPS at fixed recall@k: the same batch with more probed centroids
+    # and more kept candidates, each timed over 2 whole-batch searches
+    sweep, qps_at = None, None
+    if not args.no_recall_sweep:
+        sweep = [{"path": "gpu", "nprobe": w.nprobe, "ncand": w.ncand, "qps": qps, "recall_at_k": recall}]
+        si = torch.empty_like(ids)
+        ss = torch.empty_like(scores)
+        for mp, mc in ((2, 1), (2, 2), (4, 2), (4, 4)):
+            npb, nc = min(64, w.nprobe * mp, w.ncent), min(w.ncand * mc, CHIMERA_MAX_NCAND, w.ndocs)
+            if any(e["nprobe"] == npb and e["ncand"] == nc for e in sweep):
+                continue
+            try:
+                idx.search(Q, npb, nc, w.k, out=(si, ss), refine=rmode)
+            except _ch.ChimeraError as e:  # e.g. a walk state beyond the LDS (Tq x nprobe)
+                sweep.append({"path": "gpu", "nprobe": npb, "ncand": nc, "error": str(e)})
+                log(f"sweep nprobe {npb} ncand {nc}: {e}")
+                continue
+            torch.cuda.synchronize()
+            s0 = time.perf_counter()
+            for _ in range(2):
+                idx.search(Q, npb, nc, w.k, out=(si, ss), refine=rmode)
+            torch.cuda.synchronize()
+            q_s = 2 * w.nq / (time.perf_counter() - s0)
+            g = si[:nr].cpu().numpy()
+            r = float(np.mean([len(set(g[i]) & set(truth[i])) / w.k for i in range(nr)]))
+            sweep.append({"path": "gpu", "nprobe": npb, "ncand": nc, "qps": q_s, "recall_at_k": r})
+            log(f"sweep nprobe {npb} ncand {nc}: {q_s:.0f} QPS, recall@{w.k} {r:.3f}")
+        if len(sweep) > 1 and any("qps" in e for e in sweep[1:]):
+            idx.stage_times()  # drop these searches' events
+        qps_at = {str(t): max((e["qps"] for e in sweep if e.get("recall_at_k", 0) >= t), default=None)
+                  for t in (0.8, 0.9, 0.95)}
+
     # ---- CPU-GPU collaborative scoring (Alg. 3): the GPU path's candidates
-    # re-ranked on the host from the full-precision tokens, chunk by chunk
+    # re-ranked on the host from the full-precision tokens, chunk by chunk.
+    # The store is generated and attached in ranges of documents, so the
+    # process holds it once (150 GB at 8.8M)
     collab = None
     fb_bytes = info["ntokens"] * 2 * 128
-    if not args.no_collab and fb_bytes <= 32 * 2**30:
+    fits, why = host_memory_fits(fb_bytes)
+    if not args.no_collab and fits:
         kfb = args.kfb or 4 * w.k
-        log(f"collaborative scoring: kfb {kfb}, {args.chunks} chunks, {threads} host threads")
-        _, fb, _ = corpus.tokens_ex(want_k=False, want_cluster=False)
-        idx.attach_fullbit(fb)  # the index keeps its own grid copy
-        del fb
+        log(f"collaborative scoring: kfb {kfb}, {args.chunks} chunks, {threads} host threads; "
+            f"attaching a {fb_bytes / 2**30:.1f} GiB full-precision store")
+        t_att = time.perf_counter()
+        step_docs = max(1, int(2**32 // (256 * 180)))  # at most 4 GiB of tokens per range
+        for d0 in range(0, w.ndocs, step_docs):
+            d1 = min(w.ndocs, d0 + step_docs)
+            _, fb, _ = corpus.tokens_ex(d0, d1, want_k=False, want_cluster=False)
+            idx.attach_fullbit_range(fb, int(corpus.doc_off[d0]))  # the index keeps its own grid copy
+            del fb
+        log(f"  attached in {time.perf_counter() - t_att:.1f}s")
         runs = {}
         for c in (args.chunks, 1):
             idx.search_collab(Q, w.nprobe, w.ncand, kfb, c, w.k, nthreads=threads)  # warm-up
@@ -478,8 +546,14 @@ def main():
                   "k_hat_full_bit_mean": float(nfull.mean()), "k_hat_full_bit_max": int(nfull.max()),
                   "recall_at_k": float(np.mean([len(set(cids[i]) & set(truth[i])) / w.k for i in range(nr)])),
                   "recall_queries": nr}
+        log(f"  recall@{w.k} {collab['recall_at_k']:.3f}")
+        if sweep is not None:
+            sweep.append({"path": "collaborative", "nprobe": w.nprobe, "ncand": w.ncand, "kfb": kfb,
+                          "chunks": args.chunks, "qps": qc, "recall_at_k": collab["recall_at_k"]})
+            qps_at = {str(t): max((e["qps"] for e in sweep if e.get("recall_at_k", 0) >= t), default=None)
+                      for t in (0.8, 0.9, 0.95)}
     elif not args.no_collab:
-        collab = {"skipped": f"the full-precision host store would take {fb_bytes / 2**30:.0f} GiB"}
+        collab = {"skipped": why}
 
     # ---- CPU baseline: the oracle, untouched, on a bounded sample
     cpu = None
@@ -496,6 +570,7 @@ def main():
                    "refine": args.refine,
                    "index_device_bytes": info["device_bytes"]},
         "recall_at_k": recall, "recall_queries": nr, "source_doc_top1": src_first, "qps_by_batch": qps_by_batch,
+        "recall_sweep": sweep, "qps_at_recall": qps_at,
         "p50_ms_nq1": float(np.percentile(lat, 50)), "p95_ms_nq1": float(np.percentile(lat, 95)),
         "p99_ms_nq1": float(np.percentile(lat, 99)), "nq1_stages_ms": lat_stage_ms,
         "code_scan_GBps": score_gbs, "probe_TFLOPs": probe_tflops, "stages_ms": stage_ms,

@@ -327,6 +327,19 @@ int chimera_search_noalloc(chimera_index *idx, const void *Q, int q_dtype, int64
  * previous copy, if any, is kept), E_NOMEM if the copy cannot be allocated,
  * E_BUSY during another call on the index.
  *
+ * chimera_fullbit_attach_range: the same store, attached in consecutive
+ * token ranges, so that the caller never holds the whole array (at 600M
+ * tokens it is 150 GB): tokens is a HOST array [n][dim] holding tokens
+ * t0 .. t0+n-1 of the index's token order.  t0 = 0 drops any previous
+ * store and allocates the new one (ntok tokens); each later call must start
+ * where the previous one ended.  The store is complete, and collaborative
+ * searches accept it, once its ranges reach ntok; until then they fail with
+ * E_INVAL.  E_INVAL for a range outside [0, ntok), a range that does not
+ * start where the store ends, or a value outside [-1, 1] (the message names
+ * the first such token; the range is not counted and may be sent again),
+ * E_NOMEM if the store cannot be allocated, E_BUSY during another call on
+ * the index.  Compaction keeps a complete store and drops an incomplete one.
+ *
  * chimera_search_collab: steps 1-3 of chimera_search, then Alg. 3 over each
  * query's kept candidates S_refine, taken in ascending document id:
  *  - chunk i (0 <= i < chunks) is candidates floor(i*ncand/chunks) ..
@@ -360,6 +373,7 @@ int chimera_search_noalloc(chimera_index *idx, const void *Q, int q_dtype, int64
  * and working time per sub-batch to stderr.
  * ===================================================================== */
 int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens, int64_t ntok);
+int chimera_fullbit_attach_range(chimera_index *idx, const uint16_t *tokens, int64_t t0, int64_t n);
 int chimera_search_collab(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int32_t Tq, int32_t d,
                           int32_t nprobe, int32_t ncand, int32_t kfb, int32_t chunks, int32_t k, int32_t *ids,
                           float *scores, int32_t *n_full, int32_t nthreads, void *hip_stream);

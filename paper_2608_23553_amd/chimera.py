@@ -76,6 +76,7 @@ def lib():
         "chimera_prune_refine": ([P, P, INT, I64, I32, I32, I32, I32, I32, P, P, P, P], INT),
         "chimera_stage_times": ([P, P], INT),
         "chimera_fullbit_attach": ([P, P, I64], INT),
+        "chimera_fullbit_attach_range": ([P, P, I64, I64], INT),
         "chimera_search_collab": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, I32, P, P, P, I32, P], INT),
         "chimera_search_collab_rabitq": ([P, P, INT, I64, I32, I32, I32, I32, I32, I32, I32, P, P, P, I32, P],
                                          INT),
@@ -354,6 +355,16 @@ class Index:
         if a.ndim != 2 or a.shape[1] != dim:
             raise ValueError(f"tokens must be [ntok, {dim}], got {list(a.shape)}")
         _check(lib().chimera_fullbit_attach(self._h, _np(a), a.shape[0]))
+
+    def attach_fullbit_range(self, tokens_bf16, t0: int):
+        """Tokens t0 .. t0+n-1 of the full-precision store (chimera_fullbit_attach_range):
+        host uint16 [n, d] bf16 bits; t0 = 0 starts a new store, later ranges
+        follow on."""
+        a = np.ascontiguousarray(tokens_bf16, dtype=np.uint16)
+        dim = self._info["dim"]
+        if a.ndim != 2 or a.shape[1] != dim:
+            raise ValueError(f"tokens must be [n, {dim}], got {list(a.shape)}")
+        _check(lib().chimera_fullbit_attach_range(self._h, _np(a), t0, a.shape[0]))
 
     def search_collab(self, Q, nprobe: int, ncand: int, kfb: int, chunks: int, k: int, nthreads: int = 0,
                       stream=None):

@@ -586,7 +586,9 @@ int chimera_index_compact(chimera_index *idx) {
     h.cid.resize((size_t)h.ntok);
     h.codes.resize((size_t)(h.ntok * cb));
     std::vector<int16_t> fullbit;
-    if (!idx->fullbit.empty()) fullbit.resize((size_t)h.ntok * idx->dim);
+    // a complete store is compacted with the index; one still being attached
+    // range by range is dropped
+    if (!idx->fullbit.empty() && idx->fullbit_filled == idx->ntok) fullbit.resize((size_t)h.ntok * idx->dim);
     // RaBitQ codes: bits and factors from the device, 4-bit codes from host
     const int64_t b1 = idx->dim / 8, b4 = idx->dim / 2;
     std::vector<uint8_t> rq_bits;
@@ -646,6 +648,7 @@ int chimera_index_compact(chimera_index *idx) {
     idx->device_bytes = fresh->device_bytes;
     idx->h_doc_off.swap(fresh->h_doc_off);
     idx->fullbit.swap(fullbit);
+    idx->fullbit_filled = idx->fullbit.empty() ? 0 : idx->ntok;
     idx->rq_codes.swap(fresh->rq_codes);
     idx->rq_g4.swap(fresh->rq_g4);
     chimera_index_free(fresh);
@@ -731,6 +734,9 @@ static int collab_common(chimera_index *idx, const void *Q, int q_dtype, int64_t
   if (rabitq && !idx->rq) return fail(CHIMERA_E_UNSUPPORTED, "the index holds no RaBitQ codes");
   if (!rabitq && idx->fullbit.empty())
     return fail(CHIMERA_E_INVAL, "no full-precision store attached (chimera_fullbit_attach)");
+  if (!rabitq && idx->fullbit_filled != idx->ntok)
+    return fail(CHIMERA_E_INVAL, "full-precision store incomplete: %lld of %lld tokens attached",
+                (long long)idx->fullbit_filled, (long long)idx->ntok);
   DeviceGuard dg(idx->device);
   if (!dg.ok) return fail(CHIMERA_E_DEVICE, "cannot select device %d", idx->device);
   int nc = (int)std::min<int64_t>(ncand, idx->ndocs);

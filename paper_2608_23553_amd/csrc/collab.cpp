@@ -531,6 +531,52 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
 
 using namespace chimera;
 
+// Reads tokens [0, n) of src onto the grid into dst, in parallel slices of
+// whole tokens; returns the first token with a value that is not finite or
+// lies outside [-1, 1], or n when there is none.
+static int64_t fullbit_convert(const uint16_t *src, int64_t n, int16_t *dst) {
+  const HostKernels K = pick_kernels();
+  const unsigned nt = (unsigned)std::max<int64_t>(
+      1, std::min<int64_t>({32, (int64_t)std::thread::hardware_concurrency(), (n + 63) / 64}));
+  std::atomic<int64_t> first_bad{n};
+  auto slice = [&](unsigned w) {
+    const int64_t b = n * w / nt, e = n * (w + 1) / nt;
+    constexpr int64_t kBlock = 64;  // tokens converted, then checked while cached
+    for (int64_t t = b; t < e; t += kBlock) {
+      const int64_t m = std::min(kBlock, e - t);
+      int16_t *g = dst + t * CHIMERA_DIM;
+      K.to_grid(src + t * CHIMERA_DIM, m * CHIMERA_DIM, g);
+      if (grid_in_range(g, m * CHIMERA_DIM)) continue;
+      for (int64_t u = 0; u < m; ++u)
+        if (!grid_in_range(g + u * CHIMERA_DIM, CHIMERA_DIM)) {
+          atomic_min(first_bad, t + u);
+          break;
+        }
+      return;
+    }
+  };
+  std::vector<std::thread> th;
+  th.reserve(nt);
+  {
+    // every started thread is joined, whatever happens after it starts
+    struct JoinAll {
+      std::vector<std::thread> &v;
+      ~JoinAll() {
+        for (auto &t : v)
+          if (t.joinable()) t.join();
+      }
+    } join_all{th};
+    for (unsigned w = 0; w < nt; ++w) {
+      try {
+        th.emplace_back(slice, w);
+      } catch (...) {
+        slice(w);  // no thread available: this slice runs on the calling thread
+      }
+    }
+  }
+  return first_bad.load();
+}
+
 extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens, int64_t ntok) {
   if (!idx) return fail(CHIMERA_E_INVAL, "null index");
   if (tokens && ntok != idx->ntok)
@@ -540,60 +586,64 @@ extern "C" int chimera_fullbit_attach(chimera_index *idx, const uint16_t *tokens
   if (idx->busy.exchange(1) != 0) return fail(CHIMERA_E_BUSY, "index in use by another thread");
   if (!tokens) {
     std::vector<int16_t>().swap(idx->fullbit);
+    idx->fullbit_filled = 0;
     idx->busy.store(0);
     return CHIMERA_OK;
   }
   int rc = CHIMERA_OK;
   try {
-    // read every value onto the grid once, here, in parallel slices of
-    // whole tokens, and find the first token out of range
     std::vector<int16_t> store((size_t)ntok * CHIMERA_DIM);
-    const HostKernels K = pick_kernels();
-    const unsigned nt = std::max(1u, std::min(32u, std::thread::hardware_concurrency()));
-    std::atomic<int64_t> first_bad{ntok};
-    auto slice = [&](unsigned w) {
-      const int64_t b = ntok * w / nt, e = ntok * (w + 1) / nt;
-      constexpr int64_t kBlock = 64;  // tokens converted, then checked while cached
-      for (int64_t t = b; t < e; t += kBlock) {
-        const int64_t n = std::min(kBlock, e - t);
-        int16_t *g = store.data() + t * CHIMERA_DIM;
-        K.to_grid(tokens + t * CHIMERA_DIM, n * CHIMERA_DIM, g);
-        if (grid_in_range(g, n * CHIMERA_DIM)) continue;
-        for (int64_t u = 0; u < n; ++u)
-          if (!grid_in_range(g + u * CHIMERA_DIM, CHIMERA_DIM)) {
-            atomic_min(first_bad, t + u);
-            break;
-          }
-        return;
-      }
-    };
-    std::vector<std::thread> th;
-    th.reserve(nt);
-    {
-      // every started thread is joined, whatever happens after it starts
-      struct JoinAll {
-        std::vector<std::thread> &v;
-        ~JoinAll() {
-          for (auto &t : v)
-            if (t.joinable()) t.join();
-        }
-      } join_all{th};
-      for (unsigned w = 0; w < nt; ++w) {
-        try {
-          th.emplace_back(slice, w);
-        } catch (...) {
-          slice(w);  // no thread available: this slice runs on the calling thread
-        }
-      }
-    }
-    if (first_bad.load() < ntok)
+    const int64_t bad = fullbit_convert(tokens, ntok, store.data());
+    if (bad < ntok) {
       rc = fail(CHIMERA_E_INVAL, "full-precision token %lld has a value that is not finite or outside [-1, 1]",
-                (long long)first_bad.load());
-    else
+                (long long)bad);
+    } else {
       idx->fullbit.swap(store);
+      idx->fullbit_filled = ntok;
+    }
   } catch (const std::bad_alloc &) {
     rc = fail(CHIMERA_E_NOMEM, "full-precision store of %lld tokens", (long long)ntok);
   } catch (...) {
+    rc = fail(CHIMERA_E_NOMEM, "full-precision store: host allocation failed");
+  }
+  idx->busy.store(0);
+  return rc;
+}
+
+extern "C" int chimera_fullbit_attach_range(chimera_index *idx, const uint16_t *tokens, int64_t t0, int64_t n) {
+  if (!idx) return fail(CHIMERA_E_INVAL, "null index");
+  if (t0 < 0 || n < 0 || t0 > idx->ntok || n > idx->ntok - t0)
+    return fail(CHIMERA_E_INVAL, "token range [%lld, %lld + %lld) outside the index's %lld tokens", (long long)t0,
+                (long long)t0, (long long)n, (long long)idx->ntok);
+  if (n > 0 && !tokens) return fail(CHIMERA_E_INVAL, "null tokens");
+  if (idx->busy.exchange(1) != 0) return fail(CHIMERA_E_BUSY, "index in use by another thread");
+  int rc = CHIMERA_OK;
+  try {
+    if (t0 == 0) {
+      // a new store: the previous one, complete or not, is dropped first, so
+      // that the two never coexist in host memory
+      std::vector<int16_t>().swap(idx->fullbit);
+      idx->fullbit_filled = 0;
+      idx->fullbit.resize((size_t)idx->ntok * CHIMERA_DIM);
+    }
+    if (t0 != idx->fullbit_filled || idx->fullbit.size() != (size_t)idx->ntok * CHIMERA_DIM) {
+      rc = fail(CHIMERA_E_INVAL, "token range starts at %lld; the store being attached holds %lld tokens",
+                (long long)t0, (long long)idx->fullbit_filled);
+    } else {
+      const int64_t bad = fullbit_convert(tokens, n, idx->fullbit.data() + t0 * CHIMERA_DIM);
+      if (bad < n)
+        rc = fail(CHIMERA_E_INVAL, "full-precision token %lld has a value that is not finite or outside [-1, 1]",
+                  (long long)(t0 + bad));
+      else
+        idx->fullbit_filled = t0 + n;
+    }
+  } catch (const std::bad_alloc &) {
+    std::vector<int16_t>().swap(idx->fullbit);
+    idx->fullbit_filled = 0;
+    rc = fail(CHIMERA_E_NOMEM, "full-precision store of %lld tokens", (long long)idx->ntok);
+  } catch (...) {
+    std::vector<int16_t>().swap(idx->fullbit);
+    idx->fullbit_filled = 0;
     rc = fail(CHIMERA_E_NOMEM, "full-precision store: host allocation failed");
   }
   idx->busy.store(0);

@@ -256,6 +256,7 @@ struct chimera_index {
   // CPU-GPU collaborative scoring (collab.cpp)
   std::vector<int64_t> h_doc_off;      // host copy of doc_off [ndocs + 1]
   std::vector<int16_t> fullbit;        // full-precision tokens [ntok][dim], grid integers
+  int64_t fullbit_filled = 0;          // tokens of fullbit written; complete at ntok
   chimera::Collab *collab = nullptr;   // pinned staging, events, host threads
   // per-stage timing
   bool timing = false;

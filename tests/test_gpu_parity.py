@@ -448,6 +448,49 @@ def test_collab_store_out_of_range_is_refused():
         assert np.array_equal(x, y)
 
 
+def test_collab_store_attached_in_ranges():
+    """The store attached range by range gives the same results as the whole
+    array at once; an incomplete store, a range that does not follow on, and
+    a range past the end are refused; a bad value names its global token and
+    the range can be sent again; t0 = 0 starts over."""
+    w, c, k_, cl, oi, idx = setup("tiny")
+    good = synth.k_to_bf16_bits(k_)
+    q, _ = c.queries(4, 32)
+    Q = q_tensor(q, "bf16")
+    idx.attach_fullbit(good)
+    whole = check_collab("tiny whole store", idx, oi, k_, q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    n = good.shape[0]
+    cuts = [0, 1, 700, 700, 5000, n - 3, n]
+    idx.attach_fullbit_range(good[:cuts[1]], 0)
+    with pytest.raises(ChimeraError) as e:
+        idx.search_collab(Q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    assert e.value.code == chimera.E_INVAL and "incomplete" in str(e.value)
+    with pytest.raises(ChimeraError) as e:
+        idx.attach_fullbit_range(good[5:9], 5)  # does not follow on
+    assert e.value.code == chimera.E_INVAL
+    for a, b in zip(cuts[1:-1], cuts[2:]):
+        if b == cuts[-2]:
+            bad = good[a:b].copy()
+            bad[17, 3] = np.array([2.0], np.float32).view(np.uint32)[0] >> 16
+            with pytest.raises(ChimeraError) as e:
+                idx.attach_fullbit_range(bad, a)
+            assert e.value.code == chimera.E_INVAL and f"token {a + 17} " in str(e.value)
+        idx.attach_fullbit_range(good[a:b], a)
+    with pytest.raises(ChimeraError):
+        idx.attach_fullbit_range(good[:1], n)  # past the end
+    ranged = idx.search_collab(Q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    for x, y in zip(whole, ranged):
+        assert np.array_equal(x, y)
+    # starting over drops the complete store
+    idx.attach_fullbit_range(good[:10], 0)
+    with pytest.raises(ChimeraError):
+        idx.search_collab(Q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    idx.attach_fullbit_range(good[10:], 10)
+    again = idx.search_collab(Q, w.nprobe, w.ncand, 3 * w.k, 3, w.k)
+    for x, y in zip(whole, again):
+        assert np.array_equal(x, y)
+
+
 def test_collab_query_out_of_range_is_refused():
     """A query component outside [-2, 2] (no query token of L2 norm <= 2 has
     one) is refused with the lowest such query named; a component of exactly
