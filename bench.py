@@ -401,7 +401,7 @@ def main():
     work = {
         "probe": ("mfma", 2.0 * w.nq * w.Tq * w.ncent * 128, BF16_PEAK_TFLOPS, "TFLOP/s"),
         "walk": ("hbm", walk_bytes, HBM_PEAK_GBS, "GB/s"),
-        "select": ("hbm", 8.0 * w.nq * w.ndocs, HBM_PEAK_GBS, "GB/s"),
+        "select": ("hbm", 4.0 * w.nq * w.ndocs, HBM_PEAK_GBS, "GB/s"),  # one read of F'
         "score": ("hbm", float(code_bytes_tok * scored_tokens), HBM_PEAK_GBS, "GB/s"),
         "topk": ("hbm", 8.0 * int(nval.sum()), HBM_PEAK_GBS, "GB/s"),
         "round": ("hbm", 2.0 * 2 * w.nq * w.Tq * 128, HBM_PEAK_GBS, "GB/s"),

@@ -1178,8 +1178,11 @@ __global__ __launch_bounds__(SPLIT_THREADS) void k_sel_write(const int32_t *__re
   }
 }
 
+// Chunks per query of the split select: about 16384 workgroups over the
+// batch (measured at 8.8M: 34 ms per step against 55 ms for 2048), each
+// chunk at least 4096 documents.
 int select_chunks(int64_t nq, int64_t ndocs) {
-  const int64_t by_q = (2048 + nq - 1) / std::max<int64_t>(1, nq);
+  const int64_t by_q = (16384 + nq - 1) / std::max<int64_t>(1, nq);
   const int64_t by_docs = (ndocs + 4095) / 4096;
   return (int)std::max<int64_t>(1, std::min(by_q, by_docs));
 }

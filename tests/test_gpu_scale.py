@@ -11,7 +11,7 @@ import gc
 import os
 import sys
 import time
-from concurrent.futures import ThreadPoolExecutor
+from concurrent.futures import ThreadPoolExecutor, as_completed
 
 import numpy as np
 import pytest
@@ -25,13 +25,24 @@ pytestmark = pytest.mark.gpu
 _SKIP = {s.strip() for s in os.environ.get("CHIMERA_SKIP_BIG", "").split(",") if s.strip()}
 
 
+_capsys = None
+
+
 def say(*a):
-    print("[gpu-big]", *a, flush=True)
+    """A progress line that reaches the terminal as each step ends, past
+    pytest's output capture: these tests run for minutes."""
+    if _capsys is not None:
+        with _capsys.disabled():
+            print("[gpu-big]", *a, flush=True)
+    else:
+        print("[gpu-big]", *a, flush=True)
     sys.stdout.flush()
 
 
 @pytest.mark.parametrize("name", ["1m", "2m-long", "8.8m"])
-def test_full_size_sampled_parity(name):
+def test_full_size_sampled_parity(name, capsys):
+    global _capsys
+    _capsys = capsys
     if name in _SKIP or "all" in _SKIP:
         pytest.skip(f"full-size {name} workload skipped by CHIMERA_SKIP_BIG")
     w = synth.WORKLOADS[name]
@@ -55,7 +66,12 @@ def test_full_size_sampled_parity(name):
     sample = sorted({0, 1, w.nq // 3, w.nq // 2, (2 * w.nq) // 3, w.nq - 1})
     say(f"{name}: oracle on queries {sample}")
     with ThreadPoolExecutor(max_workers=len(sample)) as ex:
-        refs = list(ex.map(lambda qi: oracle_search_one(c, oi, q_k[qi], w.nprobe, w.ncand, w.k), sample))
+        futs = {ex.submit(oracle_search_one, c, oi, q_k[qi], w.nprobe, w.ncand, w.k): qi for qi in sample}
+        got = {}
+        for f in as_completed(futs):
+            got[futs[f]] = f.result()
+            say(f"{name}: oracle query {futs[f]} done ({time.time() - t0:.0f}s)")
+    refs = [got[qi] for qi in sample]
     for qi, ref in zip(sample, refs):
         say(f"{name}: query {qi}")
         assert np.array_equal(ci[qi], ref["cent_ids"]), f"{name} q{qi}: centroid ids differ"

@@ -58,6 +58,7 @@ def build_both(w, nthreads=0, docs_per_chunk=50_000, say=print):
         b.add_docs(bf, cl, c.lengths[d0:d1])
         if d0 % (20 * docs_per_chunk) == 0:
             say(f"pass 2: {d1}/{nd} docs")
+    say("pass 2 done; oracle index")
     oi = oracle.OracleIndex(c.centroids_k, c.doc_off, cid, w.nbits, hist=hist, with_codes=False)
     return c, b, oi
 
