@@ -40,6 +40,7 @@ METRIC = "QPS at fixed recall@k (batch) + p50 latency nq=1; code-scan HBM GB/s"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 STAGES = ["round", "probe", "walk", "select", "score", "topk"]
+RABITQ_SEED = 20260
 KERNEL_OF_STAGE = {"probe": "k_probe", "walk": "k_cand_walk", "select": "k_select", "score": "k_residual_score",
                    "topk": "k_topk", "round": "k_round_queries"}
 SOURCE_OF_STAGE = {"probe": "k_probe.hip", "walk": "k_prune.hip", "select": "k_prune.hip",
@@ -202,11 +203,13 @@ class OracleView:
 
 
 # --------------------------------------------------------------- index build
-def build(w, corpus, threads, ref, view, docs_per_chunk):
+def build(w, corpus, threads, ref, view, docs_per_chunk, rabitq_signs=None):
     """Two passes over the corpus; returns the product builder."""
     import synth
     from paper_2608_23553_amd import Builder
     b = Builder(synth.k_to_bf16_bits(corpus.centroids_k), w.nbits)
+    if rabitq_signs is not None:
+        b.rabitq(rabitq_signs)
     nd = w.ndocs
     t, t_log = time.perf_counter(), time.perf_counter()
     for d0 in range(0, nd, docs_per_chunk):
@@ -273,6 +276,9 @@ def main():
                                                          "(default 4 k)")
     ap.add_argument("--chunks", type=int, default=4, help="chunks of the collaborative scoring")
     ap.add_argument("--no-collab", action="store_true", help="skip the collaborative-scoring measurement")
+    ap.add_argument("--rabitq", action="store_true",
+                    help="also encode RaBitQ codes (B = 4) and measure the 1-bit GPU scoring and the 4-bit host "
+                         "re-rank (the encoder takes about 50 us per token per host thread)")
     ap.add_argument("--no-recall-sweep", action="store_true",
                     help="skip the QPS / recall sweep over larger nprobe and ncand")
     ap.add_argument("--docs-per-chunk", type=int, default=100_000, help="documents per generated chunk")
@@ -334,7 +340,8 @@ def main():
             ref = ExactReference(q_k[:nr], w.ndocs, dev)
             if not args.no_cpu_baseline:
                 view = OracleView(corpus, threads)
-        builder = build(w, corpus, threads, ref, view, args.docs_per_chunk)
+        builder = build(w, corpus, threads, ref, view, args.docs_per_chunk,
+                        rabitq_signs=synth.rotation_signs(RABITQ_SEED) if args.rabitq else None)
         if args.save_index:
             t = time.perf_counter()
             builder.save(args.save_index)
@@ -512,6 +519,43 @@ def main():
         qps_at = {str(t): max((e["qps"] for e in sweep if e.get("recall_at_k", 0) >= t), default=None)
                   for t in (0.8, 0.9, 0.95)}
 
+    # ---- RaBitQ codes (Sec. 2.2, Sec. 3.1): the same candidates scored on
+    # the GPU from the 1-bit codes (no S^T table), then re-ranked on the host
+    # from the 4-bit codes (Alg. 3)
+    rabitq = None
+    if args.rabitq and info.get("rabitq", True):
+        log("RaBitQ: 1-bit GPU scoring")
+        for _ in range(args.warmup):
+            idx.search_rabitq(Q, w.nprobe, w.ncand, w.k, out=(ids, scores))
+        torch.cuda.synchronize()
+        idx.stage_times()
+        s = time.perf_counter()
+        for _ in range(args.steps):
+            idx.search_rabitq(Q, w.nprobe, w.ncand, w.k, out=(ids, scores))
+        torch.cuda.synchronize()
+        el = time.perf_counter() - s
+        rst = idx.stage_times()
+        r_stage = {sname: float(rst[i]) / args.steps for i, sname in enumerate(STAGES)}
+        rq_scan = 20.0 * scored_tokens  # 16 B of sign bits and a 4 B factor per scored token
+        got = ids[:nr].cpu().numpy()
+        rabitq = {"qps": w.nq * args.steps / el, "stages_ms": r_stage,
+                  "recall_at_k": float(np.mean([len(set(got[i]) & set(truth[i])) / w.k for i in range(nr)])),
+                  "score_roofline": {"bound": "hbm", "achieved": rq_scan / (r_stage["score"] / 1e3) / 1e9,
+                                     "unit": "GB/s", "frac": rq_scan / (r_stage["score"] / 1e3) / 1e9 / HBM_PEAK_GBS,
+                                     "bytes_per_token": 20}}
+        log(f"  {rabitq['qps']:.0f} QPS, recall@{w.k} {rabitq['recall_at_k']:.3f}, stages {r_stage}")
+        kfb = args.kfb or 4 * w.k
+        idx.search_collab_rabitq(Q, w.nprobe, w.ncand, kfb, args.chunks, w.k, nthreads=threads)  # warm-up
+        reps, s = 3, time.perf_counter()
+        for _ in range(reps):
+            cids, _, nfull = idx.search_collab_rabitq(Q, w.nprobe, w.ncand, kfb, args.chunks, w.k, nthreads=threads)
+        rabitq["collab"] = {"qps": w.nq * reps / (time.perf_counter() - s), "kfb": kfb, "chunks": args.chunks,
+                            "k_hat_full_bit_mean": float(nfull.mean()),
+                            "recall_at_k": float(np.mean([len(set(cids[i]) & set(truth[i])) / w.k
+                                                          for i in range(nr)]))}
+        log(f"  4-bit host re-rank: {rabitq['collab']['qps']:.0f} QPS, "
+            f"recall@{w.k} {rabitq['collab']['recall_at_k']:.3f}")
+
     # ---- CPU-GPU collaborative scoring (Alg. 3): the GPU path's candidates
     # re-ranked on the host from the full-precision tokens, chunk by chunk.
     # The store is generated and attached in ranges of documents, so the
@@ -577,7 +621,7 @@ def main():
         "stage_rooflines": stage_rooflines,
         "work_per_step": {"posting_entries": entries, "posting_entries_walked": walked, "scored_tokens": scored_tokens,
                           "candidates": int(nval.sum())},
-        "roofline": roofline, "cpu_baseline": cpu, "collab": collab,
+        "roofline": roofline, "cpu_baseline": cpu, "collab": collab, "rabitq": rabitq,
     }
     print(json.dumps(out), flush=True)
 

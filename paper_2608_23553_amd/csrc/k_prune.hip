@@ -431,10 +431,12 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
       }
       if (ndg > 0) {  // uniform
         // dense lists of rank r: each thread applies them to the documents it
-        // owns from their masks, without atomics, once the other lists are
-        // done.  The groups of one rank hold disjoint tokens, so a document's
-        // hits add up to one token mask and one score sum; the groups are
-        // visited in the same order by every lane.
+        // owns from their masks.  The groups of one rank hold disjoint
+        // tokens, so a document's hits add up to one token mask and one
+        // score sum; the groups are visited in the same order by every lane.
+        // They are credited with the same atomics as the rank's other lists,
+        // whose tokens they do not share, so the two need no barrier between
+        // them: only the earlier ranks must be complete.
         MaskT nb[DPT];
         int32_t sall[DPT];
 #pragma unroll
@@ -453,22 +455,9 @@ __global__ __launch_bounds__(WALK_THREADS) void k_cand_walk(
             sall[i] += hit ? gs : 0;
           }
         }
-        __syncthreads();
 #pragma unroll
-        for (int i = 0; i < DPT; ++i) {
-          if (!nb[i]) continue;
-          const int v = threadIdx.x + WALK_THREADS * i;
-          const MaskT cur = smask[v];
-          const MaskT fresh = nb[i] & ~cur;
-          if (!fresh) continue;
-          smask[v] = cur | fresh;
-          int32_t add = sall[i];
-          if (fresh != nb[i]) {
-            add = 0;
-            for (MaskT m = fresh; m; m &= m - 1) add += keys[__builtin_ctzll((unsigned long long)m)];
-          }
-          sfp[v] += add;
-        }
+        for (int i = 0; i < DPT; ++i)
+          if (nb[i]) credit(smask, sfp, threadIdx.x + WALK_THREADS * i, nb[i], sall[i], keys);
       }
       __syncthreads();  // rank r's LDS updates complete before rank r+1's
     }

@@ -78,44 +78,63 @@ __device__ __forceinline__ bf16x8 rq_expand(uint32_t byte) {
   return as_bf16x8(v);
 }
 
-// One wave per kept document (candidate c of query q, lo <= c < min(hi,
-// n_valid[q])).  MFMA 32x32x16: rows are 32 query tokens (A, lane l holds
-// row l % 32), columns 32 document tokens of a tile (B, lane l holds column
+// Maximum over the 32 lanes of each half wave, in lanes 31 and 63 (lanes
+// whose DPP source is off take -inf, the identity of max).
+__device__ __forceinline__ float rq_half_max(float x) {
+  const int ninf = __float_as_int(-INFINITY);
+  int v = __float_as_int(x);
+#define CHIMERA_MX(CTRL, ROWMASK) \
+  v = __float_as_int(fmaxf(__int_as_float(v), __int_as_float(__builtin_amdgcn_update_dpp(ninf, v, CTRL, ROWMASK, 0xF, false))))
+  CHIMERA_MX(0xB1, 0xF);   // quad_perm [1,0,3,2]
+  CHIMERA_MX(0x4E, 0xF);   // quad_perm [2,3,0,1]
+  CHIMERA_MX(0x141, 0xF);  // row_half_mirror
+  CHIMERA_MX(0x140, 0xF);  // row_mirror
+  CHIMERA_MX(0x142, 0xA);  // row_bcast:15 into rows 1, 3
+#undef CHIMERA_MX
+  return __int_as_float(v);
+}
+
+// A wave scores dpw consecutive kept documents (candidates c of query q,
+// lo <= c < min(hi, n_valid[q])), holding the query operand in registers
+// across them.  MFMA 32x32x16: rows are 32 query tokens (A, lane l holds row
+// l % 32), columns 32 document tokens of a tile (B, lane l holds column
 // l % 32); contraction slot (step s, half h, element i) is dimension
 // 64h + 8s + i on both sides, so lane (col, h) reads bytes 8h .. 8h + 7 of its
 // token's 16-byte code.  D register v of lane l is query row
-// 8(v/4) + 4(l/32) + v%4, document token l % 32.
+// 8(v/4) + 4(l/32) + v%4, document token l % 32.  The estimate of row r and
+// token t is g_t (acc - sum(x_r) / 2); its maximum over the document's tokens
+// is taken per lane over the tiles, then across the 32 columns of each half
+// wave.
 template <int NCB>
 __global__ __launch_bounds__(256) void k_rq_score(const uint32_t *__restrict__ Qh, const uint32_t *__restrict__ Ql,
                                                   const float *__restrict__ qsum, const int64_t *__restrict__ doc_off,
                                                   const uint8_t *__restrict__ bits, const float *__restrict__ g1,
                                                   const int32_t *__restrict__ cand_ids,
                                                   const int32_t *__restrict__ n_valid, int ncand, int lo, int hi,
-                                                  int32_t *__restrict__ fhat) {
+                                                  int dpw, int32_t *__restrict__ fhat) {
   constexpr int TQP = 32 * NCB;
   const int lane = threadIdx.x & 63, col = lane & 31, h = lane >> 5;
   const int64_t q = blockIdx.y;
-  const int c = lo + (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
-  if (c >= min(hi, n_valid[q])) return;  // wave-uniform
-  const int32_t doc = cand_ids[q * ncand + c];
-  const int64_t beg = doc_off[doc];
-  const int len = (int)(doc_off[doc + 1] - beg);
-  long long total = 0;
-#pragma unroll 1
-  for (int rb = 0; rb < NCB; ++rb) {
+  const int c0 = lo + ((int)blockIdx.x * 4 + (int)(threadIdx.x >> 6)) * dpw;
+  const int c1 = min(c0 + dpw, min(hi, n_valid[q]));
+  if (c0 >= c1) return;  // wave-uniform
+  bf16x8 ah[8], al[8];
+  float half_sum[16];
+  auto load_block = [&](int rb) {
     const int64_t qrow = q * TQP + rb * 32 + col;
-    bf16x8 ah[8], al[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       ah[s] = as_bf16x8(*(const uint4 *)(Qh + qrow * 64 + 32 * h + 4 * s));
       al[s] = as_bf16x8(*(const uint4 *)(Ql + qrow * 64 + 32 * h + 4 * s));
     }
-    float half_sum[16], mx[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      half_sum[v] = 0.5f * qsum[q * TQP + rb * 32 + 8 * (v >> 2) + 4 * h + (v & 3)];
-      mx[v] = -INFINITY;
-    }
+    for (int v = 0; v < 16; ++v) half_sum[v] = 0.5f * qsum[q * TQP + rb * 32 + 8 * (v >> 2) + 4 * h + (v & 3)];
+  };
+  // the integer key sum of one document over the current block's 32 rows
+  auto score_doc = [&](int64_t beg, int len) -> long long {
+    float mx[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx[v] = -INFINITY;
     for (int t0 = 0; t0 < len; t0 += 32) {
       // tokens past the document read the next ones (the arrays are padded)
       const int64_t tok = beg + t0 + col;
@@ -137,20 +156,41 @@ __global__ __launch_bounds__(256) void k_rq_score(const uint32_t *__restrict__ Q
         if (valid) mx[v] = fmaxf(mx[v], e);
       }
     }
-    // the maximum over the document's tokens: over the 32 columns of a half
+    // each half holds 16 of the block's 32 rows: their maxima land in lanes
+    // 31 and 63
     long long part = 0;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float m = mx[v];
-#pragma unroll
-      for (int k = 1; k < 32; k <<= 1) m = fmaxf(m, __shfl_xor(m, k, 64));
-      part += (long long)rintf(m * KEY_SCALE);
+    for (int v = 0; v < 16; ++v) part += (long long)rintf(rq_half_max(mx[v]) * KEY_SCALE);
+    const int lo32 = __builtin_amdgcn_readlane((int)(uint32_t)part, 31), hi32 = __builtin_amdgcn_readlane((int)(part >> 32), 31);
+    const int lo63 = __builtin_amdgcn_readlane((int)(uint32_t)part, 63), hi63 = __builtin_amdgcn_readlane((int)(part >> 32), 63);
+    return (long long)(((uint64_t)(uint32_t)hi32 << 32) | (uint32_t)lo32) +
+           (long long)(((uint64_t)(uint32_t)hi63 << 32) | (uint32_t)lo63);
+  };
+  auto put = [&](int c, long long total) {
+    if (lane == 0)
+      fhat[q * ncand + c] = (int32_t)std::min<long long>(INT32_MAX, std::max<long long>(-INT32_MAX, total));
+  };
+  if constexpr (NCB == 1) {
+    load_block(0);
+    for (int c = c0; c < c1; ++c) {
+      const int32_t doc = cand_ids[q * ncand + c];
+      const int64_t beg = doc_off[doc];
+      put(c, score_doc(beg, (int)(doc_off[doc + 1] - beg)));
     }
-    // each half holds 16 of the block's 32 rows
-    part += __shfl_xor(part, 32, 64);
-    total += part;
+  } else {
+    for (int c = c0; c < c1; ++c) {
+      const int32_t doc = cand_ids[q * ncand + c];
+      const int64_t beg = doc_off[doc];
+      const int len = (int)(doc_off[doc + 1] - beg);
+      long long total = 0;
+#pragma unroll 1
+      for (int rb = 0; rb < NCB; ++rb) {
+        load_block(rb);
+        total += score_doc(beg, len);
+      }
+      put(c, total);
+    }
   }
-  if (lane == 0) fhat[q * ncand + c] = (int32_t)std::min<long long>(INT32_MAX, std::max<long long>(-INT32_MAX, total));
 }
 
 void launch_rq_prep(const uint16_t *Qs, int64_t rows, const int8_t *signs, uint32_t *Qh, uint32_t *Ql, float *qsum,
@@ -163,13 +203,18 @@ void launch_rq_score(const uint32_t *Qh, const uint32_t *Ql, const float *qsum, 
                      const int64_t *doc_off, const uint8_t *bits, const float *g1, const int32_t *cand_ids,
                      const int32_t *n_valid, int ncand, int lo, int hi, int32_t *fhat, hipStream_t s) {
   if (nq <= 0 || hi <= lo) return;
-  const dim3 grid((unsigned)((hi - lo + 3) / 4), (unsigned)nq);
+  // documents per wave: up to 8 (the query operand is loaded once per wave),
+  // fewer for small batches so that the chip still gets about 2048
+  // workgroups
+  const int span = hi - lo;
+  const int dpw = (int)std::max<int64_t>(1, std::min<int64_t>(8, (int64_t)span * nq / (4 * 2048)));
+  const dim3 grid((unsigned)((span + 4 * dpw - 1) / (4 * dpw)), (unsigned)nq);
   if (TQP == 32)
     hipLaunchKernelGGL((k_rq_score<1>), grid, dim3(256), 0, s, Qh, Ql, qsum, doc_off, bits, g1, cand_ids, n_valid,
-                       ncand, lo, hi, fhat);
+                       ncand, lo, hi, dpw, fhat);
   else
     hipLaunchKernelGGL((k_rq_score<2>), grid, dim3(256), 0, s, Qh, Ql, qsum, doc_off, bits, g1, cand_ids, n_valid,
-                       ncand, lo, hi, fhat);
+                       ncand, lo, hi, dpw, fhat);
 }
 
 }  // namespace chimera

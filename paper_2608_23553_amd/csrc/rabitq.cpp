@@ -39,20 +39,14 @@ void fwht(int64_t *x, int n) {
       }
 }
 
-struct Step {
-  int64_t m, a;  // the coordinate steps up at t = m / a
-  int i;
-};
-
 }  // namespace
 
 void rabitq_encode_rows(const int16_t *k, int64_t n, int dim, const int8_t *signs, uint8_t *bits1, float *g1,
                         uint8_t *codes4, float *g4) {
   constexpr int B = 4, half = 1 << (B - 1);
-  std::vector<int64_t> xp(dim);
-  std::vector<int> lvl(dim), best(dim);
-  std::vector<Step> steps;
-  steps.reserve((size_t)dim * (half - 1));
+  std::vector<int64_t> xp(dim), av(dim);
+  std::vector<int> lvl(dim), best(dim), ord(dim);
+  std::vector<int> seq((size_t)dim * (half - 1));  // the chain's steps, in order
   for (int64_t r = 0; r < n; ++r) {
     const int16_t *x = k + r * dim;
     int64_t k2 = 0;
@@ -63,35 +57,56 @@ void rabitq_encode_rows(const int16_t *k, int64_t n, int dim, const int8_t *sign
     fwht(xp.data(), dim);
     // the chain of codewords: start at |y| = 1/2 everywhere
     int64_t A = 0, N = dim;
-    steps.clear();
+    int nz = 0;
     for (int d = 0; d < dim; ++d) {
-      const int64_t a = xp[d] < 0 ? -xp[d] : xp[d];
-      A += a;
+      av[d] = xp[d] < 0 ? -xp[d] : xp[d];
+      A += av[d];
       lvl[d] = best[d] = 0;
-      if (a)
-        for (int m = 1; m < half; ++m) steps.push_back({m, a, d});
+      if (av[d]) ord[nz++] = d;
     }
     const int64_t a1 = A;  // <xp, 2 y1>, y1 = sign / 2
-    std::sort(steps.begin(), steps.end(), [](const Step &u, const Step &v) {
-      const int64_t l = u.m * v.a, rr = v.m * u.a;
-      return l != rr ? l < rr : u.i < v.i;
-    });
+    // Coordinate d steps from level m-1 to m at t = m / |xp_d| (m = 1 ..
+    // half-1).  For a fixed m those times increase as |xp_d| decreases, so
+    // with the coordinates in descending |xp| the steps form half-1 sorted
+    // lists, merged here in order of t (exact comparisons of m / a as
+    // m a' < m' a).  Steps of equal t are applied together before the
+    // candidate is compared; their order among themselves does not matter.
+    std::sort(ord.begin(), ord.begin() + nz, [&](int u, int v) { return av[u] != av[v] ? av[u] > av[v] : u < v; });
+    int pos[half];
+    for (int m = 1; m < half; ++m) pos[m] = 0;
     int64_t bA = A, bN = N;
-    for (size_t e = 0; e < steps.size();) {
-      const Step &s0 = steps[e];
-      while (e < steps.size() && steps[e].m * s0.a == s0.m * steps[e].a) {
-        const int d = steps[e].i;
-        A += 2 * steps[e].a;
+    int total = nz * (half - 1), done = 0, ebest = 0;
+    // the next step: the list whose head has the smallest t
+    auto next = [&](int &mb) {
+      mb = 0;
+      for (int m = 1; m < half; ++m) {
+        if (pos[m] >= nz) continue;
+        if (!mb || (int64_t)m * av[ord[pos[mb]]] < (int64_t)mb * av[ord[pos[m]]]) mb = m;
+      }
+    };
+    // the applied steps are recorded in seq and the best prefix is replayed
+    // at the end
+    while (done < total) {
+      int m0;
+      next(m0);
+      const int64_t gm = m0, ga = av[ord[pos[m0]]];  // the group's time gm / ga
+      for (;;) {
+        int m;
+        next(m);
+        if (!m || (int64_t)m * ga != gm * av[ord[pos[m]]]) break;
+        const int d = ord[pos[m]++];
+        A += 2 * av[d];
         N += 8 * (int64_t)lvl[d] + 8;
         ++lvl[d];
-        ++e;
+        seq[done++] = d;
       }
       if ((__int128)A * A * bN > (__int128)bA * bA * N) {
         bA = A;
         bN = N;
-        std::copy(lvl.begin(), lvl.end(), best.begin());
+        ebest = done;
       }
     }
+    for (int e = 0; e < ebest; ++e) ++best[seq[e]];
     uint8_t *b1 = bits1 + r * (dim / 8);
     uint8_t *c4 = codes4 + r * (dim / 2);
     std::memset(b1, 0, dim / 8);
