@@ -312,9 +312,51 @@ __attribute__((target("avx2"))) static void to_grid_avx2(const uint16_t *src, in
 static void to_grid_plain(const uint16_t *src, int64_t n, int16_t *dst) { to_grid(src, n, dst); }
 // The widest instruction set the host has, capped by CHIMERA_COLLAB_ISA
 // (plain, avx2 or vnni; read at every search, so tests can run each path).
+// ip[j] = <x_j, z> over the 128 dimensions, for the Tq rows x_j of xq (int32;
+// every product and sum stays below 2^31 for RaBitQ inputs: |x| <= 2^18,
+// |z| <= 15)
+typedef void (*RqDotFn)(const int32_t *xq, int Tq, const int32_t *z, int32_t *ip);
+
+static void rqdot_plain(const int32_t *xq, int Tq, const int32_t *z, int32_t *ip) {
+  for (int j = 0; j < Tq; ++j) {
+    const int32_t *x = xq + (size_t)j * CHIMERA_DIM;
+    int32_t acc = 0;
+    for (int d = 0; d < CHIMERA_DIM; ++d) acc += x[d] * z[d];
+    ip[j] = acc;
+  }
+}
+
+__attribute__((target("avx2"))) static void rqdot_avx2(const int32_t *xq, int Tq, const int32_t *z, int32_t *ip) {
+  __m256i zz[CHIMERA_DIM / 8];
+  for (int i = 0; i < CHIMERA_DIM / 8; ++i) zz[i] = _mm256_loadu_si256((const __m256i *)(z + 8 * i));
+  for (int j = 0; j < Tq; ++j) {
+    const int32_t *x = xq + (size_t)j * CHIMERA_DIM;
+    __m256i acc = _mm256_setzero_si256();
+    for (int i = 0; i < CHIMERA_DIM / 8; ++i)
+      acc = _mm256_add_epi32(acc, _mm256_mullo_epi32(_mm256_loadu_si256((const __m256i *)(x + 8 * i)), zz[i]));
+    __m128i h = _mm_add_epi32(_mm256_castsi256_si128(acc), _mm256_extracti128_si256(acc, 1));
+    h = _mm_add_epi32(h, _mm_shuffle_epi32(h, 0x4E));
+    h = _mm_add_epi32(h, _mm_shuffle_epi32(h, 0xB1));
+    ip[j] = _mm_cvtsi128_si32(h);
+  }
+}
+
+__attribute__((target("avx512f"))) static void rqdot_avx512(const int32_t *xq, int Tq, const int32_t *z, int32_t *ip) {
+  __m512i zz[CHIMERA_DIM / 16];
+  for (int i = 0; i < CHIMERA_DIM / 16; ++i) zz[i] = _mm512_loadu_si512((const void *)(z + 16 * i));
+  for (int j = 0; j < Tq; ++j) {
+    const int32_t *x = xq + (size_t)j * CHIMERA_DIM;
+    __m512i acc = _mm512_setzero_si512();
+    for (int i = 0; i < CHIMERA_DIM / 16; ++i)
+      acc = _mm512_add_epi32(acc, _mm512_mullo_epi32(_mm512_loadu_si512((const void *)(x + 16 * i)), zz[i]));
+    ip[j] = _mm512_reduce_add_epi32(acc);
+  }
+}
+
 struct HostKernels {
   ToGridFn to_grid;
   MaxDotFn maxdot;
+  RqDotFn rqdot;
 };
 static HostKernels pick_kernels() {
   __builtin_cpu_init();
@@ -322,9 +364,9 @@ static HostKernels pick_kernels() {
   const bool vnni = avx2 && __builtin_cpu_supports("avx512vnni") && __builtin_cpu_supports("avx512bw");
   const char *cap = std::getenv("CHIMERA_COLLAB_ISA");
   const int level = !cap ? 2 : !std::strcmp(cap, "plain") ? 0 : !std::strcmp(cap, "avx2") ? 1 : 2;
-  if (vnni && level >= 2) return {to_grid_avx2, maxdot_vnni};
-  if (avx2 && level >= 1) return {to_grid_avx2, maxdot_avx2};
-  return {to_grid_plain, maxdot_plain};
+  if (vnni && level >= 2) return {to_grid_avx2, maxdot_vnni, rqdot_avx512};
+  if (avx2 && level >= 1) return {to_grid_avx2, maxdot_avx2, rqdot_avx2};
+  return {to_grid_plain, maxdot_plain, rqdot_plain};
 }
 
 // F(V) for the document of tokens [t0, t1) of the grid-integer store; an
@@ -343,21 +385,22 @@ static int64_t full_score(const HostKernels &K, const int16_t *qp, int Tq, int T
 // factors g4 [L]) for the rotated query tokens xq [Tq][128] (grid units):
 // sum_j key(max_t g4_t * float(<xq_j, 2y_t> * 2^-12)), 2y = 2 code - 15, key
 // = rint(x * 2^22); <xq_j, 2y_t> is exact in 32 bits for |Q_j| < 2^9.
-static int64_t rq_full_score(const int32_t *xq, int Tq, const uint8_t *codes, const float *g4, int64_t L) {
+static int64_t rq_full_score(const HostKernels &K, const int32_t *xq, int Tq, const uint8_t *codes, const float *g4,
+                             int64_t L) {
   if (L <= 0) return INT64_MIN;
   float best[CHIMERA_MAX_TQ];
   for (int j = 0; j < Tq; ++j) best[j] = -INFINITY;
-  int32_t z[CHIMERA_DIM];
+  alignas(64) int32_t z[CHIMERA_DIM];
+  int32_t ips[CHIMERA_MAX_TQ];
   for (int64_t t = 0; t < L; ++t) {
     for (int i = 0; i < CHIMERA_DIM / 2; ++i) {
       const int c = codes[t * (CHIMERA_DIM / 2) + i];
       z[2 * i] = 2 * (c & 15) - 15;
       z[2 * i + 1] = 2 * (c >> 4) - 15;
     }
+    K.rqdot(xq, Tq, z, ips);
     for (int j = 0; j < Tq; ++j) {
-      const int32_t *x = xq + (size_t)j * CHIMERA_DIM;
-      int32_t ip = 0;
-      for (int d = 0; d < CHIMERA_DIM; ++d) ip += x[d] * z[d];
+      const int32_t ip = ips[j];
       const float e = g4[t] * (float)std::ldexp((double)ip, -12);
       if (e > best[j]) best[j] = e;
     }
@@ -495,7 +538,7 @@ int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64
         C.done[q][u] = 1;
         const int32_t V = cq[u];
         const int64_t F =
-            o.rabitq ? rq_full_score(C.xq.data() + (size_t)q * Tq * dim, Tq, idx->rq_codes.data() + doc_off[V] * 64,
+            o.rabitq ? rq_full_score(K, C.xq.data() + (size_t)q * Tq * dim, Tq, idx->rq_codes.data() + doc_off[V] * 64,
                                      idx->rq_g4.data() + doc_off[V], doc_off[V + 1] - doc_off[V])
                      : full_score(K, C.qk.data() + (size_t)q * TqP * dim, Tq, TqP, tok, doc_off[V], doc_off[V + 1]);
         C.full[q].emplace_back(F, V);

@@ -97,10 +97,13 @@ def test_rabitq_search_needs_rabitq_codes():
     assert e.value.code == chimera.E_UNSUPPORTED
 
 
-@pytest.mark.parametrize("kfb_mult,chunks", [(2, 1), (3, 4)])
-def test_rabitq_collab_search(kfb_mult, chunks):
+@pytest.mark.parametrize("kfb_mult,chunks,isa", [(2, 1, None), (3, 4, None), (3, 4, "avx2"), (2, 3, "plain")])
+def test_rabitq_collab_search(kfb_mult, chunks, isa, monkeypatch):
     """Alg. 3 with the code split: GPU 1-bit scores chunk by chunk, host
-    scores from the 4-bit codes."""
+    scores from the 4-bit codes, with each host instruction set's dot
+    products (capped by CHIMERA_COLLAB_ISA)."""
+    if isa:
+        monkeypatch.setenv("CHIMERA_COLLAB_ISA", isa)
     w, c, k, oi, idx, signs, codes, g1, g4 = _rq_index("tiny", with_g4=True)
     q, src = c.queries(8, w.Tq, query_seed=21)
     say("rabitq collab", kfb_mult, chunks)
