@@ -276,6 +276,9 @@ def main():
                                                          "(default 4 k)")
     ap.add_argument("--chunks", type=int, default=4, help="chunks of the collaborative scoring")
     ap.add_argument("--no-collab", action="store_true", help="skip the collaborative-scoring measurement")
+    ap.add_argument("--delete-frac", type=float, default=0.0,
+                    help="finally delete this seeded fraction of the documents and time searches with the deletion "
+                         "bitmap, the compaction, and searches after it")
     ap.add_argument("--rabitq", action="store_true",
                     help="also encode RaBitQ codes (B = 4) and measure the 1-bit GPU scoring and the 4-bit host "
                          "re-rank (the encoder takes about 50 us per token per host thread)")
@@ -605,6 +608,34 @@ def main():
         log("CPU baseline")
         cpu = view.run(w, q_k, ids.cpu().numpy(), args.cpu_seconds)
 
+    # ---- updates (Sec. 3.3): deletions through the bitmap, then compaction
+    updates = None
+    if args.delete_frac > 0:
+        gone = np.nonzero(np.random.default_rng(5).random(w.ndocs) < args.delete_frac)[0]
+        idx.delete(gone)
+
+        def timed():
+            idx.search(Q, w.nprobe, w.ncand, w.k, out=(ids, scores), refine=rmode)
+            torch.cuda.synchronize()
+            s0 = time.perf_counter()
+            for _ in range(args.steps):
+                idx.search(Q, w.nprobe, w.ncand, w.k, out=(ids, scores), refine=rmode)
+            torch.cuda.synchronize()
+            return w.nq * args.steps / (time.perf_counter() - s0)
+
+        q_del = timed()
+        got = ids.cpu().numpy()
+        assert not np.isin(got[got >= 0], gone).any(), "a deleted document was returned"
+        s0 = time.perf_counter()
+        idx.compact()
+        t_compact = time.perf_counter() - s0
+        q_cmp = timed()
+        idx.stage_times()
+        updates = {"deleted_docs": int(len(gone)), "qps_with_bitmap": q_del, "compact_s": t_compact,
+                   "qps_after_compact": q_cmp, "qps_before": qps}
+        log(f"updates: {len(gone)} documents deleted: {q_del:.0f} QPS with the bitmap, compaction "
+            f"{t_compact:.1f}s, {q_cmp:.0f} QPS after it (before: {qps:.0f})")
+
     out = {
         "metric": METRIC, "value": qps, "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
@@ -621,7 +652,7 @@ def main():
         "stage_rooflines": stage_rooflines,
         "work_per_step": {"posting_entries": entries, "posting_entries_walked": walked, "scored_tokens": scored_tokens,
                           "candidates": int(nval.sum())},
-        "roofline": roofline, "cpu_baseline": cpu, "collab": collab, "rabitq": rabitq,
+        "roofline": roofline, "cpu_baseline": cpu, "collab": collab, "rabitq": rabitq, "updates": updates,
     }
     print(json.dumps(out), flush=True)
 
