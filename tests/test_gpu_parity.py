@@ -291,6 +291,25 @@ def test_zipf_small_hot_lists(refine):
     check_search(idx, oi, q, w.nprobe, 500, 50, "bf16", f"1m recipe, 3000 docs, refine={refine}", refine=refine)
 
 
+def test_many_dense_groups_per_rank():
+    """64 centroids, each in far more than 1/16 of the documents, so all are
+    dense lists: with nprobe 16 a rank's 32 query tokens fall in up to 29
+    dense groups (more than 5 is checked here on the host), all applied from
+    the documents' masks in one rank step; with nprobe 2 and queries whose
+    tokens share centroids, a rank has a few groups of several tokens."""
+    w, c, k, cl, oi, idx = setup("tiny", ndocs=2000, ncent=64)
+    q, _ = c.queries(6, 32, query_seed=17)
+    docs_per_list = np.array([len(np.unique(np.repeat(np.arange(w.ndocs), c.lengths)[cl == e])) for e in range(64)])
+    assert np.all(docs_per_list * 16 > w.ndocs)
+    most = max(len(np.unique(ids[:, r])) for ids in
+               (np.asarray(oracle.probe(oracle.centroid_scores(qq, c.centroids_k), 16)[0]) for qq in q)
+               for r in range(16))
+    assert most > 5, most
+    check_search(idx, oi, q, 16, 400, 20, "bf16", "64 dense centroids, nprobe 16")
+    q2 = np.repeat(q[:, :4], 8, axis=1)  # 4 distinct tokens, each 8 times
+    check_search(idx, oi, q2, 2, 400, 20, "bf16", "64 dense centroids, nprobe 2, shared tokens")
+
+
 # ------------------------------------------------------ degenerate queries
 def test_binding_checks_out_tensors():
     """Caller-supplied outputs are written by the kernels through bare

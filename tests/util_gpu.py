@@ -19,12 +19,14 @@ def say(*a):
 
 
 @functools.lru_cache(maxsize=None)
-def setup(name, ndocs=None, nbits=None):
+def setup(name, ndocs=None, nbits=None, **kw):
     w = synth.WORKLOADS[name]
     if ndocs is not None:
         w = w.scaled(ndocs=ndocs)
     if nbits is not None:
         w = w.scaled(nbits=nbits)
+    if kw:
+        w = w.scaled(**kw)
     c = synth.Corpus(w.corpus_spec())
     k, cl = c.tokens()
     oi = oracle.OracleIndex(c.centroids_k, c.doc_off, cl, w.nbits, tok_k=k)
