@@ -229,7 +229,7 @@ static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int npr
   b += align_up(probe_part_bytes(plan, rows));                 // partial lists
   b += 2 * align_up((size_t)rows * nprobe * 4);                // cent ids / keys
   if (stop >= STOP_FULL && !rq) b += align_up((size_t)nb * (idx->ncent + 1) * TQP * 4);  // S^T + sentinel rows
-  if (rq) b += 2 * align_up((size_t)rows * 128 * 2) + align_up((size_t)rows * 4);  // Qh, Ql, qsum
+  if (rq) b += align_up((size_t)rows * RQ_ROW_BYTES) + align_up((size_t)rows * 4);  // query limbs, qsum
   if (stop >= STOP_CANDIDATES) {
     b += align_up((size_t)nb * idx->ndocs * 4);  // F'
     b += align_up((size_t)nb * 4096 * 4);        // select histogram
@@ -430,14 +430,13 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     launch_select(fp, hist, nb, idx->ndocs, ncand, selw, cand, candk, nval, s);
     CHIMERA_HIP(hipGetLastError());
     if (stop == STOP_PRUNE) continue;
-    // RaBitQ scoring: the rotated queries as bf16 hi and lo parts
+    // RaBitQ scoring: the rotated queries as int8 limbs
     RqQuery rq;
     if (o.rabitq) {
-      rq.Qh = cv.take<uint32_t>((size_t)rows * 64);
-      rq.Ql = cv.take<uint32_t>((size_t)rows * 64);
+      rq.Qi8 = cv.take<uint8_t>((size_t)rows * RQ_ROW_BYTES);
       rq.qsum = cv.take<float>((size_t)rows);
       if (cv.off > scratch_cap) return fail(CHIMERA_E_NOMEM, "internal: scratch plan overflow");
-      launch_rq_prep(Qs, rows, idx->d_rq_signs, rq.Qh, rq.Ql, rq.qsum, s);
+      launch_rq_prep(Qs, rows, idx->d_rq_signs, rq.Qi8, rq.qsum, s);
     }
     if (stop == STOP_COLLAB) {
       rc = collab_subbatch(idx, s, Qs, nb, q0, Tq, TQP, ST, o.rabitq ? &rq : nullptr, cand, nval, ncand, fhat,
@@ -447,7 +446,7 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     }
     stage_mark(idx, s, mark);
     if (o.rabitq) {
-      launch_rq_score(rq.Qh, rq.Ql, rq.qsum, nb, TQP, idx->d_doc_off, idx->d_rq_bits, idx->d_rq_g1, cand, nval,
+      launch_rq_score(rq.Qi8, rq.qsum, nb, TQP, idx->d_doc_off, idx->d_rq_bits, idx->d_rq_g1, cand, nval,
                       ncand, 0, ncand, fhat, s);
     } else {
       launch_residual_score(Qs, nb, Tq, TQP, ST, idx->ncent, idx->d_doc_off, idx->d_cid, idx->d_codes, idx->nbits,

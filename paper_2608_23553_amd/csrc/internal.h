@@ -159,14 +159,15 @@ void launch_residual_score(const uint16_t *Qs, int64_t nq, int Tq, int TQP, cons
                            int ncand, int lo, int hi, int32_t *fhat, hipStream_t s);
 
 // RaBitQ document scoring (k_rabitq.hip).  Query preparation: for each of
-// the rows rounded query rows Qs [rows][128], x = H diag(signs) q as bf16
-// hi and lo parts Qh, Ql [rows][64] (two bf16 per word) and qsum [rows] =
-// sum(x).  Scoring: fhat [nq][ncand] i32 keys of candidates lo .. hi-1 of
-// each query (those below n_valid) from the 1-bit codes bits [ntok][16] and
-// factors g1 [ntok] (both padded by kTokenPad tokens).
-void launch_rq_prep(const uint16_t *Qs, int64_t rows, const int8_t *signs, uint32_t *Qh, uint32_t *Ql, float *qsum,
-                    hipStream_t s);
-void launch_rq_score(const uint32_t *Qh, const uint32_t *Ql, const float *qsum, int64_t nq, int TQP,
+// the rows rounded query rows Qs [rows][128], X = 2048 H diag(signs) q as
+// three int8 limbs Qi8 [rows][RQ_ROW_BYTES] (a, b, c with X = a 2^14 + b 2^7
+// + c, 128 bytes each) and qsum [rows] = sum(x).  Scoring: fhat [nq][ncand]
+// i32 keys of candidates lo .. hi-1 of each query (those below n_valid) from
+// the 1-bit codes bits [ntok][16] and factors g1 [ntok] (both padded by
+// kTokenPad tokens).
+constexpr int RQ_ROW_BYTES = 384;
+void launch_rq_prep(const uint16_t *Qs, int64_t rows, const int8_t *signs, uint8_t *Qi8, float *qsum, hipStream_t s);
+void launch_rq_score(const uint8_t *Qi8, const float *qsum, int64_t nq, int TQP,
                      const int64_t *doc_off, const uint8_t *bits, const float *g1, const int32_t *cand_ids,
                      const int32_t *n_valid, int ncand, int lo, int hi, int32_t *fhat, hipStream_t s);
 
@@ -181,7 +182,7 @@ struct CollabOut {
 };
 // The rotated queries of a sub-batch for RaBitQ scoring (launch_rq_prep).
 struct RqQuery {
-  uint32_t *Qh = nullptr, *Ql = nullptr;
+  uint8_t *Qi8 = nullptr;  // [rows][RQ_ROW_BYTES]
   float *qsum = nullptr;
 };
 int collab_subbatch(chimera_index *idx, hipStream_t s, const uint16_t *Qs, int64_t nb, int64_t q0, int Tq, int TQP,
