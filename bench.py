@@ -587,7 +587,6 @@ def main():
             runs[c] = (w.nq * reps / (time.perf_counter() - s), cids, nfull)
             log(f"  chunks {c}: {runs[c][0]:.0f} QPS, full-precision scores per query "
                 f"mean {nfull.mean():.2f} max {nfull.max()}")
-        idx.attach_fullbit(None)
         qc, cids, nfull = runs[args.chunks]
         collab = {"qps": qc, "qps_one_chunk": runs[1][0], "kfb": kfb, "chunks": args.chunks, "host_threads": threads,
                   "k_hat_full_bit_mean": float(nfull.mean()), "k_hat_full_bit_max": int(nfull.max()),
@@ -597,8 +596,22 @@ def main():
         if sweep is not None:
             sweep.append({"path": "collaborative", "nprobe": w.nprobe, "ncand": w.ncand, "kfb": kfb,
                           "chunks": args.chunks, "qps": qc, "recall_at_k": collab["recall_at_k"]})
+            # a smaller full-precision budget (the paper's backward tuning,
+            # Sec. 3.2): the fastest configuration that holds each target wins
+            if not args.kfb and 2 * w.k < kfb:
+                k2 = 2 * w.k
+                idx.search_collab(Q, w.nprobe, w.ncand, k2, args.chunks, w.k, nthreads=threads)
+                reps, s = 3, time.perf_counter()
+                for _ in range(reps):
+                    cids2, _, _ = idx.search_collab(Q, w.nprobe, w.ncand, k2, args.chunks, w.k, nthreads=threads)
+                q2 = w.nq * reps / (time.perf_counter() - s)
+                r2 = float(np.mean([len(set(cids2[i]) & set(truth[i])) / w.k for i in range(nr)]))
+                sweep.append({"path": "collaborative", "nprobe": w.nprobe, "ncand": w.ncand, "kfb": k2,
+                              "chunks": args.chunks, "qps": q2, "recall_at_k": r2})
+                log(f"  kfb {k2}: {q2:.0f} QPS, recall@{w.k} {r2:.3f}")
             qps_at = {str(t): max((e["qps"] for e in sweep if e.get("recall_at_k", 0) >= t), default=None)
                       for t in (0.8, 0.9, 0.95)}
+        idx.attach_fullbit(None)
     elif not args.no_collab:
         collab = {"skipped": why}
 
