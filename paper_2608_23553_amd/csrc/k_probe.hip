@@ -210,13 +210,16 @@ __global__ __launch_bounds__(256) void k_probe(const uint16_t *__restrict__ Qs, 
     const bool full = t * 32 + 32 <= ncent;  // wave-uniform: only the last tile is partial
     if (WRITE_ST) {
       float *stp = ST + st_base + (int64_t)cbase * TQP;
+      // S^T is read only by the document scorer, after the walk and the
+      // select: streaming (non-temporal) stores keep it out of the way
       if (full) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) stp[(8 * (v >> 2) + (v & 3)) * TQP] = acc[v];
+        for (int v = 0; v < 16; ++v) __builtin_nontemporal_store(acc[v], &stp[(8 * (v >> 2) + (v & 3)) * TQP]);
       } else {
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          if (cbase + 8 * (v >> 2) + (v & 3) < ncent) stp[(8 * (v >> 2) + (v & 3)) * TQP] = acc[v];
+          if (cbase + 8 * (v >> 2) + (v & 3) < ncent)
+            __builtin_nontemporal_store(acc[v], &stp[(8 * (v >> 2) + (v & 3)) * TQP]);
       }
     }
     // wave-uniform; lists of 16 stay on the networks throughout (measured faster)
