@@ -313,8 +313,9 @@ static void to_grid_plain(const uint16_t *src, int64_t n, int16_t *dst) { to_gri
 // The widest instruction set the host has, capped by CHIMERA_COLLAB_ISA
 // (plain, avx2 or vnni; read at every search, so tests can run each path).
 // ip[j] = <x_j, z> over the 128 dimensions, for the Tq rows x_j of xq (int32;
-// every product and sum stays below 2^31 for RaBitQ inputs: |x| <= 2^18,
-// |z| <= 15)
+// every product and sum stays below 2^31 for RaBitQ inputs: the query's
+// grid integers are at most 4096 in magnitude, so |x| <= 128 * 4096 = 2^19,
+// and |z| <= 15, so |ip| < 128 * 2^19 * 15 < 2^31)
 typedef void (*RqDotFn)(const int32_t *xq, int Tq, const int32_t *z, int32_t *ip);
 
 static void rqdot_plain(const int32_t *xq, int Tq, const int32_t *z, int32_t *ip) {
