@@ -180,8 +180,13 @@ class OracleView:
         log(f"CPU baseline: oracle view built in {time.perf_counter() - t:.1f}s")
         regen = synth.Corpus(w.corpus_spec(), nthreads=1)  # one thread per query
 
+        lat = []
+
         def one(qi):
-            return oracle.search_streamed(oi, q_k[qi], w.nprobe, w.ncand, w.k, regen.docs_tokens)
+            t1 = time.perf_counter()
+            r = oracle.search_streamed(oi, q_k[qi], w.nprobe, w.ncand, w.k, regen.docs_tokens)
+            lat.append(time.perf_counter() - t1)
+            return r
 
         done, agree = 0, True
         t0 = time.perf_counter()
@@ -195,7 +200,7 @@ class OracleView:
         t_cpu = time.perf_counter() - t0
         self.pool.shutdown()
         return {"value": done / t_cpu, "unit": "queries/s", "cores": self.threads, "kind": "oracle",
-                "cpu_model": cpu_model(),
+                "cpu_model": cpu_model(), "s_per_query_one_thread": float(np.median(lat)) if lat else None,
                 "sample": f"first {done} of the {w.nq} benchmark queries, whole path (probe, candidates, F', "
                           f"top-ncand, document scores, top-k), {self.threads} threads, one query each, "
                           f"{t_cpu:.1f}s",
