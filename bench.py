@@ -248,12 +248,15 @@ def source_sha(name):
 
 def measured_traffic(stage, workload):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current kernel source; else None."""
+    it was taken on the current kernel and host source; else None."""
     p = os.path.join(ROOT, "profiles", f"traffic_{KERNEL_OF_STAGE[stage]}_{workload}.json")
     if not os.path.exists(p):
         return None
     d = json.load(open(p))
     if d.get("source_sha256_16") != source_sha(SOURCE_OF_STAGE[stage]):
+        return None
+    # the host code sizes the sub-batches, and with them what one launch covers
+    if "host_sha256_16" in d and d["host_sha256_16"] != source_sha("api.cpp"):
         return None
     return d.get("hbm_bytes_per_launch")
 

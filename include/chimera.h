@@ -25,10 +25,11 @@
  *    CHIMERA_E_BUSY.
  *  - Scratch: a search runs its batch in sub-batches of as many queries as
  *    fit a scratch budget of CHIMERA_SCRATCH_MB MiB (environment, read at
- *    each call; default 32768, at least 16), allocated on the index's device
- *    on first need and kept with the index.  At 8.8M documents a query needs
- *    about 70 MB (its S^T table and F' row), so the default takes about 460
- *    queries per sub-batch.
+ *    each call; default 131072, at least 16), allocated on the index's
+ *    device on first need (at most 9/8 of what the batch needs) and kept with
+ *    the index.  At 8.8M documents a query needs about 72 MB (its S^T table
+ *    and F' row), so the default takes about 1,900 queries per sub-batch, and
+ *    a 4096-query batch runs in 3 sub-batches of 1,366 (about 110 GB).
  *  - Value grid G: all vector values are used as bf16 numbers that are
  *    integer multiples of 2^-11.  Inputs are rounded onto G (nearest, ties to
  *    even), which leaves grid values unchanged.  On G every product is an

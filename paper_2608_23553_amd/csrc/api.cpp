@@ -261,9 +261,11 @@ static int ensure_scratch(chimera_index *idx, size_t bytes) {
 
 static size_t scratch_budget() {
   const char *s = std::getenv("CHIMERA_SCRATCH_MB");
-  // larger sub-batches amortise each launch's tail (8.8M: 32 GB holds about
-  // 460 queries, against 120 for 8 GB, and the step is 3% faster)
-  size_t mb = s ? (size_t)std::strtoull(s, nullptr, 10) : 32768;
+  // larger sub-batches amortise each launch's tail: at 8.8M documents a
+  // query needs about 72 MB, and a 4096-query batch takes 6,862 QPS in 9
+  // sub-batches (32 GiB), 6,898 in 5 (64 GiB) and 6,990 in 3 (128 GiB);
+  // the arena is sized to the batch, so small batches take little of it
+  size_t mb = s ? (size_t)std::strtoull(s, nullptr, 10) : 131072;
   if (mb < 16) mb = 16;
   return mb << 20;
 }
