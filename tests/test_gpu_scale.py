@@ -63,7 +63,10 @@ def test_full_size_sampled_parity(name, capsys):
     ci, ck = ci.cpu().numpy(), ck.cpu().numpy()
     cand, ckeys, nval = cand.cpu().numpy(), ckeys.cpu().numpy(), nval.cpu().numpy()
 
-    sample = sorted({0, 1, w.nq // 3, w.nq // 2, (2 * w.nq) // 3, w.nq - 1})
+    # spread over the batch, with the first and last query of each of three
+    # equal sub-batches (the split a 4096-query 8.8M batch runs in)
+    b3 = -(-w.nq // 3)
+    sample = sorted({0, 1, b3 - 1, b3, w.nq // 2, 2 * b3 - 1, 2 * b3, w.nq - 1})
     say(f"{name}: oracle on queries {sample}")
     with ThreadPoolExecutor(max_workers=len(sample)) as ex:
         futs = {ex.submit(oracle_search_one, c, oi, q_k[qi], w.nprobe, w.ncand, w.k): qi for qi in sample}
