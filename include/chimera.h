@@ -29,7 +29,10 @@
  *    device on first need (at most 9/8 of what the batch needs) and kept with
  *    the index.  At 8.8M documents a query needs about 72 MB (its S^T table
  *    and F' row), so the default takes about 1,900 queries per sub-batch, and
- *    a 4096-query batch runs in 3 sub-batches of 1,366 (about 110 GB).
+ *    a 4096-query batch runs in 3 sub-batches of 1,366 (about 110 GB).  If
+ *    the device cannot hold the arena (other allocations on it), the
+ *    sub-batches are halved until it fits; CHIMERA_E_NOMEM only when the
+ *    scratch of a single query does not fit.
  *  - Value grid G: all vector values are used as bf16 numbers that are
  *    integer multiples of 2^-11.  Inputs are rounded onto G (nearest, ties to
  *    even), which leaves grid values unchanged.  On G every product is an

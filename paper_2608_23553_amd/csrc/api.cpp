@@ -240,8 +240,18 @@ static size_t carve_bytes(const chimera_index *idx, int64_t nb, int TQP, int npr
   return b;
 }
 
+// CHIMERA_SCRATCH_DEVICE_MB (environment, for tests): an arena larger than
+// this is refused as if the device were out of memory.
+static size_t scratch_device_cap() {
+  const char *s = std::getenv("CHIMERA_SCRATCH_DEVICE_MB");
+  return s ? (size_t)std::strtoull(s, nullptr, 10) << 20 : SIZE_MAX;
+}
+
 static int ensure_scratch(chimera_index *idx, size_t bytes) {
   if (bytes <= idx->scratch_bytes) return CHIMERA_OK;
+  if (bytes + bytes / 8 > scratch_device_cap())
+    return fail(CHIMERA_E_NOMEM, "scratch allocation of %zu bytes: above CHIMERA_SCRATCH_DEVICE_MB",
+                bytes + bytes / 8);
   if (idx->scratch) {
     CHIMERA_HIP(hipDeviceSynchronize());
     CHIMERA_HIP(hipFree(idx->scratch));
@@ -253,6 +263,7 @@ static int ensure_scratch(chimera_index *idx, size_t bytes) {
   hipError_t e = hipMalloc(&idx->scratch, want);
   if (e != hipSuccess) {
     idx->scratch = nullptr;
+    (void)hipGetLastError();  // reported here; not to be seen again by a later launch check
     return hip_fail(e, "scratch allocation");
   }
   idx->scratch_bytes = want;
@@ -338,6 +349,13 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
                   "fixed scratch's %zu", need, fixed.bytes);
   } else {
     int rc = ensure_scratch(idx, need);
+    // the device cannot hold that much now (other allocations on it): halve
+    // the sub-batches until their scratch fits, down to one query
+    while (rc == CHIMERA_E_NOMEM && B > 1) {
+      B = (B + 1) / 2;
+      need = need_for(B);
+      rc = ensure_scratch(idx, need);
+    }
     if (rc) return rc;
     if (idx->scratch_pending) CHIMERA_HIP(hipStreamWaitEvent(s, idx->scratch_done, 0));
   }

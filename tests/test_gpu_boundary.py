@@ -154,6 +154,30 @@ def test_search_split_into_sub_batches():
     assert np.array_equal(gi, one[0]) and np.array_equal(gs, one[1])
 
 
+def test_sub_batches_shrink_when_the_arena_does_not_fit():
+    """A device that cannot hold the arena (forced from the host: an arena
+    above CHIMERA_SCRATCH_DEVICE_MB is refused as out of memory) halves the
+    sub-batches until it fits, with the one-pass result; a single query that
+    does not fit is E_NOMEM, and the index works again afterwards."""
+    w, c, k, cl, oi, cached = setup("100k")
+    q, _ = c.queries(48, w.Tq, query_seed=29)
+    Q = q_tensor(q, "bf16")
+    one = [t.cpu().numpy() for t in cached.search(Q, w.nprobe, w.ncand, w.k)]
+    idx = product_builder(c, w.nbits).upload(0)  # a fresh index: no arena yet
+    try:
+        with env(CHIMERA_SCRATCH_DEVICE_MB="1"):  # less than one query's ~2.5 MB
+            with pytest.raises(ChimeraError) as e:
+                idx.search(Q, w.nprobe, w.ncand, w.k)
+            assert e.value.code == chimera.E_NOMEM
+        with env(CHIMERA_SCRATCH_DEVICE_MB="8"):  # 48 -> 24 -> 12 -> 6 -> 3 -> 2 queries per pass
+            gi, gs, _ = check_search(idx, oi, q, w.nprobe, w.ncand, w.k, "bf16", "100k, 8 MB device cap")
+        assert np.array_equal(gi, one[0]) and np.array_equal(gs, one[1])
+        ids, scores = idx.search(Q, w.nprobe, w.ncand, w.k)  # no cap: one pass
+        assert np.array_equal(ids.cpu().numpy(), one[0]) and np.array_equal(scores.cpu().numpy(), one[1])
+    finally:
+        idx.close()
+
+
 def test_8_8m_knobs_on_60k_docs():
     """The 8.8M workload's recipe and knobs (262,144 Zipf(1.1) centroids,
     nprobe 16, ncand 16,384, k 100) on its first 60,000 documents."""
