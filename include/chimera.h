@@ -32,7 +32,9 @@
  *    a 4096-query batch runs in 3 sub-batches of 1,366 (about 110 GB).  If
  *    the device cannot hold the arena (other allocations on it), the
  *    sub-batches are halved until it fits; CHIMERA_E_NOMEM only when the
- *    scratch of a single query does not fit.
+ *    scratch of a single query does not fit.  A sub-batch also holds at
+ *    most 2^28 / ncand queries, so that each launch's work-item count fits
+ *    in 32 bits.
  *  - Value grid G: all vector values are used as bf16 numbers that are
  *    integer multiples of 2^-11.  Inputs are rounded onto G (nearest, ties to
  *    even), which leaves grid values unchanged.  On G every product is an

@@ -333,6 +333,10 @@ static int run(chimera_index *idx, const void *Q, int q_dtype, int64_t nq, int T
     else hi = mid - 1;
   }
   int64_t B = lo;
+  // a launch counts its work-items in 32 bits; the scorer runs about 8 per
+  // (query, candidate) (its grid rounds queries up to 8 and candidates up to
+  // 32), so a sub-batch keeps nb * ncand at most 2^28
+  B = std::min<int64_t>(B, std::max<int64_t>(1, ((int64_t)1 << 28) / std::max(1, ncand)));
   // equal sub-batches: the same number of passes, without a short last one
   const int64_t npass = (nq + B - 1) / B;
   B = (nq + npass - 1) / npass;

@@ -178,6 +178,23 @@ def test_sub_batches_shrink_when_the_arena_does_not_fit():
         idx.close()
 
 
+def test_batch_too_large_for_one_scorer_launch():
+    """5,400 queries with every one of 100,000 documents kept would need more
+    than 2^32 work-items in one scorer launch; the batch runs in sub-batches
+    of at most 2^28 (query, candidate) pairs, with each query's result that
+    of a search on its own (and the oracle's)."""
+    w, c, k, cl, oi, idx = setup("100k")
+    nq, ncand = 5400, w.ndocs
+    q, _ = c.queries(nq, w.Tq, query_seed=31)
+    ids, scores = idx.search(q_tensor(q, "bf16"), w.nprobe, ncand, w.k)
+    ids, scores = ids.cpu().numpy(), scores.cpu().numpy()
+    sample = [0, 1799, 1800, 3599, 3600, 5399]  # ends of the 3 equal sub-batches
+    si, ss = idx.search(q_tensor(q[sample], "bf16"), w.nprobe, ncand, w.k)
+    assert np.array_equal(ids[sample], si.cpu().numpy()) and np.array_equal(scores[sample], ss.cpu().numpy())
+    ref = oi.search(q[-1:], w.nprobe, ncand, w.k)
+    assert np.array_equal(ids[-1:], ref["ids"]) and np.array_equal(scores[-1:], ref["scores"])
+
+
 def test_8_8m_knobs_on_60k_docs():
     """The 8.8M workload's recipe and knobs (262,144 Zipf(1.1) centroids,
     nprobe 16, ncand 16,384, k 100) on its first 60,000 documents."""
